@@ -1,0 +1,198 @@
+"""Seeded request streams and bf16 Q/K/V tensors for the workload configurations.
+
+A *source* is a seeded token sequence with its own Q/K/V rows: a document, a
+question, a conversation session, a one-off document.  A request's prompt is
+a concatenation of source segments; the Q/K/V row of prompt position j is the
+row of the source position it came from, so a document prefix always carries
+identical K/V bytes whenever it is seen again (what prefix caching relies on).
+Inputs are synthetic: token ids uniform over the vocabulary, Q/K/V i.i.d.
+N(0, 1) rounded to bf16 (round-to-nearest-even).
+"""
+
+from __future__ import annotations
+
+from dataclasses import dataclass
+
+import numpy as np
+
+from .configs import VOCAB, Config
+
+KIND_DOC, KIND_QUESTION, KIND_SESSION, KIND_ONEOFF = 0, 1, 2, 3
+TAG_TOKENS, TAG_Q, TAG_K, TAG_V = 0, 1, 2, 3
+
+
+def derive_seed(cfg_seed: int, kind: int, index: int, tag: int) -> int:
+    return int(np.random.SeedSequence([cfg_seed, kind, index, tag]).generate_state(1, np.uint64)[0]
+               & np.uint64(0x7FFFFFFFFFFFFFFF))
+
+
+@dataclass(frozen=True)
+class Source:
+    kind: int
+    index: int
+    length: int
+
+
+@dataclass
+class Request:
+    segments: list            # [(Source, start, length)]
+    tokens: np.ndarray        # int32 [n_tokens]
+
+    @property
+    def n_tokens(self) -> int:
+        return int(self.tokens.shape[0])
+
+
+_token_cache: dict = {}
+
+
+def source_tokens(cfg: Config, src: Source) -> np.ndarray:
+    key = (cfg.seed, src.kind, src.index, src.length)
+    t = _token_cache.get(key)
+    if t is None:
+        rng = np.random.default_rng(derive_seed(cfg.seed, src.kind, src.index, TAG_TOKENS))
+        t = rng.integers(0, VOCAB, size=src.length, dtype=np.int64).astype(np.int32)
+        if len(_token_cache) > 4096:
+            _token_cache.clear()
+        _token_cache[key] = t
+    return t
+
+
+def make_request(cfg: Config, segments) -> Request:
+    toks = [source_tokens(cfg, s)[a:a + n] for (s, a, n) in segments]
+    return Request(list(segments), np.concatenate(toks).astype(np.int32))
+
+
+def free_order(seed: int, num_phys: int) -> np.ndarray:
+    """Seeded initial order of the physical blocks (a permutation of the pool)."""
+    return np.random.default_rng(seed).permutation(num_phys).astype(np.int32)
+
+
+def zipf_probs(n: int, s: float) -> np.ndarray:
+    w = np.arange(1, n + 1, dtype=np.float64) ** (-s)
+    return w / w.sum()
+
+
+# ---------------------------------------------------------------------------------------------
+# streams
+# ---------------------------------------------------------------------------------------------
+
+def stream_tiny(cfg: Config):
+    e = cfg.extra
+    doc = Source(KIND_DOC, 0, e["doc_tokens"])
+    q = Source(KIND_QUESTION, 0, e["suffix_tokens"])
+    r0 = make_request(cfg, [(doc, 0, doc.length)])
+    r1 = make_request(cfg, [(doc, 0, doc.length), (q, 0, q.length)])
+    return [r0, r1]
+
+
+def stream_docqa(cfg: Config, n_batches: int | None = None):
+    e = cfg.extra
+    n_batches = e["n_batches"] if n_batches is None else n_batches
+    rng = np.random.default_rng(derive_seed(cfg.seed, KIND_DOC, -1, 99))
+    rank_to_doc = rng.permutation(e["n_docs"])
+    ranks = rng.choice(e["n_docs"], size=n_batches * cfg.max_batch, p=zipf_probs(e["n_docs"], e["zipf_s"]))
+    out = []
+    for i, rk in enumerate(ranks):
+        doc = Source(KIND_DOC, int(rank_to_doc[rk]), e["doc_tokens"])
+        q = Source(KIND_QUESTION, i, e["question_tokens"])
+        out.append(make_request(cfg, [(doc, 0, doc.length), (q, 0, q.length)]))
+    return out
+
+
+def stream_docqa_hit(cfg: Config):
+    """Eight distinct documents (a warm pass, then the same documents with new questions)."""
+    e = cfg.extra
+    warm, hot = [], []
+    for i in range(cfg.max_batch):
+        doc = Source(KIND_DOC, i, e["doc_tokens"])
+        warm.append(make_request(cfg, [(doc, 0, doc.length)]))
+        q = Source(KIND_QUESTION, 100000 + i, e["question_tokens"])
+        hot.append(make_request(cfg, [(doc, 0, doc.length), (q, 0, q.length)]))
+    return warm, hot
+
+
+def stream_longctx(cfg: Config):
+    e = cfg.extra
+    warm, hot = [], []
+    for i in range(e["n_docs"]):
+        doc = Source(KIND_DOC, i, e["doc_tokens"])
+        q = Source(KIND_QUESTION, i, e["suffix_tokens"])
+        warm.append(make_request(cfg, [(doc, 0, doc.length)]))
+        hot.append(make_request(cfg, [(doc, 0, doc.length), (q, 0, q.length)]))
+    return warm, hot
+
+
+def make_stream(cfg: Config, **kw):
+    if cfg.name == "tiny":
+        return stream_tiny(cfg)
+    if cfg.name == "docqa":
+        return stream_docqa(cfg, **kw)
+    if cfg.name == "longctx":
+        return stream_longctx(cfg)
+    raise KeyError(cfg.name)
+
+
+# ---------------------------------------------------------------------------------------------
+# tensors
+# ---------------------------------------------------------------------------------------------
+
+def _randn_bf16(shape, seed: int, device):
+    import torch
+    g = torch.Generator(device=device)
+    g.manual_seed(seed)
+    return torch.randn(shape, generator=g, device=device, dtype=torch.float32).to(torch.bfloat16)
+
+
+class TensorBank:
+    """Per-source Q/K/V rows (bf16) on one device, generated on first use."""
+
+    def __init__(self, cfg: Config, device="cpu", max_sources: int = 1 << 30):
+        self.cfg = cfg
+        self.device = device
+        self.cache: dict = {}
+        self.max_sources = max_sources
+
+    def source(self, src: Source):
+        key = (src.kind, src.index, src.length)
+        t = self.cache.get(key)
+        if t is None:
+            c = self.cfg
+            q = _randn_bf16((src.length, c.num_q_heads, c.head_dim),
+                            derive_seed(c.seed, src.kind, src.index, TAG_Q), self.device)
+            k = _randn_bf16((src.length, c.num_kv_heads, c.head_dim),
+                            derive_seed(c.seed, src.kind, src.index, TAG_K), self.device)
+            v = _randn_bf16((src.length, c.num_kv_heads, c.head_dim),
+                            derive_seed(c.seed, src.kind, src.index, TAG_V), self.device)
+            if len(self.cache) >= self.max_sources:
+                self.cache.pop(next(iter(self.cache)))
+            t = (q, k, v)
+            self.cache[key] = t
+        return t
+
+    def rows(self, req: Request, start: int, end: int):
+        """Q, K, V rows of prompt positions [start, end) of one request."""
+        import torch
+        qs, ks, vs = [], [], []
+        pos = 0
+        for (src, a, n) in req.segments:
+            lo, hi = max(start, pos), min(end, pos + n)
+            if lo < hi:
+                q, k, v = self.source(src)
+                qs.append(q[a + lo - pos: a + hi - pos])
+                ks.append(k[a + lo - pos: a + hi - pos])
+                vs.append(v[a + lo - pos: a + hi - pos])
+            pos += n
+        return torch.cat(qs), torch.cat(ks), torch.cat(vs)
+
+    def batch_suffix(self, reqs, prefix_lens):
+        """Q_new [sum S, Hq, D], K_new / V_new [sum S, Hkv, D] for the computed tokens of a batch."""
+        import torch
+        parts = [self.rows(r, int(p), r.n_tokens) for r, p in zip(reqs, prefix_lens)]
+        return tuple(torch.cat([p[i] for p in parts]).contiguous() for i in range(3))
+
+
+def bits(t) -> np.ndarray:
+    """bf16 torch tensor -> uint16 numpy bit patterns (host copy)."""
+    import torch
+    return t.detach().contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
