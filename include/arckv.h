@@ -1,0 +1,257 @@
+/*
+ * arckv.h -- C ABI of libarckv: prefix-cached paged prefill attention with an
+ * ARC (or LRU) KV-block cache, for AMD Instinct MI355X (gfx950).
+ *
+ * The library covers the path whose work a higher prefix-cache hit rate cuts:
+ * for every request of a batch, the computed (uncached) suffix tokens attend,
+ * through a block table, to the KV blocks the cache kept and, causally, to
+ * themselves; their new K/V are scattered into physical blocks first.  The
+ * host side decides hits and evictions with ARC over chained block hashes.
+ * Paper: "Recency/Frequency Adaptive KV Caching for Large Language Model
+ * Serving" -- Sec. 2 (prefill, prefix caching, paged attention with
+ * fixed-size KV blocks), Sec. 3 and Fig. 2 (ARC evictor: T1/T2/B1/B2 and the
+ * adaptive target p, block-level decisions), Sec. 4 (16-token blocks, batched
+ * offline prefill).
+ *
+ * Conventions
+ *  - Every call returns an int32 status: ARCKV_OK (0) or a negative ARCKV_E*
+ *    code; arckv_last_error() then returns a thread-local message.  No C++
+ *    exception crosses this boundary.
+ *  - Host objects are opaque and owned by the library (create/destroy pairs).
+ *  - Device memory is always owned by the caller.  The library never
+ *    allocates or frees device memory; device pointers are borrowed until the
+ *    work queued on the given stream has completed.
+ *  - Device calls enqueue asynchronously on the caller's HIP stream (passed as
+ *    void*, NULL = the null stream).  Argument checks are synchronous; a launch
+ *    failure returns ARCKV_EDEVICE.  Nothing synchronises implicitly.
+ *  - bf16 values are passed as 16-bit patterns; arrays are row-major, C order.
+ *  - Block size is 16 tokens.  Pool layout version 1 (ARCKV_LAYOUT_V1):
+ *      K pool: [num_blocks][num_kv_heads][16][head_dim]   (token-major block)
+ *      V pool: [num_blocks][num_kv_heads][head_dim][16]   (dim-major block)
+ *    Token j of a request lives in block table[j / 16] at offset j % 16; its
+ *    slot is table[j / 16] * 16 + j % 16.
+ */
+#ifndef ARCKV_H
+#define ARCKV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define ARCKV_BLOCK_TOKENS 16
+#define ARCKV_LAYOUT_V1 1
+
+/* status codes */
+#define ARCKV_OK 0
+#define ARCKV_EINVAL (-1)       /* malformed arguments                                  */
+#define ARCKV_ENOSPC (-2)       /* batch does not fit: capacity, scratch or buffer caps */
+#define ARCKV_EDEVICE (-3)      /* a HIP call failed (message holds the HIP error)      */
+#define ARCKV_ESTATE (-4)       /* call order violated (plan/release)                   */
+#define ARCKV_EUNSUPPORTED (-5) /* head_dim / group size / block size not supported     */
+
+/* policies and reference order */
+#define ARCKV_POLICY_ARC 0
+#define ARCKV_POLICY_LRU 1
+#define ARCKV_REF_TAIL_FIRST 0
+#define ARCKV_REF_HEAD_FIRST 1
+
+/* decision-log case codes (ARC cases I..IV of the published algorithm, plus LRU) */
+#define ARCKV_CASE_I 0          /* hit in T1 or T2 -> MRU of T2                      */
+#define ARCKV_CASE_II 1         /* ghost hit in B1: p grows, REPLACE, -> T2           */
+#define ARCKV_CASE_III 2        /* ghost hit in B2: p shrinks, REPLACE, -> T2         */
+#define ARCKV_CASE_IVA 3        /* new, |T1|+|B1| = c, |T1| < c: drop B1 LRU, REPLACE */
+#define ARCKV_CASE_IVA_T1DEL 4  /* new, |T1| = c: drop the T1 LRU page (no ghost)     */
+#define ARCKV_CASE_IVB 5        /* new, |T1|+|B1| < c (REPLACE once the cache is full) */
+#define ARCKV_CASE_LRU_HIT 6
+#define ARCKV_CASE_LRU_MISS 7
+/* list tags used in the log and in snapshots */
+#define ARCKV_LIST_NONE 0
+#define ARCKV_LIST_T1 1
+#define ARCKV_LIST_T2 2
+#define ARCKV_LIST_B1 3
+#define ARCKV_LIST_B2 4
+
+/* Thread-local message describing the last failing call on this thread. */
+const char* arckv_last_error(void);
+/* Library ABI version (the pool layout version is ARCKV_LAYOUT_V1). */
+int32_t arckv_version(void);
+
+/* ---------------------------------------------------------------------------------------
+ * Block hashing (host).  Block-level identity of cached KV (Sec. 3, last paragraph) under
+ * prefix caching (Sec. 2): h_i = FNV-1a-64(le64(h_{i-1}) || le32 token ids of block i),
+ * h_{-1} = root, for every full 16-token block; a trailing partial block is not hashed.
+ * tokens: n_tokens int32 ids (host).  out: capacity out_cap (host, caller-owned).
+ * *n_full receives n_tokens / 16.  ENOSPC if out_cap < n_tokens / 16; EINVAL on NULL /
+ * negative sizes.
+ * ------------------------------------------------------------------------------------- */
+int32_t arckv_hash_blocks(const int32_t* tokens, int64_t n_tokens, uint64_t root,
+                          uint64_t* out, int64_t out_cap, int64_t* n_full);
+
+/* ---------------------------------------------------------------------------------------
+ * Block cache: ARC(c) or LRU over block identities, with physical placement (host).
+ * ARC per Sec. 3 / Fig. 2 (resident T1 "seen once", T2 "seen again", ghost lists B1/B2,
+ * adaptive target p for |T1|; ghost hits steer p), with the published case rules and
+ * real-valued p in IEEE binary64.  Pages used by the batch in flight are pinned: a victim
+ * is the LRU-most unpinned page of the list the rule selects, else of the other list (it
+ * then goes to the ghost list of the list it left).  A new page takes the physical block
+ * of the page its reference evicted, else the head of a FIFO free list.
+ * ------------------------------------------------------------------------------------- */
+typedef struct arckv_cache arckv_cache;
+
+typedef struct {
+  int32_t policy;                    /* ARCKV_POLICY_ARC or ARCKV_POLICY_LRU             */
+  int32_t ref_order;                 /* ARCKV_REF_TAIL_FIRST (default) or HEAD_FIRST     */
+  int64_t capacity_blocks;           /* c >= 1: cacheable pages                          */
+  int64_t num_phys_blocks;           /* pool size; >= capacity_blocks + scratch_blocks   */
+  int64_t scratch_blocks;            /* blocks for partial last blocks of requests       */
+  const int32_t* initial_free_order; /* permutation of [0, num_phys_blocks) or NULL for  */
+                                     /* ascending; the first num_phys - scratch entries  */
+                                     /* are the page free list, the rest the scratch FIFO */
+} arckv_cache_cfg;
+
+/* Creates a cache (host memory only).  EINVAL on a bad configuration. */
+int32_t arckv_cache_create(const arckv_cache_cfg* cfg, arckv_cache** out);
+int32_t arckv_cache_destroy(arckv_cache* cache);
+
+/* One request of a batch: its chained hashes (n_full = n_tokens / 16) and length. */
+typedef struct {
+  const uint64_t* hashes;
+  int64_t n_full;
+  int64_t n_tokens;
+} arckv_req;
+
+/* Caller-allocated host output arrays of arckv_plan_batch, with their capacities. */
+typedef struct {
+  int32_t* block_tables;   /* [n_reqs][bt_stride]: physical block of every logical block */
+                           /* (full and partial), -1 padded                              */
+  int32_t bt_stride;       /* >= max over requests of ceil(n_tokens / 16)                */
+  int32_t* cu_q;           /* [n_reqs + 1]: prefix sums of computed tokens S             */
+  int32_t* seq_lens;       /* [n_reqs]: prompt length L                                   */
+  int32_t* prefix_lens;    /* [n_reqs]: cached prefix P = 16 k (L - S)                    */
+  int32_t* hit_blocks;     /* [n_reqs]: k, the leading resident blocks reused             */
+  int32_t* slot_mapping;   /* [slot_cap]: slot of every computed token, request order    */
+  int64_t slot_cap;
+  /* filled by the call */
+  int64_t n_slots;         /* sum of S                                                    */
+  int32_t max_q_len;       /* max S                                                       */
+  int32_t max_seq_len;     /* max L                                                       */
+} arckv_plan;
+
+/* Number of consecutive requests (from the start of n_tokens[0..n_avail)) that form the next
+ * batch: at most max_batch, while the sum of full blocks stays <= capacity and partial last
+ * blocks <= scratch.  *n_take = 0 with ENOSPC if the first request alone does not fit. */
+int32_t arckv_next_batch(const int64_t* n_tokens, int32_t n_avail, int32_t max_batch,
+                         int64_t capacity, int64_t scratch, int32_t* n_take);
+
+/* Plans one batch, requests in order (Sec. 2 prefix reuse; Sec. 3 miss handling):
+ *  1. k = leading full blocks resident; if 16 k == L then k -= 1 (one block recomputed);
+ *  2. pin the k prefix pages; 3. reference every full block once, tail first, and pin it;
+ *  4. a partial last block takes a scratch block; 5. fill table row, cu_q, lengths and the
+ *  slots of tokens [P, L).  A later request may hit blocks an earlier one created.
+ * ESTATE if a batch is in flight; ENOSPC if the batch needs more than c full blocks, more
+ * scratch blocks than free, or outputs exceed their capacities (state is then unchanged);
+ * EINVAL on inconsistent requests. */
+int32_t arckv_plan_batch(arckv_cache* cache, const arckv_req* reqs, int32_t n_reqs,
+                         arckv_plan* plan);
+
+/* Ends the batch in flight: unpins its pages, returns its scratch blocks (FIFO tail). */
+int32_t arckv_release_batch(arckv_cache* cache);
+
+typedef struct {
+  int64_t t1, t2, b1, b2;   /* list sizes (LRU policy: t1 = resident pages)          */
+  double p;                 /* ARC adaptive target (0 for LRU)                       */
+  int64_t capacity;
+  int64_t references;       /* policy references issued                              */
+  int64_t requests, prompt_tokens, prefix_hit_tokens, computed_tokens;
+  int64_t case_counts[8];   /* per ARCKV_CASE_*                                      */
+  int64_t free_blocks, scratch_free;
+  int32_t in_flight;
+  int32_t policy;
+} arckv_stats;
+
+int32_t arckv_cache_stats(const arckv_cache* cache, arckv_stats* out);
+
+/* One policy reference, in issue order. */
+typedef struct {
+  uint64_t key;          /* identity referenced                                      */
+  uint64_t evicted;      /* page moved to a ghost list (or evicted, LRU) by it, or 0 */
+  uint64_t dropped;      /* ghost dropped from B1/B2, or T1 page dropped (IV-A), or 0 */
+  double p_after;        /* ARC target after the reference                           */
+  int32_t kase;          /* ARCKV_CASE_*                                             */
+  int32_t evicted_from;  /* ARCKV_LIST_T1 / T2 / NONE                                */
+  int32_t dropped_from;  /* ARCKV_LIST_B1 / B2 / T1 / NONE                           */
+  int32_t phys_block;    /* physical block of the referenced page afterwards         */
+} arckv_event;
+
+/* Routes the decision log into buf (host, caller-owned, cap events); references after the
+ * buffer is full are counted but not stored.  buf = NULL switches the log off. */
+int32_t arckv_cache_set_log(arckv_cache* cache, arckv_event* buf, int64_t cap);
+/* Events issued since the last set_log (may exceed the capacity). */
+int32_t arckv_cache_log_count(const arckv_cache* cache, int64_t* n);
+
+/* Contents of one list (ARCKV_LIST_T1..B2), LRU to MRU: keys and physical blocks (-1 for
+ * ghosts).  *n receives the list size; ENOSPC if it exceeds cap (nothing written). */
+int32_t arckv_cache_snapshot(const arckv_cache* cache, int32_t list, uint64_t* keys,
+                             int32_t* phys, int64_t cap, int64_t* n);
+
+/* ---------------------------------------------------------------------------------------
+ * Device: KV scatter (Sec. 3: the engine processes a miss by regenerating the block).
+ * ------------------------------------------------------------------------------------- */
+
+/* Bytes of one pool (K or V) in layout V1. */
+int64_t arckv_pool_bytes(int64_t num_blocks, int32_t num_kv_heads, int32_t head_dim);
+
+/* pool[slot[t]] <- (k_new[t], v_new[t]) for t < n_tokens, as an exact bit copy.
+ * k_pool, v_pool: device, layout V1, num_blocks blocks.  k_new, v_new: device bf16
+ * [n_tokens][num_kv_heads][head_dim].  slot_mapping: device int32 [n_tokens]; a slot
+ * outside [0, 16 num_blocks) is skipped.  head_dim in {64, 128}.  Enqueued on stream. */
+int32_t arckv_kv_scatter(void* k_pool, void* v_pool, const void* k_new, const void* v_new,
+                         const int32_t* slot_mapping, int64_t n_tokens, int64_t num_blocks,
+                         int32_t num_kv_heads, int32_t head_dim, void* stream);
+
+/* ---------------------------------------------------------------------------------------
+ * Device: prefix-cached paged prefill attention (Sec. 2: prefill runs the uncached part of
+ * the prompt; its queries attend to the reused prefix KV and causally to each other).
+ * For request r with L tokens, P cached, S = L - P computed, query head h, position j in
+ * [P, L):  o = softmax(scale * q . K[0..j]^T) V[0..j], KV head h / (num_q_heads /
+ * num_kv_heads); K/V read through the block table.  bf16 in, fp32 accumulate, bf16 out.
+ * ------------------------------------------------------------------------------------- */
+
+/* Work decomposition (host): one work item is a 256-column query tile (column = token x
+ * query head of one KV group, token-major) of one (request, KV head) over a key range.
+ * Long key ranges are split when the batch has too few tiles to fill num_cus compute units;
+ * split tiles are merged by a log-sum-exp combine pass.
+ * cu_q, seq_lens: HOST copies of the plan's arrays.  work: host int32 buffer of
+ * 8 * work_cap entries (ARCKV_WORK_INTS per item) or NULL to query sizes.
+ * Outputs: *n_work attention items, *n_combine combine items (both stored in work, the
+ * combine items after the attention items), *ws_bytes device workspace needed.
+ * ENOSPC if n_work + n_combine > work_cap (sizes still reported). */
+#define ARCKV_WORK_INTS 8
+int32_t arckv_attention_plan(const int32_t* cu_q, const int32_t* seq_lens, int32_t n_reqs,
+                             int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                             int32_t num_cus, int32_t* work, int64_t work_cap,
+                             int64_t* n_work, int64_t* n_combine, int64_t* ws_bytes);
+
+/* Runs attention for one planned batch.
+ * k_pool, v_pool: device, layout V1 (num_blocks blocks).  q: device bf16
+ * [n_q][num_q_heads][head_dim], rows ordered by cu_q.  out: device bf16, same shape.
+ * block_tables: device int32 [n_reqs][bt_stride]; cu_q: device [n_reqs + 1]; seq_lens:
+ * device [n_reqs] (the same values given to arckv_attention_plan).  work: device copy of
+ * the plan's items.  workspace: device, >= the planned ws_bytes (may be NULL if 0).
+ * Block-table entries outside [0, num_blocks) are read as zero keys/values.
+ * head_dim in {64, 128}; num_q_heads / num_kv_heads in {1, 2, 4, 8}. */
+int32_t arckv_prefill_attention(const void* k_pool, const void* v_pool, const void* q, void* out,
+                                const int32_t* block_tables, int32_t bt_stride,
+                                const int32_t* cu_q, const int32_t* seq_lens, int32_t n_reqs,
+                                int64_t n_q, int64_t num_blocks, const int32_t* work,
+                                int64_t n_work, int64_t n_combine, int32_t num_q_heads,
+                                int32_t num_kv_heads, int32_t head_dim, float scale,
+                                void* workspace, int64_t ws_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* ARCKV_H */

@@ -1,0 +1,250 @@
+"""arckv: prefix-cached paged prefill attention with an ARC KV-block cache on MI355X.
+
+Thin Python binding over libarckv (include/arckv.h).  Every step of the path runs in the
+library: the host cache/planner in C++, scatter and attention in HIP kernels for gfx950.
+This module only converts arguments (numpy arrays and torch device tensors to pointers) and
+raises on error statuses; if the library has not been built it raises -- there is no
+fallback implementation.
+"""
+
+from __future__ import annotations
+
+import ctypes as C
+from dataclasses import dataclass
+
+import numpy as np
+
+from . import _lib
+from ._lib import ArckvError, SYMBOLS, WORK_INTS  # noqa: F401
+
+BLOCK_TOKENS = 16
+LIST_T1, LIST_T2, LIST_B1, LIST_B2 = 1, 2, 3, 4
+
+
+def lib():
+    return _lib.load()
+
+
+def _ptr(a: np.ndarray, ctype):
+    return a.ctypes.data_as(C.POINTER(ctype))
+
+
+# ------------------------------------------------------------------------------------------
+# host: hashing and the block cache
+# ------------------------------------------------------------------------------------------
+
+def hash_blocks(tokens, root: int = 0) -> np.ndarray:
+    """Chained identities (uint64) of the full 16-token blocks of one token sequence."""
+    t = np.ascontiguousarray(tokens, dtype=np.int32)
+    out = np.empty(len(t) // BLOCK_TOKENS, dtype=np.uint64)
+    nf = _lib.i64()
+    _lib.check(lib().arckv_hash_blocks(_ptr(t, _lib.i32), len(t), C.c_uint64(root), _ptr(out, _lib.u64),
+                                       len(out), C.byref(nf)), "arckv_hash_blocks")
+    return out
+
+
+def next_batch(n_tokens, max_batch: int, capacity: int, scratch: int) -> int:
+    a = np.ascontiguousarray(n_tokens, dtype=np.int64)
+    n = _lib.i32()
+    _lib.check(lib().arckv_next_batch(_ptr(a, _lib.i64), len(a), max_batch, capacity, scratch,
+                                      C.byref(n)), "arckv_next_batch")
+    return int(n.value)
+
+
+@dataclass
+class BatchPlan:
+    block_tables: np.ndarray   # int32 [n_reqs, bt_stride], -1 padded
+    cu_q: np.ndarray           # int32 [n_reqs + 1]
+    seq_lens: np.ndarray       # int32 [n_reqs]
+    prefix_lens: np.ndarray    # int32 [n_reqs]
+    hit_blocks: np.ndarray     # int32 [n_reqs]
+    slot_mapping: np.ndarray   # int32 [n_slots]
+    max_q_len: int
+    max_seq_len: int
+
+    @property
+    def n_reqs(self) -> int:
+        return len(self.seq_lens)
+
+
+class BlockCache:
+    """Host ARC (or LRU) cache with physical block placement; plans batches."""
+
+    def __init__(self, policy: str, capacity: int, num_phys: int, scratch: int,
+                 initial_order=None, ref_order: str = "tail_first"):
+        self._order = None if initial_order is None else np.ascontiguousarray(initial_order, dtype=np.int32)
+        cfg = _lib.CacheCfg(_lib.POLICY[policy], _lib.REF_ORDER[ref_order], capacity, num_phys, scratch,
+                            None if self._order is None else _ptr(self._order, _lib.i32))
+        h = C.c_void_p()
+        _lib.check(lib().arckv_cache_create(C.byref(cfg), C.byref(h)), "arckv_cache_create")
+        self._h = h
+        self._log = None
+        self.capacity = capacity
+
+    def close(self):
+        if getattr(self, "_h", None) is not None and self._h.value:
+            lib().arckv_cache_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def plan_batch(self, reqs, bt_stride: int | None = None) -> BatchPlan:
+        """reqs: sequence of (hashes uint64 array, n_tokens)."""
+        n = len(reqs)
+        keep = [np.ascontiguousarray(h, dtype=np.uint64) for h, _ in reqs]
+        arr = (_lib.Req * max(n, 1))()
+        for i, ((_, nt), h) in enumerate(zip(reqs, keep)):
+            arr[i] = _lib.Req(_ptr(h, _lib.u64), len(h), int(nt))
+        lens = [int(nt) for _, nt in reqs]
+        stride = bt_stride or max([(x + BLOCK_TOKENS - 1) // BLOCK_TOKENS for x in lens] + [1])
+        bt = np.empty((n, stride), dtype=np.int32)
+        cu = np.empty(n + 1, dtype=np.int32)
+        sl = np.empty(n, dtype=np.int32)
+        pl = np.empty(n, dtype=np.int32)
+        hb = np.empty(n, dtype=np.int32)
+        cap = max(sum(lens), 1)
+        slots = np.empty(cap, dtype=np.int32)
+        pc = _lib.PlanC(_ptr(bt, _lib.i32), stride, _ptr(cu, _lib.i32), _ptr(sl, _lib.i32), _ptr(pl, _lib.i32),
+                        _ptr(hb, _lib.i32), _ptr(slots, _lib.i32), cap, 0, 0, 0)
+        _lib.check(lib().arckv_plan_batch(self._h, arr, n, C.byref(pc)), "arckv_plan_batch")
+        return BatchPlan(bt, cu, sl, pl, hb, slots[: pc.n_slots].copy(), pc.max_q_len, pc.max_seq_len)
+
+    def release_batch(self):
+        _lib.check(lib().arckv_release_batch(self._h), "arckv_release_batch")
+
+    def stats(self) -> dict:
+        s = _lib.Stats()
+        _lib.check(lib().arckv_cache_stats(self._h, C.byref(s)), "arckv_cache_stats")
+        d = {k: getattr(s, k) for k, _ in _lib.Stats._fields_}
+        d["case_counts"] = list(s.case_counts)
+        return d
+
+    def set_log(self, cap: int):
+        """Start recording up to `cap` policy decisions (0 switches the log off)."""
+        if cap <= 0:
+            self._log = None
+            _lib.check(lib().arckv_cache_set_log(self._h, None, 0), "arckv_cache_set_log")
+            return
+        self._log = (_lib.Event * cap)()
+        _lib.check(lib().arckv_cache_set_log(self._h, self._log, cap), "arckv_cache_set_log")
+
+    def log(self) -> list:
+        """Recorded decisions as tuples (key, case, evicted, evicted_from, dropped, dropped_from,
+        phys, p_after)."""
+        n = _lib.i64()
+        _lib.check(lib().arckv_cache_log_count(self._h, C.byref(n)), "arckv_cache_log_count")
+        if self._log is None:
+            return []
+        m = min(n.value, len(self._log))
+        return [(e.key, e.kase, e.evicted, e.evicted_from, e.dropped, e.dropped_from, e.phys_block,
+                 e.p_after) for e in self._log[:m]]
+
+    def log_count(self) -> int:
+        n = _lib.i64()
+        _lib.check(lib().arckv_cache_log_count(self._h, C.byref(n)), "arckv_cache_log_count")
+        return int(n.value)
+
+    def snapshot(self, which: int):
+        n = _lib.i64()
+        lib().arckv_cache_snapshot(self._h, which, None, None, 0, C.byref(n))
+        keys = np.empty(n.value, dtype=np.uint64)
+        phys = np.empty(n.value, dtype=np.int32)
+        _lib.check(lib().arckv_cache_snapshot(self._h, which, _ptr(keys, _lib.u64), _ptr(phys, _lib.i32),
+                                              n.value, C.byref(n)), "arckv_cache_snapshot")
+        return keys, phys
+
+
+# ------------------------------------------------------------------------------------------
+# device: pool, scatter, attention
+# ------------------------------------------------------------------------------------------
+
+def pool_bytes(num_blocks: int, num_kv_heads: int, head_dim: int) -> int:
+    return int(lib().arckv_pool_bytes(num_blocks, num_kv_heads, head_dim))
+
+
+def _stream(stream):
+    if stream is not None:
+        return stream
+    import torch
+    return torch.cuda.current_stream().cuda_stream
+
+
+def _dev(t, dtype_bits: int | None = None, name: str = "tensor"):
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype_bits is not None and t.element_size() * 8 != dtype_bits:
+        raise ValueError(f"{name} must have {dtype_bits}-bit elements")
+    return C.c_void_p(t.data_ptr())
+
+
+def kv_scatter(k_pool, v_pool, k_new, v_new, slot_mapping, stream=None):
+    """pool[slot[t]] <- (k_new[t], v_new[t]); pools [blocks, Hkv, 16, D] / [blocks, Hkv, D, 16]."""
+    nb, hkv = int(k_pool.shape[0]), int(k_pool.shape[1])
+    d = int(k_new.shape[-1])
+    n = int(k_new.shape[0])
+    if tuple(k_new.shape) != (n, hkv, d) or tuple(v_new.shape) != (n, hkv, d):
+        raise ValueError("k_new / v_new must be [n_tokens, num_kv_heads, head_dim]")
+    if tuple(k_pool.shape) != (nb, hkv, 16, d) or tuple(v_pool.shape) != (nb, hkv, d, 16):
+        raise ValueError("pools must be [blocks, Hkv, 16, D] (K) and [blocks, Hkv, D, 16] (V)")
+    if slot_mapping.numel() != n:
+        raise ValueError("slot_mapping must hold one slot per token")
+    _lib.check(lib().arckv_kv_scatter(_dev(k_pool, 16, "k_pool"), _dev(v_pool, 16, "v_pool"),
+                                      _dev(k_new, 16, "k_new"), _dev(v_new, 16, "v_new"),
+                                      _dev(slot_mapping, 32, "slot_mapping"), int(k_new.shape[0]), nb,
+                                      hkv, d, C.c_void_p(_stream(stream))), "arckv_kv_scatter")
+
+
+@dataclass
+class AttnPlan:
+    work: np.ndarray     # int32 [n_work + n_combine, 8]
+    n_work: int
+    n_combine: int
+    ws_bytes: int
+
+
+def attention_plan(cu_q, seq_lens, num_q_heads: int, num_kv_heads: int, head_dim: int,
+                   num_cus: int = 256) -> AttnPlan:
+    cu = np.ascontiguousarray(cu_q, dtype=np.int32)
+    sl = np.ascontiguousarray(seq_lens, dtype=np.int32)
+    nw, nc, ws = _lib.i64(), _lib.i64(), _lib.i64()
+    L = lib()
+    _lib.check(L.arckv_attention_plan(_ptr(cu, _lib.i32), _ptr(sl, _lib.i32), len(sl), num_q_heads,
+                                      num_kv_heads, head_dim, num_cus, None, 0, C.byref(nw), C.byref(nc),
+                                      C.byref(ws)), "arckv_attention_plan")
+    work = np.zeros((max(nw.value + nc.value, 1), WORK_INTS), dtype=np.int32)
+    _lib.check(L.arckv_attention_plan(_ptr(cu, _lib.i32), _ptr(sl, _lib.i32), len(sl), num_q_heads,
+                                      num_kv_heads, head_dim, num_cus, _ptr(work, _lib.i32), len(work),
+                                      C.byref(nw), C.byref(nc), C.byref(ws)), "arckv_attention_plan")
+    return AttnPlan(work, int(nw.value), int(nc.value), int(ws.value))
+
+
+def prefill_attention(k_pool, v_pool, q, out, block_tables, cu_q, seq_lens, work, n_work: int,
+                      n_combine: int, scale: float, workspace=None, ws_bytes: int = 0, stream=None):
+    """Device tensors: pools (layout V1), q/out [n_q, Hq, D] bf16, block_tables [n, stride] int32,
+    cu_q [n+1], seq_lens [n], work [n_work + n_combine, 8] int32, workspace (bytes >= ws_bytes)."""
+    n_q, hq, d = int(q.shape[0]), int(q.shape[1]), int(q.shape[2])
+    nb, hkv = int(k_pool.shape[0]), int(k_pool.shape[1])
+    n_reqs = int(seq_lens.shape[0])
+    if tuple(out.shape) != (n_q, hq, d):
+        raise ValueError("out must have the shape of q")
+    if tuple(k_pool.shape) != (nb, hkv, 16, d) or tuple(v_pool.shape) != (nb, hkv, d, 16):
+        raise ValueError("pools must be [blocks, Hkv, 16, D] (K) and [blocks, Hkv, D, 16] (V)")
+    if block_tables.dim() != 2 or int(block_tables.shape[0]) != n_reqs or cu_q.numel() != n_reqs + 1:
+        raise ValueError("block_tables must be [n_reqs, stride] and cu_q [n_reqs + 1]")
+    if work.dim() != 2 or int(work.shape[1]) != WORK_INTS or int(work.shape[0]) < n_work + n_combine:
+        raise ValueError("work must be [>= n_work + n_combine, 8]")
+    if ws_bytes and (workspace is None or workspace.numel() * workspace.element_size() < ws_bytes):
+        raise ValueError("workspace smaller than ws_bytes")
+    ws = C.c_void_p(0) if workspace is None else _dev(workspace, None, "workspace")
+    _lib.check(lib().arckv_prefill_attention(
+        _dev(k_pool, 16, "k_pool"), _dev(v_pool, 16, "v_pool"), _dev(q, 16, "q"), _dev(out, 16, "out"),
+        _dev(block_tables, 32, "block_tables"), int(block_tables.shape[1]), _dev(cu_q, 32, "cu_q"),
+        _dev(seq_lens, 32, "seq_lens"), int(seq_lens.shape[0]), n_q, int(k_pool.shape[0]),
+        _dev(work, 32, "work"), n_work, n_combine, hq, hkv, d, float(scale), ws, int(ws_bytes),
+        C.c_void_p(_stream(stream))), "arckv_prefill_attention")

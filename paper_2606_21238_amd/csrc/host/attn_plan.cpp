@@ -1,0 +1,145 @@
+// Work decomposition of prefix-cached prefill attention (host side).
+//
+// A work item covers one query tile of 256 "columns" of one (request, KV head): column
+// c = token * G + g (G query heads share a KV head, token-major), so the K/V tiles a work
+// item streams serve all G heads of its group at once.  The key range of a tile ends at the
+// last visible key of its last column (causal: suffix token i of a request with P cached
+// tokens sees keys 0..P+i).  When a batch has too few tiles to give every compute unit a
+// couple of work items (short suffixes over long cached prefixes), tiles are split along the
+// key range into chunks of >= 256 keys; split tiles write fp32 partials plus a base-2
+// log-sum-exp, merged afterwards by one combine item per tile.
+//
+// Items are ordered longest key range first so the longest ones start first, and the order
+// is interleaved over the 8 XCDs (work-groups are dispatched round-robin over XCDs, each with
+// its own L2): all tiles of one (request, KV head) group land on the same XCD, so the K/V
+// they all stream is fetched into that XCD's L2 once.
+#include <algorithm>
+#include <unordered_map>
+#include <vector>
+
+#include "internal.hpp"
+
+namespace {
+
+constexpr int kCols = 256;    // query columns per work-group
+constexpr int kKeyTile = 64;  // keys per K/V tile (split boundaries are multiples of this)
+constexpr int kXcds = 8;      // MI355X: 8 XCDs; dispatch round-robins work-groups over them
+
+struct Item {
+  int32_t v[ARCKV_WORK_INTS];
+  int64_t cost;
+  int64_t group;
+};
+
+}  // namespace
+
+extern "C" int32_t arckv_attention_plan(const int32_t* cu_q, const int32_t* seq_lens,
+                                        int32_t n_reqs, int32_t num_q_heads, int32_t num_kv_heads,
+                                        int32_t head_dim, int32_t num_cus, int32_t* work,
+                                        int64_t work_cap, int64_t* n_work, int64_t* n_combine,
+                                        int64_t* ws_bytes) {
+  if (n_work == nullptr || n_combine == nullptr || ws_bytes == nullptr || n_reqs < 0 ||
+      (n_reqs > 0 && (cu_q == nullptr || seq_lens == nullptr)) || num_cus < 1 ||
+      num_kv_heads < 1 || num_q_heads < 1)
+    return arckv::fail(ARCKV_EINVAL, "attention_plan: bad arguments");
+  if (num_q_heads % num_kv_heads != 0)
+    return arckv::fail(ARCKV_EINVAL, "attention_plan: num_q_heads %% num_kv_heads != 0");
+  const int G = num_q_heads / num_kv_heads;
+  if (G != 1 && G != 2 && G != 4 && G != 8)
+    return arckv::fail(ARCKV_EUNSUPPORTED, "attention_plan: group size %d not in {1,2,4,8}", G);
+  if (head_dim != 64 && head_dim != 128)
+    return arckv::fail(ARCKV_EUNSUPPORTED, "attention_plan: head_dim %d not in {64,128}", head_dim);
+  if (n_reqs > 0 && cu_q[0] != 0) return arckv::fail(ARCKV_EINVAL, "attention_plan: cu_q[0] != 0");
+
+  struct Tile { int32_t req, kvh, col_start, kv_end; };
+  std::vector<Tile> tiles;
+  int64_t total_keys = 0;
+  for (int32_t r = 0; r < n_reqs; ++r) {
+    const int64_t S = static_cast<int64_t>(cu_q[r + 1]) - cu_q[r];
+    const int64_t L = seq_lens[r];
+    if (S < 0 || L < S) return arckv::fail(ARCKV_EINVAL, "attention_plan: request %d has S=%lld L=%lld", r, (long long)S, (long long)L);
+    const int64_t P = L - S;
+    const int64_t ncols = S * G;
+    for (int64_t cs = 0; cs < ncols; cs += kCols) {
+      const int64_t last = std::min<int64_t>(cs + kCols, ncols) - 1;
+      const int32_t kv_end = static_cast<int32_t>(P + last / G + 1);
+      for (int32_t h = 0; h < num_kv_heads; ++h) {
+        tiles.push_back({r, h, static_cast<int32_t>(cs), kv_end});
+        total_keys += kv_end;
+      }
+    }
+  }
+  const int64_t base = static_cast<int64_t>(tiles.size());
+  const int64_t target = 2 * static_cast<int64_t>(num_cus);
+  int64_t chunk = INT32_MAX;
+  if (base > 0 && base < target) {
+    const int64_t want = (total_keys + target - 1) / target;
+    chunk = std::max<int64_t>(256, (want + kKeyTile - 1) / kKeyTile * kKeyTile);
+  }
+
+  std::vector<Item> items, combines;
+  int64_t slot = 0;
+  for (const Tile& t : tiles) {
+    const int64_t ns = (t.kv_end + chunk - 1) / chunk;
+    const int64_t group = static_cast<int64_t>(t.req) * num_kv_heads + t.kvh;
+    if (ns <= 1) {
+      items.push_back({{t.req, t.kvh, t.col_start, 0, t.kv_end, -1, 0, 0}, t.kv_end, group});
+      continue;
+    }
+    for (int64_t s = 0; s < ns; ++s) {
+      const int32_t a = static_cast<int32_t>(s * chunk);
+      const int32_t b = static_cast<int32_t>(std::min<int64_t>((s + 1) * chunk, t.kv_end));
+      items.push_back({{t.req, t.kvh, t.col_start, a, b, static_cast<int32_t>(slot + s), 0, 0}, b - a, group});
+    }
+    combines.push_back({{t.req, t.kvh, t.col_start, static_cast<int32_t>(slot), static_cast<int32_t>(ns), 0, 0, 0}, 0, group});
+    slot += ns;
+  }
+
+  // XCD-aware order: assign whole groups to XCDs (largest first, to the least-loaded XCD),
+  // then emit position-major so work-group i runs on XCD i % 8; each XCD's list is longest first.
+  std::unordered_map<int64_t, int64_t> cost_of;
+  for (const Item& it : items) cost_of[it.group] += it.cost;
+  std::vector<std::pair<int64_t, int64_t>> groups(cost_of.begin(), cost_of.end());  // (group, cost)
+  std::sort(groups.begin(), groups.end(), [](const auto& a, const auto& b) {
+    return a.second != b.second ? a.second > b.second : a.first < b.first;
+  });
+  std::unordered_map<int64_t, int> xcd_of;
+  int64_t load[kXcds] = {0};
+  for (const auto& g : groups) {
+    int best = 0;
+    for (int x = 1; x < kXcds; ++x) if (load[x] < load[best]) best = x;
+    xcd_of[g.first] = best;
+    load[best] += g.second;
+  }
+  std::vector<std::vector<Item>> per_xcd(kXcds);
+  if (groups.size() >= static_cast<size_t>(kXcds)) {
+    for (const Item& it : items) per_xcd[xcd_of[it.group]].push_back(it);
+  } else {  // fewer groups than XCDs: spread tiles over all XCDs instead
+    for (size_t i = 0; i < items.size(); ++i) per_xcd[i % kXcds].push_back(items[i]);
+  }
+  for (auto& v : per_xcd)
+    std::stable_sort(v.begin(), v.end(), [](const Item& a, const Item& b) { return a.cost > b.cost; });
+  size_t longest = 0;
+  for (auto& v : per_xcd) longest = std::max(longest, v.size());
+  std::vector<Item> ordered;
+  ordered.reserve(longest * kXcds);
+  for (size_t i = 0; i < longest; ++i)
+    for (int x = 0; x < kXcds; ++x) {
+      if (i < per_xcd[x].size()) ordered.push_back(per_xcd[x][i]);
+      else ordered.push_back({{-1, 0, 0, 0, 0, -1, 0, 0}, 0, -1});  // idle slot keeps the XCD phase
+    }
+  // trailing idle slots carry no work; drop them
+  while (!ordered.empty() && ordered.back().v[0] < 0) ordered.pop_back();
+
+  *n_work = static_cast<int64_t>(ordered.size());
+  *n_combine = static_cast<int64_t>(combines.size());
+  *ws_bytes = slot * kCols * (static_cast<int64_t>(head_dim) + 1) * 4;
+  if (work == nullptr) return ARCKV_OK;
+  if (*n_work + *n_combine > work_cap)
+    return arckv::fail(ARCKV_ENOSPC, "attention_plan: %lld items, capacity %lld",
+                       (long long)(*n_work + *n_combine), (long long)work_cap);
+  int32_t* w = work;
+  for (const Item& it : ordered) { std::copy(it.v, it.v + ARCKV_WORK_INTS, w); w += ARCKV_WORK_INTS; }
+  for (const Item& it : combines) { std::copy(it.v, it.v + ARCKV_WORK_INTS, w); w += ARCKV_WORK_INTS; }
+  return ARCKV_OK;
+}

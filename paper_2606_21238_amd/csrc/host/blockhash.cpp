@@ -1,0 +1,46 @@
+// Chained block identities: the key the block cache decides on.
+//
+// Cached KV is identified and evicted per 16-token block (paper, Sec. 3, last paragraph);
+// a block's KV can only be reused when every earlier token is the same (prefix caching,
+// Sec. 2), so its identity chains in the parent's identity:
+//   h_i = FNV-1a-64(le64(h_{i-1}) || le32(tok[16 i]) .. le32(tok[16 i + 15])),  h_{-1} = root.
+// FNV-1a-64: offset basis 0xcbf29ce484222325, prime 0x100000001b3, per byte h ^= b, h *= prime.
+#include <cstring>
+
+#include "internal.hpp"
+
+namespace {
+
+constexpr uint64_t kFnvOffset = 0xcbf29ce484222325ull;
+constexpr uint64_t kFnvPrime = 0x100000001b3ull;
+
+inline uint64_t mix_byte(uint64_t h, uint8_t b) { return (h ^ b) * kFnvPrime; }
+
+inline uint64_t hash_block(uint64_t parent, const int32_t* tok) {
+  uint64_t h = kFnvOffset;
+  for (int i = 0; i < 8; ++i) h = mix_byte(h, static_cast<uint8_t>(parent >> (8 * i)));
+  for (int t = 0; t < ARCKV_BLOCK_TOKENS; ++t) {
+    const uint32_t v = static_cast<uint32_t>(tok[t]);
+    for (int i = 0; i < 4; ++i) h = mix_byte(h, static_cast<uint8_t>(v >> (8 * i)));
+  }
+  return h;
+}
+
+}  // namespace
+
+extern "C" int32_t arckv_hash_blocks(const int32_t* tokens, int64_t n_tokens, uint64_t root,
+                                     uint64_t* out, int64_t out_cap, int64_t* n_full) {
+  if (n_tokens < 0 || n_full == nullptr || (n_tokens > 0 && tokens == nullptr))
+    return arckv::fail(ARCKV_EINVAL, "hash_blocks: bad arguments");
+  const int64_t nf = n_tokens / ARCKV_BLOCK_TOKENS;
+  *n_full = nf;
+  if (nf > out_cap || (nf > 0 && out == nullptr))
+    return arckv::fail(ARCKV_ENOSPC, "hash_blocks: %lld blocks, capacity %lld",
+                       (long long)nf, (long long)out_cap);
+  uint64_t h = root;
+  for (int64_t i = 0; i < nf; ++i) {
+    h = hash_block(h, tokens + i * ARCKV_BLOCK_TOKENS);
+    out[i] = h;
+  }
+  return ARCKV_OK;
+}

@@ -1,0 +1,100 @@
+"""PrefillEngine: the per-batch hot path wired over libarckv.
+
+hash blocks -> plan the batch on the host cache -> copy metadata to the device ->
+scatter the computed tokens' K/V -> prefix-cached prefill attention -> release.
+Every step is a libarckv call; this class owns the device buffers (PyTorch tensors used
+only as device memory) and the host cache handle.
+"""
+
+from __future__ import annotations
+
+from dataclasses import dataclass
+
+import numpy as np
+
+from . import (BlockCache, BatchPlan, attention_plan, hash_blocks, kv_scatter, prefill_attention)
+
+
+@dataclass
+class DeviceBatch:
+    plan: BatchPlan
+    block_tables: object
+    cu_q: object
+    seq_lens: object
+    slot_mapping: object
+    work: object
+    n_work: int
+    n_combine: int
+    ws_bytes: int
+
+
+class PrefillEngine:
+    def __init__(self, num_q_heads: int, num_kv_heads: int, head_dim: int, capacity: int,
+                 num_phys: int, scratch: int, policy: str = "arc", initial_order=None,
+                 ref_order: str = "tail_first", device: str = "cuda", num_cus: int | None = None,
+                 pool_fill: int = -1):
+        import torch
+        self.hq, self.hkv, self.d = num_q_heads, num_kv_heads, head_dim
+        self.scale = head_dim ** -0.5
+        self.device = torch.device(device)
+        self.num_phys = num_phys
+        # pools hold bf16 bit patterns; the fill (0xFFFF, a NaN pattern) marks untouched slots
+        self.k_pool = torch.full((num_phys, num_kv_heads, 16, head_dim), pool_fill, dtype=torch.int16,
+                                 device=self.device)
+        self.v_pool = torch.full((num_phys, num_kv_heads, head_dim, 16), pool_fill, dtype=torch.int16,
+                                 device=self.device)
+        self.cache = BlockCache(policy, capacity, num_phys, scratch, initial_order, ref_order)
+        if num_cus is None:
+            num_cus = torch.cuda.get_device_properties(self.device).multi_processor_count
+        self.num_cus = int(num_cus)
+        self._ws = torch.empty(0, dtype=torch.uint8, device=self.device)
+
+    # ---- host steps ----------------------------------------------------------------------
+    def plan(self, token_lists) -> BatchPlan:
+        reqs = [(hash_blocks(t), len(t)) for t in token_lists]
+        return self.cache.plan_batch(reqs)
+
+    def release(self):
+        self.cache.release_batch()
+
+    def upload(self, plan: BatchPlan, stream=None) -> DeviceBatch:
+        import torch
+        ap = attention_plan(plan.cu_q, plan.seq_lens, self.hq, self.hkv, self.d, self.num_cus)
+        host = np.concatenate([plan.block_tables.ravel(), plan.cu_q, plan.seq_lens, plan.slot_mapping,
+                               ap.work.ravel()]).astype(np.int32)
+        pinned = torch.from_numpy(host).pin_memory()
+        dev = pinned.to(self.device, non_blocking=True)
+        n = plan.n_reqs
+        o = 0
+        bt = dev[o:o + plan.block_tables.size].view(n, plan.block_tables.shape[1]); o += plan.block_tables.size
+        cu = dev[o:o + n + 1]; o += n + 1
+        sl = dev[o:o + n]; o += n
+        sm = dev[o:o + len(plan.slot_mapping)]; o += len(plan.slot_mapping)
+        wk = dev[o:o + ap.work.size].view(-1, 8)
+        if ap.ws_bytes > self._ws.numel():
+            self._ws = torch.empty(ap.ws_bytes, dtype=torch.uint8, device=self.device)
+        return DeviceBatch(plan, bt, cu, sl, sm, wk, ap.n_work, ap.n_combine, ap.ws_bytes)
+
+    # ---- device steps --------------------------------------------------------------------
+    def scatter(self, db: DeviceBatch, k_new, v_new, stream=None):
+        kv_scatter(self.k_pool, self.v_pool, k_new, v_new, db.slot_mapping, stream)
+
+    def attention(self, db: DeviceBatch, q, out, stream=None):
+        prefill_attention(self.k_pool, self.v_pool, q, out, db.block_tables, db.cu_q, db.seq_lens,
+                          db.work, db.n_work, db.n_combine, self.scale,
+                          self._ws if db.ws_bytes else None, db.ws_bytes, stream)
+
+    def step(self, token_lists, qkv_for_plan, stream=None):
+        """One batch: plan, upload, scatter, attend, release.  qkv_for_plan(plan) returns the
+        computed tokens' (q, k_new, v_new) device tensors.  Returns (plan, out)."""
+        import torch
+        plan = self.plan(token_lists)
+        try:
+            db = self.upload(plan, stream)
+            q, k_new, v_new = qkv_for_plan(plan)
+            out = torch.empty_like(q)
+            self.scatter(db, k_new, v_new, stream)
+            self.attention(db, q, out, stream)
+        finally:
+            self.release()
+        return plan, out

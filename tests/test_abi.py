@@ -1,0 +1,53 @@
+"""The C-ABI library loads and exports every entry point include/arckv.h declares (CPU only)."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2606_21238_amd as ak
+from paper_2606_21238_amd import _lib
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "arckv.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(arckv_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_header_declares_the_binding_symbols():
+    decl = declared_functions()
+    assert decl == sorted(_lib.SYMBOLS)
+
+
+def test_library_exports_every_declared_symbol():
+    lib = ctypes.CDLL(_lib.LIB_PATH)
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def test_version_and_pool_bytes():
+    assert ak.lib().arckv_version() == 1
+    assert ak.pool_bytes(10, 8, 128) == 10 * 8 * 16 * 128 * 2
+    assert ak.pool_bytes(-1, 8, 128) == -1
+
+
+def test_device_calls_validate_arguments_without_touching_a_device():
+    L = ak.lib()
+    # unsupported head_dim / group size are refused before any launch
+    assert L.arckv_kv_scatter(None, None, None, None, None, 4, 4, 2, 96, None) == _lib.EUNSUPPORTED
+    assert L.arckv_prefill_attention(None, None, None, None, None, 1, None, None, 1, 1, 1, None, 1, 0,
+                                     12, 4, 128, 0.1, None, 0, None) == _lib.EUNSUPPORTED
+    assert L.arckv_prefill_attention(None, None, None, None, None, 1, None, None, 1, 1, 1, None, 1, 0,
+                                     8, 4, 128, 0.1, None, 0, None) == _lib.EINVAL
+    assert b"NULL" in L.arckv_last_error()
+    # nothing to do is a no-op
+    assert L.arckv_kv_scatter(None, None, None, None, None, 0, 4, 2, 64, None) == _lib.OK
+
+
+def test_missing_library_fails_loudly(tmp_path):
+    with pytest.raises(RuntimeError, match="not built"):
+        _lib.load(str(tmp_path / "nope.so"))

@@ -1,0 +1,286 @@
+"""GPU parity: libarckv's HIP scatter and prefill attention against the CPU oracle.
+
+Every case drives the library through its C ABI (via the ctypes binding) on seeded
+synthetic inputs and checks: pool bytes bit-exact (scatter), block tables / slots equal to
+the oracle planner's, attention within max-abs 1e-2 and mean-abs 1e-3 of the fp64 oracle
+(bf16 inputs, fp32 accumulation, bf16 output).
+"""
+
+from __future__ import annotations
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+pytestmark = pytest.mark.gpu
+
+import paper_2606_21238_amd as ak  # noqa: E402
+from paper_2606_21238_amd.engine import PrefillEngine  # noqa: E402
+from oracle import attention as oatt  # noqa: E402
+from oracle import blockhash as obh  # noqa: E402
+from oracle import kvpool as okv  # noqa: E402
+from oracle.planner import Planner, form_batches  # noqa: E402
+from workloads import get_config  # noqa: E402
+from workloads.streams import TensorBank, free_order, make_stream, stream_docqa_hit  # noqa: E402
+from tests.gpu_helpers import bits, compare, print_case, sample_rows  # noqa: E402
+
+DEV = "cuda"
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    ak.lib()
+
+
+def randn_bf16(shape, seed):
+    g = torch.Generator(device=DEV)
+    g.manual_seed(seed)
+    return torch.randn(shape, generator=g, device=DEV).to(torch.bfloat16)
+
+
+# ------------------------------------------------------------------------------------------
+# scatter
+# ------------------------------------------------------------------------------------------
+
+@pytest.mark.parametrize("d,hkv,n", [(64, 2, 1), (64, 2, 63), (128, 8, 64), (128, 8, 65), (128, 8, 1000),
+                                     (64, 1, 300)])
+def test_scatter_bit_exact(d, hkv, n):
+    print_case(f"scatter d={d} hkv={hkv} n={n}")
+    rng = np.random.default_rng(n * 13 + d)
+    nblk = (n + 15) // 16 + 7
+    slots = rng.permutation(nblk * 16)[:n].astype(np.int32)
+    slots[rng.integers(0, n, max(1, n // 50))] = -1            # padding slots are skipped
+    k_new = randn_bf16((n, hkv, d), 1 + n)
+    v_new = randn_bf16((n, hkv, d), 2 + n)
+    eng_k = torch.full((nblk, hkv, 16, d), -1, dtype=torch.int16, device=DEV)
+    eng_v = torch.full((nblk, hkv, d, 16), -1, dtype=torch.int16, device=DEV)
+    ak.kv_scatter(eng_k, eng_v, k_new, v_new, torch.from_numpy(slots).to(DEV))
+    torch.cuda.synchronize()
+    kp, vp = okv.new_pool(nblk, hkv, d)
+    keep = slots >= 0
+    okv.scatter(kp, vp, bits(k_new)[keep], bits(v_new)[keep], slots[keep])
+    assert np.array_equal(bits(eng_k), kp)
+    assert np.array_equal(bits(eng_v), vp)
+
+
+# ------------------------------------------------------------------------------------------
+# attention on directly built batches (random placement, edge lengths)
+# ------------------------------------------------------------------------------------------
+
+def build_batch(reqs, hq, hkv, d, seed, extra_blocks=5):
+    """reqs: [(L, P)].  Random placement of every request's blocks in one pool; all L tokens'
+    K/V written by the library scatter; returns device tensors and oracle-side copies."""
+    rng = np.random.default_rng(seed)
+    nb = [(L + 15) // 16 for L, _ in reqs]
+    nphys = sum(nb) + extra_blocks
+    perm = rng.permutation(nphys)
+    tables, o = [], 0
+    for n in nb:
+        tables.append(perm[o:o + n].astype(np.int32))
+        o += n
+    stride = max(nb)
+    bt = np.full((len(reqs), stride), -1, dtype=np.int32)
+    for r, t in enumerate(tables):
+        bt[r, : len(t)] = t
+    Ls = [L for L, _ in reqs]
+    Ss = [L - P for L, P in reqs]
+    cu = np.concatenate([[0], np.cumsum(Ss)]).astype(np.int32)
+    k_all = randn_bf16((sum(Ls), hkv, d), seed + 1)
+    v_all = randn_bf16((sum(Ls), hkv, d), seed + 2)
+    q_all = randn_bf16((sum(Ss), hq, d), seed + 3)
+    slots = np.concatenate([tables[r][np.arange(L) // 16] * 16 + np.arange(L) % 16
+                            for r, L in enumerate(Ls)]).astype(np.int32)
+    kp = torch.full((nphys, hkv, 16, d), -1, dtype=torch.int16, device=DEV)
+    vp = torch.full((nphys, hkv, d, 16), -1, dtype=torch.int16, device=DEV)
+    ak.kv_scatter(kp, vp, k_all, v_all, torch.from_numpy(slots).to(DEV))
+    okp, ovp = okv.new_pool(nphys, hkv, d)
+    okv.scatter(okp, ovp, bits(k_all), bits(v_all), slots)
+    return dict(kp=kp, vp=vp, q=q_all, bt=bt, cu=cu, seq=np.array(Ls, dtype=np.int32), tables=tables,
+                okp=okp, ovp=ovp, qbits=bits(q_all))
+
+
+def run_attention(b, hq, hkv, d, num_cus=256, table_override=None, kp=None, vp=None):
+    ap = ak.attention_plan(b["cu"], b["seq"], hq, hkv, d, num_cus)
+    bt = b["bt"] if table_override is None else table_override
+    out = torch.empty_like(b["q"])
+    ws = torch.empty(max(ap.ws_bytes, 1), dtype=torch.uint8, device=DEV)
+    ak.prefill_attention(b["kp"] if kp is None else kp, b["vp"] if vp is None else vp, b["q"], out,
+                         torch.from_numpy(bt).to(DEV), torch.from_numpy(b["cu"]).to(DEV),
+                         torch.from_numpy(b["seq"]).to(DEV), torch.from_numpy(ap.work).to(DEV),
+                         ap.n_work, ap.n_combine, d ** -0.5, ws, ap.ws_bytes)
+    torch.cuda.synchronize()
+    return bits(out), ap
+
+
+def oracle_out(b, hq, hkv, d, rows=None):
+    return oatt.prefill_attention(b["qbits"], b["okp"], b["ovp"], b["tables"], b["cu"], b["seq"],
+                                  d ** -0.5, rows_per_request=rows)
+
+
+SWEEP = [
+    # (reqs [(L, P)], hq, hkv, d)
+    ([(1, 0)], 4, 2, 64),
+    ([(64, 0)], 4, 4, 64),
+    ([(320, 256)], 4, 2, 64),
+    ([(17, 16), (15, 0), (65, 64), (100, 48)], 8, 2, 128),
+    ([(63, 0), (64, 0), (65, 0), (129, 0)], 8, 1, 128),
+    ([(1040, 1024), (300, 16), (77, 0)], 32, 8, 128),
+    ([(2000, 1536)], 16, 2, 64),
+    ([(700, 0), (33, 32), (1, 0)], 8, 8, 128),
+]
+
+
+@pytest.mark.parametrize("num_cus", [256, 100000])   # 100000 forces key-range splits + combine
+@pytest.mark.parametrize("case", range(len(SWEEP)))
+def test_attention_sweep(case, num_cus):
+    reqs, hq, hkv, d = SWEEP[case]
+    print_case(f"attention sweep {reqs} hq={hq} hkv={hkv} d={d} num_cus={num_cus}")
+    b = build_batch(reqs, hq, hkv, d, seed=1000 + case)
+    got, ap = run_attention(b, hq, hkv, d, num_cus)
+    ref = oracle_out(b, hq, hkv, d)
+    compare(got, ref, f"case {case}")
+    if num_cus > 1000 and max(L for L, _ in reqs) > 256:
+        assert ap.n_combine > 0
+
+
+def test_block_table_permutation_bitwise():
+    hq, hkv, d = 16, 4, 128
+    reqs = [(900, 512), (260, 0)]
+    print_case(f"permutation invariance {reqs}")
+    b = build_batch(reqs, hq, hkv, d, seed=77, extra_blocks=40)
+    got1, _ = run_attention(b, hq, hkv, d)
+    # move every block to a new physical place and rewrite the tables
+    nphys = b["kp"].shape[0]
+    perm = torch.from_numpy(np.random.default_rng(5).permutation(nphys)).to(DEV)
+    kp2 = torch.empty_like(b["kp"])
+    vp2 = torch.empty_like(b["vp"])
+    kp2[perm] = b["kp"]
+    vp2[perm] = b["vp"]
+    pm = perm.cpu().numpy()
+    bt2 = np.where(b["bt"] >= 0, pm[np.maximum(b["bt"], 0)], -1).astype(np.int32)
+    got2, _ = run_attention(b, hq, hkv, d, table_override=bt2, kp=kp2, vp=vp2)
+    assert np.array_equal(got1, got2)
+
+
+def test_prefix_cached_equals_full_recompute():
+    # the suffix rows computed with a cached prefix equal the same rows of a full recompute
+    hq, hkv, d = 8, 2, 128
+    L, P = 640, 448
+    print_case("prefix-cached vs recompute")
+    full = build_batch([(L, 0)], hq, hkv, d, seed=91)
+    got_full, _ = run_attention(full, hq, hkv, d, num_cus=1)
+    cached = dict(full)
+    cached["q"] = full["q"][P:].contiguous()
+    cached["qbits"] = full["qbits"][P:]
+    cached["cu"] = np.array([0, L - P], dtype=np.int32)
+    got_cached, _ = run_attention(cached, hq, hkv, d, num_cus=1)
+    assert np.array_equal(got_cached, got_full[P:])
+    compare(got_cached, oracle_out(cached, hq, hkv, d), "cached")
+
+
+# ------------------------------------------------------------------------------------------
+# the workload configurations end to end (planner + scatter + attention)
+# ------------------------------------------------------------------------------------------
+
+class Lockstep:
+    """Library engine and oracle (planner + pool image) over the same request stream."""
+
+    def __init__(self, cfg, device_bank=True):
+        order = free_order(cfg.seed, cfg.num_phys)
+        self.cfg = cfg
+        self.eng = PrefillEngine(cfg.num_q_heads, cfg.num_kv_heads, cfg.head_dim, cfg.capacity,
+                                 cfg.num_phys, cfg.scratch, cfg.policy, order)
+        self.orc = Planner(cfg.policy, cfg.capacity, cfg.num_phys, cfg.scratch, order)
+        self.okp, self.ovp = okv.new_pool(cfg.num_phys, cfg.num_kv_heads, cfg.head_dim)
+        self.bank = TensorBank(cfg, DEV)
+
+    def batch(self, reqs, rows_fn=None, check_pool=True):
+        cfg = self.cfg
+        toks = [r.tokens for r in reqs]
+        oplan = self.orc.plan_batch([(obh.hash_blocks(t), len(t)) for t in toks])
+        plan = self.eng.plan(toks)
+        assert plan.prefix_lens.tolist() == oplan.prefix_lens
+        assert plan.slot_mapping.tolist() == oplan.slot_mapping
+        for r, row in enumerate(oplan.block_tables):
+            assert plan.block_tables[r, : len(row)].tolist() == row
+        db = self.eng.upload(plan)
+        q, kn, vn = self.bank.batch_suffix(reqs, oplan.prefix_lens)
+        out = torch.empty_like(q)
+        self.eng.scatter(db, kn, vn)
+        self.eng.attention(db, q, out)
+        torch.cuda.synchronize()
+        self.eng.release()
+        self.orc.release_batch()
+        okv.scatter(self.okp, self.ovp, bits(kn), bits(vn), oplan.slot_mapping)
+        if check_pool:
+            touched = sorted(okv.touched_blocks(oplan.slot_mapping))
+            assert np.array_equal(bits(self.eng.k_pool[touched]), self.okp[touched])
+            assert np.array_equal(bits(self.eng.v_pool[touched]), self.ovp[touched])
+        rows = None if rows_fn is None else [rows_fn(r, oplan) for r in range(len(reqs))]
+        ref = oatt.prefill_attention(bits(q), self.okp, self.ovp, oplan.block_tables, oplan.cu_q,
+                                     oplan.seq_lens, cfg.scale, rows_per_request=rows)
+        return oplan, bits(out), ref
+
+
+def test_tiny_config():
+    cfg = get_config("tiny")
+    print_case("config tiny")
+    ls = Lockstep(cfg)
+    r0, r1 = make_stream(cfg)
+    _, got0, ref0 = ls.batch([r0])
+    compare(got0, ref0, "tiny warm")
+    plan, got, ref = ls.batch([r1])
+    assert plan.prefix_lens == [256] and plan.cu_q == [0, 64]
+    compare(got, ref, "tiny")
+    # the whole pool image matches, untouched blocks included
+    assert np.array_equal(bits(ls.eng.k_pool), ls.okp)
+    assert np.array_equal(bits(ls.eng.v_pool), ls.ovp)
+
+
+def test_docqa_all_hit_batch():
+    cfg = get_config("docqa")
+    print_case("config docqa 2-hit (8 x (8192 cached + 128))")
+    ls = Lockstep(cfg)
+    warm, hot = stream_docqa_hit(cfg)
+    rng = np.random.default_rng(2)
+    ls.batch(warm, rows_fn=lambda r, p: [0, 63, 64, 4095, 8191])
+    plan, got, ref = ls.batch(hot)
+    assert plan.prefix_lens == [8192] * 8
+    compare(got, ref, "docqa 2-hit")
+
+
+def test_docqa_stream_batches():
+    cfg = get_config("docqa")
+    print_case("config docqa stream, 6 batches, row-sampled")
+    ls = Lockstep(cfg)
+    stream = make_stream(cfg, n_batches=6)
+    rng = np.random.default_rng(3)
+    fn = lambda r, p: sample_rows(p.cu_q[r + 1] - p.cu_q[r], rng, 24)
+    for a, b in form_batches([r.n_tokens for r in stream], cfg.max_batch, cfg.capacity, cfg.scratch):
+        _, got, ref = ls.batch(stream[a:b], rows_fn=fn)
+        compare(got, ref, f"docqa batch {a}")
+
+
+def test_longctx_sampled_rows():
+    cfg = get_config("longctx")
+    print_case("config longctx (4 x (32768 cached + 2048)), row-sampled")
+    ls = Lockstep(cfg)
+    warm, hot = make_stream(cfg)
+    rng = np.random.default_rng(4)
+    ls.batch(warm, rows_fn=lambda r, p: [0, 32767], check_pool=True)
+    plan, got, ref = ls.batch(hot, rows_fn=lambda r, p: sample_rows(2048, rng, 16))
+    assert plan.prefix_lens == [32768] * 4
+    compare(got, ref, "longctx")
+
+
+def test_empty_work_is_a_noop():
+    b = build_batch([(32, 0)], 4, 2, 64, seed=3)
+    out = torch.zeros_like(b["q"])
+    ak.prefill_attention(b["kp"], b["vp"], b["q"], out, torch.from_numpy(b["bt"]).to(DEV),
+                         torch.from_numpy(b["cu"]).to(DEV), torch.from_numpy(b["seq"]).to(DEV),
+                         torch.zeros((1, 8), dtype=torch.int32, device=DEV), 0, 0, 0.125)
+    torch.cuda.synchronize()
+    assert int(out.abs().sum()) == 0

@@ -1,0 +1,236 @@
+"""Native host side (hash, ARC/LRU cache, planner) against the oracle, bit-exact (CPU only).
+
+Both sides take the same seeded inputs (token streams from ``workloads``); the library
+hashes with its own C++ hasher, the oracle with its own Python one.  Compared: hashes,
+block tables, cu_q, lengths, hit blocks, slot mappings, every policy decision (case,
+evicted / dropped identities and lists, physical block, p), final list contents and p.
+"""
+
+import numpy as np
+import pytest
+
+import paper_2606_21238_amd as ak
+from oracle import blockhash as obh
+from oracle.planner import Planner, PlanError, form_batches
+from workloads import get_config
+from workloads.streams import (Source, make_request, free_order, make_stream, stream_docqa_hit,
+                               KIND_DOC, KIND_QUESTION)
+
+
+def test_hash_matches_oracle():
+    rng = np.random.default_rng(11)
+    seqs = [rng.integers(0, 128256, n).astype(np.int32) for n in (0, 1, 15, 16, 17, 160, 1000)]
+    for s in seqs:
+        assert [int(x) for x in ak.hash_blocks(s)] == obh.hash_blocks(s)
+        assert [int(x) for x in ak.hash_blocks(s, root=12345)] == obh.hash_blocks(s, root=12345)
+    neg = np.array([-1, -(2 ** 31)] + [7] * 14, dtype=np.int32)
+    assert [int(x) for x in ak.hash_blocks(neg)] == obh.hash_blocks(neg)
+
+
+class Pair:
+    """Library cache and oracle planner driven in lockstep."""
+
+    def __init__(self, policy, c, nphys, scratch, order=None, ref_order="tail_first"):
+        self.lib = ak.BlockCache(policy, c, nphys, scratch, order, ref_order)
+        self.lib.set_log(1 << 20)
+        self.orc = Planner(policy, c, nphys, scratch, order, ref_order)
+        self.n_events = 0
+
+    def run(self, token_lists):
+        lib_reqs = [(ak.hash_blocks(t), len(t)) for t in token_lists]
+        orc_reqs = [(obh.hash_blocks(t), len(t)) for t in token_lists]
+        p = self.lib.plan_batch(lib_reqs)
+        q = self.orc.plan_batch(orc_reqs)
+        n = len(token_lists)
+        assert p.hit_blocks.tolist() == q.hit_blocks
+        assert p.prefix_lens.tolist() == q.prefix_lens
+        assert p.seq_lens.tolist() == q.seq_lens
+        assert p.cu_q.tolist() == q.cu_q
+        assert p.slot_mapping.tolist() == q.slot_mapping
+        for r in range(n):
+            row = q.block_tables[r]
+            assert p.block_tables[r, : len(row)].tolist() == row
+            assert (p.block_tables[r, len(row):] == -1).all()
+        self.lib.release_batch()
+        self.orc.release_batch()
+        return p, q
+
+    def check_log_and_state(self):
+        got = self.lib.log()
+        want = self.orc.cache.log
+        assert len(got) == len(want)
+        for g, e in zip(got, want):
+            assert g == (e.key, e.case, e.evicted, e.evicted_from, e.dropped, e.dropped_from, e.phys,
+                         e.p_after), (g, e)
+        snap = self.orc.cache.snapshot()
+        for li, keys in zip((ak.LIST_T1, ak.LIST_T2, ak.LIST_B1, ak.LIST_B2), snap[:4]):
+            k, ph = self.lib.snapshot(li)
+            assert [int(x) for x in k] == list(keys)
+        st = self.lib.stats()
+        assert st["p"] == snap[4]
+        t = self.orc.totals
+        assert (st["requests"], st["prompt_tokens"], st["prefix_hit_tokens"], st["computed_tokens"]) == \
+            (t.requests, t.prompt_tokens, t.prefix_hit_tokens, t.computed_tokens)
+        assert st["case_counts"] == t.case_counts
+
+
+@pytest.mark.parametrize("policy", ["arc", "lru"])
+@pytest.mark.parametrize("ref_order", ["tail_first", "head_first"])
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_random_streams_bit_exact(policy, ref_order, seed):
+    cfg = get_config("tiny")
+    rng = np.random.default_rng(100 + seed)
+    c, scratch = int(rng.integers(8, 40)), 8
+    nphys = c + scratch + int(rng.integers(0, 5))
+    pair = Pair(policy, c, nphys, scratch, rng.permutation(nphys), ref_order)
+    docs = [make_request(cfg, [(Source(KIND_DOC, d, 200), 0, 200)]).tokens for d in range(12)]
+    pops = 1.0 / np.arange(1, 13) ** 1.1
+    pops /= pops.sum()
+    for step in range(120):
+        nreq = int(rng.integers(1, 4))
+        toks = []
+        for _ in range(nreq):
+            d = int(rng.choice(12, p=pops))
+            n = int(rng.integers(1, 200))
+            extra = rng.integers(0, 128256, int(rng.integers(0, 40))).astype(np.int32)
+            toks.append(np.concatenate([docs[d][:n], extra]))
+        if sum(len(t) // 16 for t in toks) > c or sum(1 for t in toks if len(t) % 16) > scratch:
+            continue
+        pair.run(toks)
+    pair.check_log_and_state()
+    assert pair.orc.totals.prefix_hit_tokens > 0
+
+
+def test_tiny_config_host_phase():
+    cfg = get_config("tiny")
+    order = free_order(cfg.seed, cfg.num_phys)
+    pair = Pair("arc", cfg.capacity, cfg.num_phys, cfg.scratch, order)
+    r0, r1 = make_stream(cfg)
+    pair.run([r0.tokens])
+    p, _ = pair.run([r1.tokens])
+    assert p.hit_blocks.tolist() == [16] and p.cu_q.tolist() == [0, 64]
+    pair.check_log_and_state()
+
+
+def test_docqa_stream_host_phase_and_batching():
+    cfg = get_config("docqa")
+    order = free_order(cfg.seed, cfg.num_phys)
+    stream = make_stream(cfg, n_batches=24)
+    lens = [r.n_tokens for r in stream]
+    batches = form_batches(lens, cfg.max_batch, cfg.capacity, cfg.scratch)
+    # the library's batch formation agrees with the oracle's
+    i, lib_batches = 0, []
+    while i < len(lens):
+        n = ak.next_batch(lens[i:], cfg.max_batch, cfg.capacity, cfg.scratch)
+        lib_batches.append((i, i + n))
+        i += n
+    assert lib_batches == batches
+    pair = Pair("arc", cfg.capacity, cfg.num_phys, cfg.scratch, order)
+    hits = 0
+    for a, b in batches:
+        p, _ = pair.run([r.tokens for r in stream[a:b]])
+        hits += int(p.prefix_lens.sum())
+    pair.check_log_and_state()
+    assert hits > 0
+    warm, hot = stream_docqa_hit(cfg)
+    pair2 = Pair("arc", cfg.capacity, cfg.num_phys, cfg.scratch, order)
+    pair2.run([r.tokens for r in warm])
+    p, _ = pair2.run([r.tokens for r in hot])
+    assert p.prefix_lens.tolist() == [8192] * 8 and p.cu_q[-1] == 8 * 128
+    pair2.check_log_and_state()
+
+
+def test_longctx_host_phase():
+    cfg = get_config("longctx")
+    order = free_order(cfg.seed, cfg.num_phys)
+    warm, hot = make_stream(cfg)
+    pair = Pair("arc", cfg.capacity, cfg.num_phys, cfg.scratch, order)
+    pair.run([r.tokens for r in warm])
+    p, _ = pair.run([r.tokens for r in hot])
+    assert p.prefix_lens.tolist() == [32768] * 4 and p.cu_q.tolist() == [0, 2048, 4096, 6144, 8192]
+    pair.check_log_and_state()
+
+
+def test_error_statuses_match_the_oracle():
+    cfg = get_config("tiny")
+    lib = ak.BlockCache("arc", 8, 16, 4)
+    orc = Planner("arc", 8, 16, 4)
+    big = make_request(cfg, [(Source(KIND_DOC, 1, 144), 0, 144)]).tokens
+    with pytest.raises(ak.ArckvError) as e1:
+        lib.plan_batch([(ak.hash_blocks(big), len(big))])
+    with pytest.raises(PlanError) as e2:
+        orc.plan_batch([(obh.hash_blocks(big), len(big))])
+    assert e1.value.code == e2.value.code == "ENOSPC"
+    with pytest.raises(ak.ArckvError) as e1:
+        lib.release_batch()
+    assert e1.value.code == "ESTATE"
+    small = big[:40]
+    with pytest.raises(ak.ArckvError) as e1:
+        lib.plan_batch([(ak.hash_blocks(small)[:1], len(small))])
+    assert e1.value.code == "EINVAL"
+    lib.plan_batch([(ak.hash_blocks(small), len(small))])
+    with pytest.raises(ak.ArckvError) as e1:
+        lib.plan_batch([(ak.hash_blocks(small), len(small))])
+    assert e1.value.code == "ESTATE"
+    lib.release_batch()
+    assert lib.stats()["in_flight"] == 0
+    with pytest.raises(ak.ArckvError):
+        ak.BlockCache("arc", 10, 12, 4)              # pool too small for c + scratch
+    with pytest.raises(ak.ArckvError):
+        ak.BlockCache("arc", 4, 8, 2, initial_order=[0, 1, 2, 3, 4, 5, 6, 6])
+
+
+def attention_plan_coverage(cu_q, seq_lens, hq, hkv, d, num_cus):
+    ap = ak.attention_plan(cu_q, seq_lens, hq, hkv, d, num_cus)
+    g = hq // hkv
+    items = ap.work[: ap.n_work]
+    comb = ap.work[ap.n_work: ap.n_work + ap.n_combine]
+    cover = {}
+    for it in items:
+        req, kvh, cs, a, b, slot = (int(x) for x in it[:6])
+        if req < 0:
+            continue
+        assert a % 64 == 0 and b > a
+        cover.setdefault((req, kvh, cs), []).append((a, b, slot))
+    for r in range(len(seq_lens)):
+        S = cu_q[r + 1] - cu_q[r]
+        P = seq_lens[r] - S
+        for cs in range(0, S * g, 256):
+            last = min(cs + 256, S * g) - 1
+            kv_end = P + last // g + 1
+            for h in range(hkv):
+                ranges = sorted(cover.pop((r, h, cs)))
+                assert ranges[0][0] == 0 and ranges[-1][1] == kv_end
+                assert all(x[1] == y[0] for x, y in zip(ranges, ranges[1:]))
+                if len(ranges) == 1:
+                    assert ranges[0][2] == -1
+                else:
+                    slots = [x[2] for x in ranges]
+                    assert slots == list(range(slots[0], slots[0] + len(slots)))
+                    assert any(list(c[:5]) == [r, h, cs, slots[0], len(slots)] for c in comb)
+    assert not cover
+    return ap
+
+
+def test_attention_plan_covers_every_tile_once():
+    attention_plan_coverage([0, 64], [320], 4, 2, 64, 256)
+    ap = attention_plan_coverage(np.cumsum([0] + [128] * 8).tolist(), [8320] * 8, 32, 8, 128, 256)
+    assert ap.n_combine > 0 and ap.ws_bytes > 0            # short suffixes: split key ranges
+    ap = attention_plan_coverage([0, 2048, 4096, 6144, 8192], [34816] * 4, 64, 8, 128, 256)
+    assert ap.n_combine == 0                                # plenty of tiles: no split
+    rng = np.random.default_rng(3)
+    S = rng.integers(1, 700, 10)
+    L = S + 16 * rng.integers(0, 300, 10)
+    attention_plan_coverage(np.concatenate([[0], np.cumsum(S)]).tolist(), L.tolist(), 32, 8, 128, 256)
+    attention_plan_coverage([0, 1], [1], 8, 1, 128, 256)
+
+
+def test_attention_plan_places_a_group_on_one_xcd():
+    cu = np.cumsum([0] + [2048] * 4).tolist()
+    ap = ak.attention_plan(cu, [34816] * 4, 64, 8, 128, 256)
+    xcd_of = {}
+    for i, it in enumerate(ap.work[: ap.n_work]):
+        if it[0] < 0:
+            continue
+        key = (int(it[0]), int(it[1]))
+        assert xcd_of.setdefault(key, i % 8) == i % 8

@@ -17,7 +17,7 @@ import numpy as np
 
 from .configs import VOCAB, Config
 
-KIND_DOC, KIND_QUESTION, KIND_SESSION, KIND_ONEOFF = 0, 1, 2, 3
+KIND_DOC, KIND_QUESTION, KIND_SESSION, KIND_ONEOFF, KIND_STREAM = 0, 1, 2, 3, 4
 TAG_TOKENS, TAG_Q, TAG_K, TAG_V = 0, 1, 2, 3
 
 
@@ -89,7 +89,7 @@ def stream_tiny(cfg: Config):
 def stream_docqa(cfg: Config, n_batches: int | None = None):
     e = cfg.extra
     n_batches = e["n_batches"] if n_batches is None else n_batches
-    rng = np.random.default_rng(derive_seed(cfg.seed, KIND_DOC, -1, 99))
+    rng = np.random.default_rng(derive_seed(cfg.seed, KIND_STREAM, 0, 0))
     rank_to_doc = rng.permutation(e["n_docs"])
     ranks = rng.choice(e["n_docs"], size=n_batches * cfg.max_batch, p=zipf_probs(e["n_docs"], e["zipf_s"]))
     out = []
