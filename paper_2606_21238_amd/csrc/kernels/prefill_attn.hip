@@ -30,6 +30,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cmath>
+#include <type_traits>
 
 #include "../host/internal.hpp"
 
@@ -37,26 +38,41 @@ namespace {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef float f32x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void lds_void;
 
 constexpr int kThreads = 256;  // 4 wave64
 constexpr int kCols = 256;     // query columns per work-group (64 per wave)
-constexpr int kBK = 64;        // keys per K/V tile
+constexpr int kBK = 64;        // keys per K/V tile (4 blocks of 16)
+constexpr float kLazy = 8.0f;  // rescale O only when a column max grows by > 2^8
 
 struct Work {
   int32_t req, kvh, col_start, kv_start, kv_end, slot, pad0, pad1;
 };
 
-// LDS swizzles (16-byte chunk index XOR a function of the row) so that the 8 lanes served
-// together by ds_read_b128 hit 8 different bank groups.
-__device__ __forceinline__ int swz_k(int row) { return (row & 3) | ((row >> 1) & 4); }
-__device__ __forceinline__ int swz_v(int row) { return row & 7; }
-// MFMA row i of S^T is fed by K row pi(i): bits 2 and 3 swapped.
+// MFMA row i of S^T is fed by K row pi(i) (bits 2 and 3 swapped): then accumulator register r
+// of a lane in half hg holds key 16 (r / 8) + 8 hg + r % 8 of its 32-key block, which is the
+// B-operand order of the P.V step.
 __device__ __forceinline__ int pi_row(int i) { return (i & ~12) | ((i & 4) << 1) | ((i & 8) >> 1); }
 
+// LDS layouts (ds_read_b128 is conflict-free when each 16-lane group reads 16 different
+// 16-byte slots of a 256-byte bank window):
+//  K tile: 64 key rows of D bf16; 16-byte chunk c of row r stored at chunk c ^ fk(r).
+//  V tile: block-major [4][D][16 keys]; 16-byte half h of dim row d stored at h ^ sv(d).
+template <int D>
+__device__ __forceinline__ int fk(int r) { return D == 128 ? (r & 15) : ((r >> 1) & 7); }
+__device__ __forceinline__ int sv(int d) { return (d >> 3) & 1; }
+
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+__device__ __forceinline__ void load_lds16(const void* g, lds_void* l) {
+  __builtin_amdgcn_global_load_lds(g, l, 16, 0, 0);
+}
 
 template <int D, int G>
 __global__ __launch_bounds__(kThreads, 1) void prefill_attn_kernel(
@@ -66,17 +82,17 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_attn_kernel(
     const int32_t* __restrict__ cu_q, const int32_t* __restrict__ seq_lens, int n_reqs,
     const Work* __restrict__ work, int64_t n_q, int64_t num_blocks, int hq, int hkv,
     float scale_log2, float* __restrict__ ws_o, float* __restrict__ ws_lse, int64_t ws_slots) {
-  constexpr int KCH = D / 8;                        // 16-byte chunks per K row
-  constexpr int KSTEPS = D / 16;                    // k-steps of Q.K^T
-  constexpr int DM = D / 32;                        // 32-row blocks of O^T
-  constexpr int KLOADS = kBK * KCH / kThreads;      // K chunks per thread per tile
-  constexpr int VLOADS = D * (kBK / 8) / kThreads;  // V chunks per thread per tile
-  __shared__ __attribute__((aligned(16))) uint16_t sk[2][kBK * D];
-  __shared__ __attribute__((aligned(16))) uint16_t sv[2][D * kBK];
+  constexpr int KSTEPS = D / 16;                 // k-steps of Q.K^T
+  constexpr int DM = D / 32;                     // 32-row blocks of O^T
+  constexpr int TILE = kBK * D * 2;              // bytes of one K (or V) tile
+  constexpr int NLD = TILE / (kThreads * 16);    // 16-byte direct loads per thread per tile
+  constexpr int BLK_BYTES = 16 * D * 2;          // one block of one head, K or V
+  __shared__ __attribute__((aligned(1024))) char smem[4 * TILE];  // K0 K1 V0 V1
 
   const Work w = work[blockIdx.x];
   if (w.req < 0 || w.req >= n_reqs || w.kvh < 0 || w.kvh >= hkv || w.col_start < 0) return;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l32 = lane & 31, hg = lane >> 5;
   const int q0 = cu_q[w.req];
   const int S = cu_q[w.req + 1] - q0;
@@ -85,9 +101,8 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_attn_kernel(
   const int ncols = S * G;
   const int32_t* bt = block_tables + static_cast<int64_t>(w.req) * bt_stride;
   const int nblk = min((L + 15) >> 4, bt_stride);
-  const int64_t kvh_off = w.kvh;
 
-  // ---- this lane's two query columns and their Q^T operands --------------------------
+  // ---- this lane's two query columns and their Q^T operands ----------------------------
   int pos[2];
   bool cval[2];
   int64_t qrow[2];
@@ -100,12 +115,9 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_attn_kernel(
     pos[nb] = cval[nb] ? P + tok : -1;
     qrow[nb] = static_cast<int64_t>(q0 + tok) * hq + w.kvh * G + g;
 #pragma unroll
-    for (int ks = 0; ks < KSTEPS; ++ks) {
-      if (cval[nb])
-        qf[nb][ks] = *reinterpret_cast<const bf16x8_t*>(q + qrow[nb] * D + ks * 16 + hg * 8);
-      else
-        qf[nb][ks] = bf16x8_t{};
-    }
+    for (int ks = 0; ks < KSTEPS; ++ks)
+      qf[nb][ks] = cval[nb] ? *reinterpret_cast<const bf16x8_t*>(q + qrow[nb] * D + ks * 16 + hg * 8)
+                            : bf16x8_t{};
   }
 
   const int last_col = min(w.col_start + kCols, ncols) - 1;
@@ -113,58 +125,59 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_attn_kernel(
   const int wg_min_pos = P + w.col_start / G;
   const int kv_lo = max(w.kv_start, 0);
   const int kv_hi = min(w.kv_end, wg_max_pos + 1);
+  const int ntiles = kv_hi > kv_lo ? (kv_hi - kv_lo + kBK - 1) / kBK : 0;
 
-  // ---- K/V tile gather: pool -> registers -> LDS ---------------------------------------
-  uint4 kreg[KLOADS], vreg[VLOADS];
-  auto load_tile = [&](int t0) {
+  // ---- direct global -> LDS tile loads -------------------------------------------------
+  // load i of a thread covers LDS bytes [i*4096 + wave*1024 + lane*16, +16) of the tile; each
+  // wave's 1 KiB lies inside one block, so the block's physical address is wave-uniform.
+  int k_off[NLD], v_off[NLD], blk_of[NLD];
 #pragma unroll
-    for (int i = 0; i < KLOADS; ++i) {
-      const int c = tid + i * kThreads;
-      const int row = c / KCH, ch = c % KCH;
-      const int tok = t0 + row, b = tok >> 4;
-      const int32_t phys = b < nblk ? bt[b] : -1;
-      uint4 v = make_uint4(0, 0, 0, 0);
-      if (tok < L && phys >= 0 && phys < num_blocks)
-        v = *reinterpret_cast<const uint4*>(
-            k_pool + ((static_cast<int64_t>(phys) * hkv + kvh_off) * 16 + (tok & 15)) * D + ch * 8);
-      kreg[i] = v;
-    }
-#pragma unroll
-    for (int i = 0; i < VLOADS; ++i) {
-      const int c = tid + i * kThreads;
-      const int d = c >> 3, ch = c & 7;  // 8 chunks of 8 keys per 64-key row
-      const int tok = t0 + ch * 8, b = tok >> 4;
-      const int32_t phys = b < nblk ? bt[b] : -1;
-      uint4 v = make_uint4(0, 0, 0, 0);
-      if (tok < L && phys >= 0 && phys < num_blocks) {
-        v = *reinterpret_cast<const uint4*>(
-            v_pool + ((static_cast<int64_t>(phys) * hkv + kvh_off) * D + d) * 16 + (ch & 1) * 8);
-        const int valid = L - tok;  // keys past the prompt end hold stale bytes: zero them
-        if (valid < 8) {
-          uint32_t* u = reinterpret_cast<uint32_t*>(&v);
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            if (2 * j >= valid) u[j] = 0;
-            else if (2 * j + 1 >= valid) u[j] &= 0xFFFFu;
-          }
-        }
-      }
-      vreg[i] = v;
-    }
+  for (int i = 0; i < NLD; ++i) {
+    const int posb = i * 4096 + wave * 1024 + lane * 16;
+    const int r = posb / (2 * D), p = (posb % (2 * D)) / 16;      // K: row r, stored chunk p
+    blk_of[i] = posb / BLK_BYTES;
+    k_off[i] = (r & 15) * D + ((p ^ fk<D>(r)) * 8);               // elements inside the block
+    const int qv = posb % BLK_BYTES, d = qv / 32, h = ((qv / 16) & 1) ^ sv(d);
+    v_off[i] = d * 16 + h * 8;
+  }
+  const int64_t head_k = static_cast<int64_t>(w.kvh) * 16 * D;   // head offset inside a block
+  const int64_t blk_stride = static_cast<int64_t>(hkv) * 16 * D;  // elements per physical block
+  auto phys_of = [&](int b) -> int64_t {
+    int32_t ph = b < nblk ? bt[b] : 0;
+    if (ph < 0 || ph >= num_blocks) ph = 0;  // never dereferenced unmasked (see masking)
+    return static_cast<int64_t>(ph) * blk_stride + head_k;
   };
-  auto store_tile = [&](int buf) {
+  auto load_k = [&](int tile, int buf) {
+    const int b0 = (kv_lo + tile * kBK) >> 4;
 #pragma unroll
-    for (int i = 0; i < KLOADS; ++i) {
-      const int c = tid + i * kThreads;
-      const int row = c / KCH, ch = c % KCH;
-      *reinterpret_cast<uint4*>(&sk[buf][row * D + ((ch ^ swz_k(row)) * 8)]) = kreg[i];
-    }
+    for (int i = 0; i < NLD; ++i)
+      load_lds16(k_pool + phys_of(b0 + blk_of[i]) + k_off[i],
+                 (lds_void*)(smem + buf * TILE + i * 4096 + wave * 1024));
+  };
+  auto load_v = [&](int tile, int buf) {
+    const int b0 = (kv_lo + tile * kBK) >> 4;
 #pragma unroll
-    for (int i = 0; i < VLOADS; ++i) {
-      const int c = tid + i * kThreads;
-      const int d = c >> 3, ch = c & 7;
-      *reinterpret_cast<uint4*>(&sv[buf][d * kBK + ((ch ^ swz_v(d)) * 8)]) = vreg[i];
-    }
+    for (int i = 0; i < NLD; ++i)
+      load_lds16(v_pool + phys_of(b0 + blk_of[i]) + v_off[i],
+                 (lds_void*)(smem + (2 + buf) * TILE + i * 4096 + wave * 1024));
+  };
+
+  // ---- MFMA pieces ------------------------------------------------------------------------
+  // S^T (64 keys x this wave's 64 columns) = K . Q^T
+  auto mma_s = [&](f32x16_t (&s)[2][2], int buf) {
+    const char* kb = smem + buf * TILE;
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb) s[mb][0] = s[mb][1] = f32x16_t{};
+#pragma unroll
+    for (int ks = 0; ks < KSTEPS; ++ks)
+#pragma unroll
+      for (int mb = 0; mb < 2; ++mb) {
+        const int r = mb * 32 + pi_row(l32);
+        const int c = 2 * ks + hg;
+        const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(kb + r * 2 * D + ((c ^ fk<D>(r)) * 16));
+        s[mb][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[0][ks], s[mb][0], 0, 0, 0);
+        s[mb][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[1][ks], s[mb][1], 0, 0, 0);
+      }
   };
 
   f32x16_t o[DM][2];
@@ -173,93 +186,136 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_attn_kernel(
   float m_run[2] = {-INFINITY, -INFINITY};
   float l_run[2] = {0.f, 0.f};
 
-  if (kv_lo < kv_hi) {
-    load_tile(kv_lo);
-    store_tile(0);
-  }
-  __syncthreads();
-
-  int buf = 0;
-  for (int t0 = kv_lo; t0 < kv_hi; t0 += kBK, buf ^= 1) {
-    const bool has_next = t0 + kBK < kv_hi;
-    if (has_next) load_tile(t0 + kBK);
-
-    // S^T (64 keys x 64 columns per wave) = K . Q^T
-    f32x16_t s[2][2];
+  // causal / prompt-end mask: accumulator register r of S^T block mb holds key
+  // t0 + 32 mb + 16 (r / 8) + 8 hg + r % 8 of this lane's column
+  auto apply_mask = [&](f32x16_t (&s)[2][2], int t0) {
 #pragma unroll
-    for (int mb = 0; mb < 2; ++mb) {
-      s[mb][0] = s[mb][1] = f32x16_t{};
-      const int row = mb * 32 + pi_row(l32);
-#pragma unroll
-      for (int ks = 0; ks < KSTEPS; ++ks) {
-        const int ch = 2 * ks + hg;
-        const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(&sk[buf][row * D + ((ch ^ swz_k(row)) * 8)]);
-        s[mb][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[0][ks], s[mb][0], 0, 0, 0);
-        s[mb][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[1][ks], s[mb][1], 0, 0, 0);
-      }
-    }
-
-    // online softmax; accumulator register r of S^T block mb holds key
-    // t0 + 32 mb + 16 (r / 8) + 8 hg + r % 8 for this lane's column
-    const bool need_mask = (t0 + kBK - 1 > wg_min_pos) || (t0 + kBK > L);
-    bf16x8_t pb[2][4];
-#pragma unroll
-    for (int nb = 0; nb < 2; ++nb) {
-      float mx = -INFINITY;
+    for (int nb = 0; nb < 2; ++nb)
 #pragma unroll
       for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          float x = s[mb][nb][r];
-          if (need_mask) {
-            const int key = t0 + mb * 32 + 16 * (r >> 3) + 8 * hg + (r & 7);
-            if (key > pos[nb]) x = -INFINITY;
-          }
-          s[mb][nb][r] = x;
-          mx = fmaxf(mx, x);
+          const int key = t0 + mb * 32 + 16 * (r >> 3) + 8 * hg + (r & 7);
+          s[mb][nb][r] = key > pos[nb] ? -INFINITY : s[mb][nb][r];
         }
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const float m_new = fmaxf(m_run[nb], mx * scale_log2);
-      const float m_use = m_new == -INFINITY ? 0.f : m_new;
-      const float alpha = fast_exp2(m_run[nb] - m_use);
-      m_run[nb] = m_new;
+  };
+  // column maxima (base-2 scaled) and the lazy rescale of O when a maximum grew by > 2^kLazy
+  auto update_max = [&](f32x16_t (&s)[2][2]) {
+    float mx[2];
 #pragma unroll
-      for (int md = 0; md < DM; ++md) o[md][nb] *= alpha;
+    for (int nb = 0; nb < 2; ++nb) {
+      float m = -INFINITY;
+#pragma unroll
+      for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) m = fmaxf(m, s[mb][nb][r]);
+      m = fmaxf(m, __shfl_xor(m, 32));
+      mx[nb] = m * scale_log2;
+    }
+    const bool grow = (mx[0] > m_run[0] + kLazy) || (mx[1] > m_run[1] + kLazy);
+    if (__builtin_amdgcn_ballot_w64(grow) != 0) {
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb) {
+        const float m_new = fmaxf(m_run[nb], mx[nb]);
+        const float alpha = m_new == -INFINITY ? 1.f : fast_exp2(m_run[nb] - m_new);
+        m_run[nb] = m_new;
+        l_run[nb] *= alpha;
+#pragma unroll
+        for (int md = 0; md < DM; ++md) o[md][nb] *= alpha;
+      }
+    }
+  };
+  // p = 2^(s * scale * log2 e - m) rounded to bf16 (the P^T operands); row sums of the rounded p
+  auto exp_phase = [&](f32x16_t (&s)[2][2], bf16x8_t (&pb)[2][4]) {
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb) {
+      const float mu = m_run[nb] == -INFINITY ? 0.f : m_run[nb];
       float lsum = 0.f;
 #pragma unroll
       for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
         for (int half = 0; half < 2; ++half) {
-          f32x8_t pv;
+          // pairs are converted (and summed) one 32-bit register at a time: the row sum reads
+          // exactly the registers that feed the P.V MFMA
+          uint32_t wd[4];
 #pragma unroll
-          for (int j = 0; j < 8; ++j) {
-            const float p = fast_exp2(fmaf(s[mb][nb][8 * half + j], scale_log2, -m_use));
-            pv[j] = p;
-            lsum += p;
+          for (int j = 0; j < 4; ++j) {
+            const f32x2_t two = {fast_exp2(fmaf(s[mb][nb][8 * half + 2 * j], scale_log2, -mu)),
+                                 fast_exp2(fmaf(s[mb][nb][8 * half + 2 * j + 1], scale_log2, -mu))};
+            const bf16x2_t pr = __builtin_convertvector(two, bf16x2_t);
+            lsum = __builtin_amdgcn_fdot2_f32_bf16(pr, __builtin_bit_cast(bf16x2_t, 0x3F803F80u), lsum, false);
+            wd[j] = __builtin_bit_cast(uint32_t, pr);
           }
-          pb[nb][2 * mb + half] = __builtin_convertvector(pv, bf16x8_t);
+          const u32x4_t w4 = {wd[0], wd[1], wd[2], wd[3]};
+          pb[nb][2 * mb + half] = __builtin_bit_cast(bf16x8_t, w4);
         }
-      l_run[nb] = l_run[nb] * alpha + lsum;
+      l_run[nb] += lsum;
     }
-
-    // O^T (D x 64 columns per wave) += V^T . P^T
+  };
+  // O^T (D x this wave's 64 columns) += V^T . P^T
+  auto mma_pv = [&](bf16x8_t (&pb)[2][4], int buf) {
+    const char* vb = smem + (2 + buf) * TILE;
 #pragma unroll
-    for (int md = 0; md < DM; ++md) {
-      const int d = md * 32 + l32;
+    for (int sp = 0; sp < 4; ++sp)
 #pragma unroll
-      for (int sp = 0; sp < 4; ++sp) {
-        const int ch = 2 * sp + hg;
-        const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(&sv[buf][d * kBK + ((ch ^ swz_v(d)) * 8)]);
+      for (int md = 0; md < DM; ++md) {
+        const int d = md * 32 + l32;
+        const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(vb + sp * BLK_BYTES + d * 32 + ((hg ^ sv(d)) * 16));
         o[md][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[0][sp], o[md][0], 0, 0, 0);
         o[md][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[1][sp], o[md][1], 0, 0, 0);
       }
+  };
+  // keys >= L of the last tile may hold stale bytes (even NaN patterns): zero their V in LDS
+  auto zero_v_tail = [&](int buf, int t0) {
+    uint16_t* vb = reinterpret_cast<uint16_t*>(smem + (2 + buf) * TILE);
+    for (int e = tid; e < kBK * D; e += kThreads) {
+      const int key = e & (kBK - 1), d = e / kBK;
+      if (t0 + key >= L) {
+        const int blk = key >> 4, kk = key & 15;
+        const int h = ((kk >> 3) ^ sv(d));
+        vb[(blk * BLK_BYTES + d * 32 + h * 16) / 2 + (kk & 7)] = 0;
+      }
     }
+  };
 
-    if (has_next) store_tile(buf ^ 1);
+  // ---- main pipeline ----------------------------------------------------------------------
+  // LDS: K(i+1) in K[(i+1)&1], V(i) in V[i&1]; the loads of K(i+2) and V(i+1) fly during step
+  // i, and S(i+1) = K(i+1) Q^T is multiplied in the same basic block as the exponentials of
+  // tile i, so the scheduler can overlap the MFMAs with the VALU work.
+  f32x16_t sa[2][2], sb[2][2];
+  bf16x8_t pb[2][4];
+  if (ntiles > 0) {
+    load_k(0, 0);
+    load_v(0, 0);
+    if (ntiles > 1) load_k(1, 1);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
+    mma_s(sa, 0);
   }
+  auto step = [&](f32x16_t (&sc)[2][2], f32x16_t (&sn)[2][2], int i) {
+    const int t0 = kv_lo + i * kBK;
+    if (t0 + kBK > L) {  // uniform: only the tile holding the prompt end
+      zero_v_tail(i & 1, t0);
+      __syncthreads();
+    }
+    if (i + 2 < ntiles) load_k(i + 2, i & 1);
+    if (i + 1 < ntiles) load_v(i + 1, (i + 1) & 1);
+    if ((t0 + kBK - 1 > wg_min_pos) || (t0 + kBK > L)) apply_mask(sc, t0);
+    update_max(sc);
+    mma_s(sn, (i + 1) & 1);  // on the last tile this multiplies stale LDS; the result is unused
+    exp_phase(sc, pb);
+    mma_pv(pb, i & 1);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+  };
+  int i = 0;
+  for (; i + 1 < ntiles; i += 2) {
+    step(sa, sb, i);
+    step(sb, sa, i + 1);
+  }
+  if (i < ntiles) step(sa, sb, i);
 
-  // ---- epilogue: O^T register r of block md holds dim 32 md + 8 (r / 4) + 4 hg + r % 4 ----
+  // ---- epilogue: O^T register r of block md holds dim 32 md + 8 (r / 4) + 4 hg + r % 4 ------
 #pragma unroll
   for (int nb = 0; nb < 2; ++nb) {
     const float lt = l_run[nb] + __shfl_xor(l_run[nb], 32);
@@ -275,8 +331,7 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_attn_kernel(
           f32x4_t v;
 #pragma unroll
           for (int j = 0; j < 4; ++j) v[j] = o[md][nb][4 * r4 + j] * inv;
-          const bf16x4_t b = __builtin_convertvector(v, bf16x4_t);
-          *reinterpret_cast<bf16x4_t*>(dst + md * 32 + 8 * r4 + 4 * hg) = b;
+          *reinterpret_cast<bf16x4_t*>(dst + md * 32 + 8 * r4 + 4 * hg) = __builtin_convertvector(v, bf16x4_t);
         }
     } else if (w.slot < ws_slots) {
       float* po = ws_o + (static_cast<int64_t>(w.slot) * kCols + local) * D;
