@@ -1,18 +1,24 @@
 #!/usr/bin/env python3
 """Benchmark: prefix-cached prefill attention + KV scatter under an ARC block cache, one MI355X.
 
-Workload (document QA on a Llama-3-8B-shaped attention layer): 32 query / 8 KV heads,
-head_dim 128, 16-token blocks, bf16 Q/K/V ~ N(0, 1).  A stream of batches of 8 requests,
-each an 8192-token document drawn Zipf(1.1) from 64 seeded documents plus a fresh 128-token
-question; the KV pool holds 25 % of all document tokens (8192 blocks); the host ARC cache
-decides which prefix blocks hit.  One step = one batch through the whole path:
-block hashing -> ARC plan -> metadata H2D -> KV scatter -> prefill attention -> release.
-Warm-up steps also warm the cache (the stream continues across warm-up and timed steps).
+Default workload, `docqa` (document QA on a Llama-3-8B-shaped attention layer): 32 query /
+8 KV heads, head_dim 128, 16-token blocks, bf16 Q/K/V ~ N(0, 1).  A stream of batches of 8
+requests, each an 8192-token document drawn Zipf(1.1) from 64 seeded documents plus a fresh
+128-token question; the KV pool holds 25 % of all document tokens (8192 blocks); the host ARC
+cache decides which prefix blocks hit.  Warm-up steps also warm the cache (the stream
+continues across warm-up and timed steps).
 
-Inputs (token ids on the host, each batch's computed-token Q/K/V in HBM) are staged before
-the timed region.  Printed: one JSON line with algorithmic attention TFLOP/s over the
-whole step time (value), suffix tokens/s, the roofline of the attention kernel (measured
-with HIP events on its stream) and the CPU oracle timed on a bounded sample.
+Other workloads (`--workload`): `docqa_hit` (8 cached 8192-token documents + fresh 128-token
+questions), `longctx` (70B-shaped layer, 64/8 heads: 4 cached 32768-token documents + fresh
+2048-token suffixes), `short32|short48|short64` (16 sessions per batch adding S new tokens to
+fully cached lognormal histories; KV-read bound).
+
+One step = one batch through the whole path: block hashing -> ARC plan -> metadata H2D ->
+KV scatter -> prefill attention -> release.  Each batch's computed-token Q/K/V are staged in
+HBM before the timed region (token ids stay on the host).  Printed: one JSON line with the
+algorithmic attention TFLOP/s over the whole step time (value), suffix tokens/s, the roofline
+of the attention kernel measured with HIP events on its stream, and the CPU oracle timed on a
+bounded sample.
 """
 
 from __future__ import annotations
@@ -31,6 +37,9 @@ sys.path.insert(0, ROOT)
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA (published)
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E (published)
 
+DEFAULT_STEPS = {"docqa": (48, 16), "docqa_hit": (20, 3), "longctx": (8, 2), "short32": (40, 4),
+                 "short48": (40, 4), "short64": (40, 4)}
+
 
 def attn_flops(S, L, hq, d):
     """Algorithmic flops of prefix-cached attention: QK^T and PV over unmasked scores only."""
@@ -40,16 +49,19 @@ def attn_flops(S, L, hq, d):
 
 
 def attn_bytes(S, L, hq, hkv, d):
-    """Algorithmic HBM bytes: Q read + O write, K/V of every visible key read once, scatter."""
+    """Algorithmic HBM bytes of attention: Q read + O write + K/V of every visible key once."""
     S = np.asarray(S, dtype=np.float64)
     L = np.asarray(L, dtype=np.float64)
-    return float(np.sum(4.0 * S * hq * d + 4.0 * L * hkv * d + 8.0 * S * hkv * d))
+    return float(np.sum(4.0 * S * hq * d + 4.0 * L * hkv * d))
+
+
+def scatter_bytes(S, hkv, d):
+    return float(np.sum(8.0 * np.asarray(S, dtype=np.float64) * hkv * d))
 
 
 def cpu_baseline(cfg, sample, budget_s: float):
-    """Times the fp64 oracle on rows of staged batches (bounded by budget_s seconds)."""
+    """Times the fp64 oracle on query rows of staged batches (bounded by budget_s seconds)."""
     from oracle import attention as oatt
-    from oracle import kvpool as okv
     rows_done, flops, t_used = 0, 0.0, 0.0
     hq, d = cfg.num_q_heads, cfg.head_dim
     for (q_bits, k_bits, v_bits, P) in sample:
@@ -66,11 +78,47 @@ def cpu_baseline(cfg, sample, budget_s: float):
     return rows_done, flops, t_used
 
 
+def make_workload(name: str, steps: int, warmup: int):
+    """-> (cfg, untimed batches, timed batches, description, bound)"""
+    from workloads import get_config
+    from workloads import streams as st
+    if name == "docqa":
+        cfg = get_config("docqa")
+        stream = st.stream_docqa(cfg, n_batches=warmup + steps)
+        b = [stream[i * cfg.max_batch:(i + 1) * cfg.max_batch] for i in range(warmup + steps)]
+        desc = ("docqa: 8 requests/batch, 8192-token documents drawn Zipf(1.1) from 64 + 128-token "
+                "question; 32 q / 8 kv heads, head_dim 128, block 16; KV pool 25% of document tokens "
+                "(8192 blocks)")
+        return cfg, b[:warmup], b[warmup:], desc, "mfma"
+    if name == "docqa_hit":
+        cfg = get_config("docqa")
+        warm, st_b = st.steps_docqa_hit(cfg, warmup + steps)
+        desc = ("docqa_hit: 8 cached 8192-token documents + fresh 128-token questions per step; 32 q / "
+                "8 kv heads, head_dim 128, block 16")
+        return cfg, warm + st_b[:warmup], st_b[warmup:], desc, "mfma"
+    if name == "longctx":
+        cfg = get_config("longctx")
+        warm, st_b = st.steps_longctx(cfg, warmup + steps)
+        desc = ("longctx: 70B-shaped layer, 64 q / 8 kv heads, head_dim 128, block 16; 4 cached "
+                "32768-token documents scattered over a 16384-block pool + fresh 2048-token suffixes")
+        return cfg, warm + st_b[:warmup], st_b[warmup:], desc, "mfma"
+    if name.startswith("short"):
+        S = int(name[5:])
+        cfg = get_config("short")
+        warm, st_b = st.steps_short(cfg, warmup + steps, S)
+        desc = (f"short{S}: 16 sessions/batch rotating over 64, each adding {S} new tokens to a fully "
+                f"cached lognormal(7.5, 0.8) history (block-aligned, clipped to [256, 16384]); 32 q / "
+                f"8 kv heads, head_dim 128, block 16")
+        return cfg, warm + st_b[:warmup], st_b[warmup:], desc, "hbm"
+    raise SystemExit(f"unknown workload {name}")
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=48)
-    ap.add_argument("--warmup", type=int, default=16)
+    ap.add_argument("--workload", default="docqa", choices=sorted(DEFAULT_STEPS))
+    ap.add_argument("--steps", type=int, default=None)
+    ap.add_argument("--warmup", type=int, default=None)
     ap.add_argument("--policy", default="arc", choices=["arc", "lru"])
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle CPU time")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -79,42 +127,41 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": "this path runs on one GPU; --gpus must be 1 (requests are "
-                                   "independent: multi-GPU would run one engine per GPU)"}))
+                                   "independent: several GPUs would each run their own engine)"}))
         sys.exit(2)
+    steps = args.steps if args.steps is not None else DEFAULT_STEPS[args.workload][0]
+    warmup = args.warmup if args.warmup is not None else DEFAULT_STEPS[args.workload][1]
 
     import torch
     import paper_2606_21238_amd as ak
     from paper_2606_21238_amd.engine import PrefillEngine
-    from workloads import get_config
-    from workloads.streams import TensorBank, free_order, stream_docqa, bits
+    from workloads.streams import TensorBank, free_order, bits
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     ak.lib()
-    cfg = get_config("docqa")
+    cfg, untimed, timed, desc, bound = make_workload(args.workload, steps, warmup)
     hq, hkv, d = cfg.num_q_heads, cfg.num_kv_heads, cfg.head_dim
-    n_batches = args.warmup + args.steps
-    stream = stream_docqa(cfg, n_batches=n_batches)
     order = free_order(cfg.seed, cfg.num_phys)
-    batches = [stream[i * cfg.max_batch:(i + 1) * cfg.max_batch] for i in range(n_batches)]
+    batches = untimed + timed
+    n_untimed = len(untimed)
     tokens = [[r.tokens for r in b] for b in batches]
 
     # ---- staging (untimed): plans on a shadow cache, then every batch's Q/K/V in HBM ----
     shadow = ak.BlockCache(args.policy, cfg.capacity, cfg.num_phys, cfg.scratch, order)
-    lru = ak.BlockCache("lru" if args.policy == "arc" else "arc", cfg.capacity, cfg.num_phys,
-                        cfg.scratch, order)
+    other = ak.BlockCache("lru" if args.policy == "arc" else "arc", cfg.capacity, cfg.num_phys,
+                          cfg.scratch, order)
     prefix = []
-    for tl in tokens:
+    s_w = l_w = {"prefix_hit_tokens": 0, "prompt_tokens": 0}
+    for bi, tl in enumerate(tokens):
+        if bi == n_untimed:
+            s_w, l_w = shadow.stats(), other.stats()
         reqs = [(ak.hash_blocks(t), len(t)) for t in tl]
         p = shadow.plan_batch(reqs)
         shadow.release_batch()
         prefix.append(p.prefix_lens.copy())
-        lru.plan_batch(reqs)
-        lru.release_batch()
-        if len(prefix) == args.warmup:
-            s_w, l_w = shadow.stats(), lru.stats()
-    s_e, l_e = shadow.stats(), lru.stats()
-    if args.warmup == 0:
-        s_w = l_w = {"prefix_hit_tokens": 0, "prompt_tokens": 0}
+        other.plan_batch(reqs)
+        other.release_batch()
+    s_e, l_e = shadow.stats(), other.stats()
 
     bank = TensorBank(cfg, "cuda")
     staged = []
@@ -133,7 +180,6 @@ def main():
         del src, dst
 
     eng = PrefillEngine(hq, hkv, d, cfg.capacity, cfg.num_phys, cfg.scratch, args.policy, order)
-    S_list, L_list = [], []
 
     def step(i, ev=None):
         q, kn, vn, out = staged[i]
@@ -150,26 +196,25 @@ def main():
         eng.release()
         return plan, db
 
-    for i in range(args.warmup):
+    for i in range(n_untimed):
         step(i)
     torch.cuda.synchronize()
 
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
-    plans = []
-    n_work = []
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(steps)]
+    plans, n_work = [], []
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for k in range(args.steps):
-        plan, db = step(args.warmup + k, events[k])
+    for k in range(steps):
+        plan, db = step(n_untimed + k, events[k])
         plans.append(plan)
         n_work.append((db.n_work, db.n_combine))
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
 
+    S_list, L_list = [], []
     for k, plan in enumerate(plans):
-        assert np.array_equal(plan.prefix_lens, prefix[args.warmup + k])
-        S = np.diff(plan.cu_q)
-        S_list.append(S)
+        assert np.array_equal(plan.prefix_lens, prefix[n_untimed + k])
+        S_list.append(np.diff(plan.cu_q))
         L_list.append(plan.seq_lens.astype(np.int64))
     F = [attn_flops(S, L, hq, d) for S, L in zip(S_list, L_list)]
     B = [attn_bytes(S, L, hq, hkv, d) for S, L in zip(S_list, L_list)]
@@ -177,8 +222,13 @@ def main():
     t_attn = [e[1].elapsed_time(e[2]) * 1e-3 for e in events]
     total_f = float(np.sum(F))
     suffix_tokens = int(sum(int(s.sum()) for s in S_list))
-    achieved = total_f / np.sum(t_attn) / 1e12                 # per launch: sum F / sum time
     roof_t = [max(f / (PEAK_BF16_TFLOPS * 1e12), b / (PEAK_HBM_GBS * 1e9)) for f, b in zip(F, B)]
+    if bound == "mfma":
+        achieved, peak, unit = total_f / np.sum(t_attn) / 1e12, PEAK_BF16_TFLOPS, "TFLOP/s"
+        per_launch = float(np.mean(F))
+    else:
+        achieved, peak, unit = float(np.sum(B)) / np.sum(t_attn) / 1e9, PEAK_HBM_GBS, "GB/s"
+        per_launch = float(np.mean(B))
     hit = lambda a, b: (a["prefix_hit_tokens"] - b["prefix_hit_tokens"]) / max(
         1, a["prompt_tokens"] - b["prompt_tokens"])
 
@@ -187,38 +237,41 @@ def main():
         "value": round(total_f / wall / 1e12, 2),
         "unit": "TFLOP/s",
         "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
-        "ms_per_step": round(wall / args.steps * 1e3, 3),
+        "steps": steps,
+        "warmup": warmup,
+        "ms_per_step": round(wall / steps * 1e3, 3),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
         "config": {
-            "workload": "docqa: 8 requests/batch, 8192-token documents drawn Zipf(1.1) from 64 + "
-                        "128-token question; 32 q / 8 kv heads, head_dim 128, block 16; KV pool 25% "
-                        "of document tokens (8192 blocks); " + args.policy.upper() + " host cache",
-            "global_batch": cfg.max_batch,
-            "seq_len": cfg.extra["doc_tokens"] + cfg.extra["question_tokens"],
+            "workload": desc + "; " + args.policy.upper() + " host cache",
+            "global_batch": len(timed[0]) if timed else 0,
+            "seq_len": int(np.max(np.concatenate(L_list))) if L_list else 0,
             "parallelism": "single GPU",
         },
         "suffix_tokens_per_s": round(suffix_tokens / wall, 1),
         "roofline": {
-            "bound": "mfma",
+            "bound": bound,
             "kernel": "prefill_attn (+ split-KV combine when planned)",
             "achieved": round(achieved, 2),
-            "peak": PEAK_BF16_TFLOPS,
-            "unit": "TFLOP/s",
-            "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+            "peak": peak,
+            "unit": unit,
+            "frac": round(achieved / peak, 4),
             "traffic": None,
+            "algorithmic_per_launch": per_launch,
             "mean_launch_us": round(float(np.mean(t_attn)) * 1e6, 1),
             "mixed_roofline_frac": round(float(np.sum(roof_t) / np.sum(t_attn)), 4),
+            "tflops_attention": round(total_f / np.sum(t_attn) / 1e12, 2),
+            "hbm_gbs_attention": round(float(np.sum(B)) / np.sum(t_attn) / 1e9, 1),
         },
         "breakdown_ms_per_step": {
             "scatter": round(float(np.mean(t_scatter)) * 1e3, 4),
             "attention": round(float(np.mean(t_attn)) * 1e3, 4),
-            "step_wall": round(wall / args.steps * 1e3, 4),
+            "step_wall": round(wall / steps * 1e3, 4),
+            "scatter_gbs": round(scatter_bytes(np.concatenate(S_list), hkv, d)
+                                 / max(float(np.sum(t_scatter)), 1e-12) / 1e9, 1),
         },
         "cache": {
             "policy": args.policy,
@@ -230,14 +283,13 @@ def main():
     }
 
     if not args.no_cpu_baseline:
-        # bounded oracle sample: the first timed batch's requests, 16 rows at a time
-        from oracle import kvpool as okv  # noqa: F401  (oracle is only used for this leg)
+        # bounded oracle sample: the first timed batch's requests, 16 query rows at a time
         k = 0
         plan = plans[k]
-        q, kn, vn, _ = staged[args.warmup + k]
+        q, _, _, _ = staged[n_untimed + k]
         qb = bits(q)
         sample = []
-        for r, req in enumerate(batches[args.warmup + k]):
+        for r, req in enumerate(timed[k]):
             P = int(plan.prefix_lens[r])
             q0, q1 = int(plan.cu_q[r]), int(plan.cu_q[r + 1])
             _, kf, vf = bank.rows(req, 0, req.n_tokens)
@@ -252,7 +304,7 @@ def main():
         result["cpu_baseline"] = {
             "value": round(fl / tcpu / 1e12, 6), "unit": "TFLOP/s",
             "cores": int(cores), "kind": "oracle",
-            "sample": f"{rows} suffix query rows (all 32 heads) of the first timed batch, fp64 numpy "
+            "sample": f"{rows} suffix query rows (all {hq} heads) of the first timed batch, fp64 numpy "
                       f"oracle, {tcpu:.1f} s",
         }
     print(json.dumps(result))

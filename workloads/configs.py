@@ -48,6 +48,7 @@ CONFIGS = {
                                n_batches=64, warmup_batches=16)),
     # 3: multi-turn conversation, 8B shape: 64 sessions, lognormal histories,
     #    uniform new turns, Zipf(1.0) session activity, capacity 40 % of the working set.
+    #    (capacity 0 = derived from the generated working set)
     "multiturn": Config("multiturn", 1003, 32, 8, 128, capacity=0, scratch=16, num_phys=0, max_batch=16,
                         extra=dict(n_sessions=64, hist_mu=7.5, hist_sigma=0.8, hist_min=256,
                                    hist_max=16384, turn_min=32, turn_max=512, activity_s=1.0,
@@ -56,6 +57,11 @@ CONFIGS = {
     #    document + 2048-token suffix; prefix blocks scattered over a 16384-block pool.
     "longctx": Config("longctx", 1004, 64, 8, 128, capacity=16380, scratch=4, num_phys=16384, max_batch=4,
                       extra=dict(n_docs=4, doc_tokens=32768, suffix_tokens=2048)),
+    # 3-short: the same layer shape, 16 sessions per batch each adding 32-64 new tokens to a
+    #    fully cached lognormal history (the key-read-bound case); pool large enough for all
+    #    64 histories.
+    "short": Config("short", 1003, 32, 8, 128, capacity=16384, scratch=16, num_phys=16400, max_batch=16,
+                    extra=dict(hist_mu=7.5, hist_sigma=0.8, hist_min=256, hist_max=16384)),
     # 5: trace replay: 10,000 requests over 500 documents of U[4096, 16384] tokens,
     #    Zipf(1.1) popularity, 30 % one-off documents; capacity 20 % of the working set.
     "trace": Config("trace", 1005, 32, 8, 128, capacity=0, scratch=16, num_phys=0, max_batch=16,

@@ -196,3 +196,69 @@ def bits(t) -> np.ndarray:
     """bf16 torch tensor -> uint16 numpy bit patterns (host copy)."""
     import torch
     return t.detach().contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+
+
+# ---------------------------------------------------------------------------------------------
+# measured step streams: warm-up batches (fill the cache) followed by timed batches that each
+# carry fresh uncached tokens after cached prefixes
+# ---------------------------------------------------------------------------------------------
+
+def steps_docqa_hit(cfg: Config, n_steps: int):
+    """Warm: 8 distinct documents.  Step k: the same documents + a fresh 128-token question."""
+    e = cfg.extra
+    docs = [Source(KIND_DOC, i, e["doc_tokens"]) for i in range(cfg.max_batch)]
+    warm = [[make_request(cfg, [(d, 0, d.length)]) for d in docs]]
+    steps = []
+    for k in range(n_steps):
+        steps.append([make_request(cfg, [(d, 0, d.length),
+                                         (Source(KIND_QUESTION, 200000 + k * 16 + i, e["question_tokens"]),
+                                          0, e["question_tokens"])]) for i, d in enumerate(docs)])
+    return warm, steps
+
+
+def steps_longctx(cfg: Config, n_steps: int):
+    """Warm: 4 documents of 32768 tokens.  Step k: the same documents + a fresh 2048-token suffix."""
+    e = cfg.extra
+    docs = [Source(KIND_DOC, i, e["doc_tokens"]) for i in range(e["n_docs"])]
+    warm = [[make_request(cfg, [(d, 0, d.length)]) for d in docs]]
+    steps = []
+    for k in range(n_steps):
+        steps.append([make_request(cfg, [(d, 0, d.length),
+                                         (Source(KIND_QUESTION, 300000 + k * 16 + i, e["suffix_tokens"]),
+                                          0, e["suffix_tokens"])]) for i, d in enumerate(docs)])
+    return warm, steps
+
+
+def session_lengths(cfg: Config, n: int, seed_index: int = 0) -> np.ndarray:
+    """Conversation histories: lognormal(mu, sigma) clipped, rounded down to whole blocks."""
+    e = cfg.extra
+    rng = np.random.default_rng(derive_seed(cfg.seed, KIND_STREAM, 10 + seed_index, 0))
+    h = np.clip(np.round(np.exp(rng.normal(e["hist_mu"], e["hist_sigma"], n))), e["hist_min"], e["hist_max"])
+    return (h.astype(np.int64) // 16) * 16
+
+
+def steps_short(cfg: Config, n_steps: int, suffix: int, batch: int = 16, n_sessions: int = 64):
+    """Short new turns over resident histories (the key-read-bound case).
+
+    Warm: every session's history (block-aligned, so all of it is cached).  Step k: a batch of
+    `batch` sessions, rotating through all sessions so consecutive steps read different KV,
+    each with `suffix` fresh tokens after its history."""
+    hist = session_lengths(cfg, n_sessions)
+    srcs = [Source(KIND_SESSION, s, int(hist[s])) for s in range(n_sessions)]
+    warm, cur, blocks = [], [], 0
+    for s in srcs:
+        if cur and (len(cur) == batch or blocks + s.length // 16 > cfg.capacity):
+            warm.append(cur)
+            cur, blocks = [], 0
+        cur.append(make_request(cfg, [(s, 0, s.length)]))
+        blocks += s.length // 16
+    if cur:
+        warm.append(cur)
+    steps = []
+    per = n_sessions // batch
+    for k in range(n_steps):
+        g = k % per
+        steps.append([make_request(cfg, [(srcs[s], 0, srcs[s].length),
+                                         (Source(KIND_QUESTION, 400000 + k * batch + j, suffix), 0, suffix)])
+                      for j, s in enumerate(range(g * batch, (g + 1) * batch))])
+    return warm, steps
