@@ -220,16 +220,18 @@ int32_t arckv_kv_scatter(void* k_pool, void* v_pool, const void* k_new, const vo
  * num_kv_heads); K/V read through the block table.  bf16 in, fp32 accumulate, bf16 out.
  * ------------------------------------------------------------------------------------- */
 
-/* Work decomposition (host): one work item is a 256-column query tile (column = token x
+/* Work decomposition (host): one work item is a query tile of arckv_attention_tile_cols() (column = token x
  * query head of one KV group, token-major) of one (request, KV head) over a key range.
  * Long key ranges are split when the batch has too few tiles to fill num_cus compute units;
  * split tiles are merged by a log-sum-exp combine pass.
  * cu_q, seq_lens: HOST copies of the plan's arrays.  work: host int32 buffer of
- * 8 * work_cap entries (ARCKV_WORK_INTS per item) or NULL to query sizes.
+ * ARCKV_WORK_INTS * work_cap entries or NULL to query sizes.
  * Outputs: *n_work attention items, *n_combine combine items (both stored in work, the
  * combine items after the attention items), *ws_bytes device workspace needed.
  * ENOSPC if n_work + n_combine > work_cap (sizes still reported). */
 #define ARCKV_WORK_INTS 8
+/* Query columns per attention work item (the tile width the plan and the kernel share). */
+int32_t arckv_attention_tile_cols(void);
 int32_t arckv_attention_plan(const int32_t* cu_q, const int32_t* seq_lens, int32_t n_reqs,
                              int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
                              int32_t num_cus, int32_t* work, int64_t work_cap,

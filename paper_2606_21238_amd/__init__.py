@@ -208,6 +208,10 @@ class AttnPlan:
     ws_bytes: int
 
 
+def attention_tile_cols() -> int:
+    return int(lib().arckv_attention_tile_cols())
+
+
 def attention_plan(cu_q, seq_lens, num_q_heads: int, num_kv_heads: int, head_dim: int,
                    num_cus: int = 256) -> AttnPlan:
     cu = np.ascontiguousarray(cu_q, dtype=np.int32)

@@ -1,6 +1,6 @@
 // Work decomposition of prefix-cached prefill attention (host side).
 //
-// A work item covers one query tile of 256 "columns" of one (request, KV head): column
+// A work item covers one query tile of kTileCols "columns" of one (request, KV head): column
 // c = token * G + g (G query heads share a KV head, token-major), so the K/V tiles a work
 // item streams serve all G heads of its group at once.  The key range of a tile ends at the
 // last visible key of its last column (causal: suffix token i of a request with P cached
@@ -21,7 +21,7 @@
 
 namespace {
 
-constexpr int kCols = 256;    // query columns per work-group
+constexpr int kCols = arckv::kTileCols;  // query columns per work-group
 constexpr int kKeyTile = 64;  // keys per K/V tile (split boundaries are multiples of this)
 constexpr int kXcds = 8;      // MI355X: 8 XCDs; dispatch round-robins work-groups over them
 
@@ -32,6 +32,8 @@ struct Item {
 };
 
 }  // namespace
+
+extern "C" int32_t arckv_attention_tile_cols(void) { return kCols; }
 
 extern "C" int32_t arckv_attention_plan(const int32_t* cu_q, const int32_t* seq_lens,
                                         int32_t n_reqs, int32_t num_q_heads, int32_t num_kv_heads,

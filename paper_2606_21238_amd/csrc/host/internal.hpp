@@ -9,6 +9,11 @@
 
 namespace arckv {
 
+// Query columns (token x query head of one KV group) per attention work-group: 4 wave64,
+// each owning kWaveCols columns.  Shared by the host work plan and the kernel.
+constexpr int kWaveCols = 32;
+constexpr int kTileCols = 4 * kWaveCols;
+
 // Records a thread-local message for arckv_last_error() and returns `code`.
 int32_t fail(int32_t code, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
 void clear_error();

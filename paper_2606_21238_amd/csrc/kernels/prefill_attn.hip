@@ -8,14 +8,15 @@
 // Sec. 4; layout V1: K [blk][kvh][16][D], V [blk][kvh][D][16]).
 //
 // Design (MI355X-first):
-//  * One work-group = 4 wave64s = one 256-column query tile of one (request, KV head); a
+//  * One work-group = 4 wave64s = one kTileCols-column query tile of one (request, KV head); a
 //    column is (token, head-of-group), token-major, so every K/V tile a work-group loads
 //    serves all G query heads of its KV head (GQA packed into the MFMA N dimension).
 //  * Transposed formulation: S^T = K . Q^T and O^T = V^T . P^T with v_mfma_f32_32x32x16_bf16.
 //    Query columns sit on lanes, keys / head dims on the M (register) dimension, so a lane
 //    owns whole columns: row max and row sum are in-lane plus one exchange with lane +- 32.
-//    Each wave owns 64 columns (two 32-column N blocks), so every K/V operand read from LDS
-//    feeds two MFMAs.
+//    Each wave owns kWaveCols columns (32-column MFMA N blocks); with 32 columns a wave fits
+//    in 256 registers and two work-groups share a CU, so each SIMD interleaves two waves'
+//    MFMA and softmax work.
 //  * K rows are fed to the MFMA in an order that swaps bits 2 and 3 of the row index; the
 //    accumulator layout of S^T then puts 8 consecutive keys per lane half, which is exactly
 //    the B-operand layout of the P.V step, so P^T goes from registers to the next MFMA with
@@ -46,8 +47,9 @@ typedef float f32x2_t __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void lds_void;
 
-constexpr int kThreads = 256;  // 4 wave64
-constexpr int kCols = 256;     // query columns per work-group (64 per wave)
+constexpr int kThreads = 256;                // 4 wave64
+constexpr int kNB = arckv::kWaveCols / 32;    // 32-column MFMA blocks per wave
+constexpr int kCols = arckv::kTileCols;       // query columns per work-group
 constexpr int kBK = 64;        // keys per K/V tile (4 blocks of 16)
 constexpr float kLazy = 8.0f;  // rescale O only when a column max grows by > 2^8
 
@@ -75,7 +77,7 @@ __device__ __forceinline__ void load_lds16(const void* g, lds_void* l) {
 }
 
 template <int D, int G>
-__global__ __launch_bounds__(kThreads, 1) void prefill_attn_kernel(
+__global__ __launch_bounds__(kThreads, kNB == 1 ? 2 : 1) void prefill_attn_kernel(
     const uint16_t* __restrict__ k_pool, const uint16_t* __restrict__ v_pool,
     const uint16_t* __restrict__ q, uint16_t* __restrict__ out,
     const int32_t* __restrict__ block_tables, int bt_stride,
@@ -103,13 +105,13 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_attn_kernel(
   const int nblk = min((L + 15) >> 4, bt_stride);
 
   // ---- this lane's two query columns and their Q^T operands ----------------------------
-  int pos[2];
-  bool cval[2];
-  int64_t qrow[2];
-  bf16x8_t qf[2][KSTEPS];
+  int pos[kNB];
+  bool cval[kNB];
+  int64_t qrow[kNB];
+  bf16x8_t qf[kNB][KSTEPS];
 #pragma unroll
-  for (int nb = 0; nb < 2; ++nb) {
-    const int col = w.col_start + wave * 64 + nb * 32 + l32;
+  for (int nb = 0; nb < kNB; ++nb) {
+    const int col = w.col_start + wave * arckv::kWaveCols + nb * 32 + l32;
     const int tok = col / G, g = col % G;
     cval[nb] = col < ncols && (q0 + tok) < n_q;
     pos[nb] = cval[nb] ? P + tok : -1;
@@ -164,10 +166,12 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_attn_kernel(
 
   // ---- MFMA pieces ------------------------------------------------------------------------
   // S^T (64 keys x this wave's 64 columns) = K . Q^T
-  auto mma_s = [&](f32x16_t (&s)[2][2], int buf) {
+  auto mma_s = [&](f32x16_t (&s)[2][kNB], int buf) {
     const char* kb = smem + buf * TILE;
 #pragma unroll
-    for (int mb = 0; mb < 2; ++mb) s[mb][0] = s[mb][1] = f32x16_t{};
+    for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+      for (int nb = 0; nb < kNB; ++nb) s[mb][nb] = f32x16_t{};
 #pragma unroll
     for (int ks = 0; ks < KSTEPS; ++ks)
 #pragma unroll
@@ -175,22 +179,26 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_attn_kernel(
         const int r = mb * 32 + pi_row(l32);
         const int c = 2 * ks + hg;
         const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(kb + r * 2 * D + ((c ^ fk<D>(r)) * 16));
-        s[mb][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[0][ks], s[mb][0], 0, 0, 0);
-        s[mb][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[1][ks], s[mb][1], 0, 0, 0);
+#pragma unroll
+        for (int nb = 0; nb < kNB; ++nb)
+          s[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[nb][ks], s[mb][nb], 0, 0, 0);
       }
   };
 
-  f32x16_t o[DM][2];
+  f32x16_t o[DM][kNB];
 #pragma unroll
-  for (int md = 0; md < DM; ++md) o[md][0] = o[md][1] = f32x16_t{};
-  float m_run[2] = {-INFINITY, -INFINITY};
-  float l_run[2] = {0.f, 0.f};
+  for (int md = 0; md < DM; ++md)
+#pragma unroll
+    for (int nb = 0; nb < kNB; ++nb) o[md][nb] = f32x16_t{};
+  float m_run[kNB], l_run[kNB];
+#pragma unroll
+  for (int nb = 0; nb < kNB; ++nb) { m_run[nb] = -INFINITY; l_run[nb] = 0.f; }
 
   // causal / prompt-end mask: accumulator register r of S^T block mb holds key
   // t0 + 32 mb + 16 (r / 8) + 8 hg + r % 8 of this lane's column
-  auto apply_mask = [&](f32x16_t (&s)[2][2], int t0) {
+  auto apply_mask = [&](f32x16_t (&s)[2][kNB], int t0) {
 #pragma unroll
-    for (int nb = 0; nb < 2; ++nb)
+    for (int nb = 0; nb < kNB; ++nb)
 #pragma unroll
       for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
@@ -200,10 +208,11 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_attn_kernel(
         }
   };
   // column maxima (base-2 scaled) and the lazy rescale of O when a maximum grew by > 2^kLazy
-  auto update_max = [&](f32x16_t (&s)[2][2]) {
-    float mx[2];
+  auto update_max = [&](f32x16_t (&s)[2][kNB]) {
+    float mx[kNB];
+    bool grow = false;
 #pragma unroll
-    for (int nb = 0; nb < 2; ++nb) {
+    for (int nb = 0; nb < kNB; ++nb) {
       float m = -INFINITY;
 #pragma unroll
       for (int mb = 0; mb < 2; ++mb)
@@ -211,11 +220,11 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_attn_kernel(
         for (int r = 0; r < 16; ++r) m = fmaxf(m, s[mb][nb][r]);
       m = fmaxf(m, __shfl_xor(m, 32));
       mx[nb] = m * scale_log2;
+      grow = grow || (mx[nb] > m_run[nb] + kLazy);
     }
-    const bool grow = (mx[0] > m_run[0] + kLazy) || (mx[1] > m_run[1] + kLazy);
     if (__builtin_amdgcn_ballot_w64(grow) != 0) {
 #pragma unroll
-      for (int nb = 0; nb < 2; ++nb) {
+      for (int nb = 0; nb < kNB; ++nb) {
         const float m_new = fmaxf(m_run[nb], mx[nb]);
         const float alpha = m_new == -INFINITY ? 1.f : fast_exp2(m_run[nb] - m_new);
         m_run[nb] = m_new;
@@ -226,9 +235,9 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_attn_kernel(
     }
   };
   // p = 2^(s * scale * log2 e - m) rounded to bf16 (the P^T operands); row sums of the rounded p
-  auto exp_phase = [&](f32x16_t (&s)[2][2], bf16x8_t (&pb)[2][4]) {
+  auto exp_phase = [&](f32x16_t (&s)[2][kNB], bf16x8_t (&pb)[kNB][4]) {
 #pragma unroll
-    for (int nb = 0; nb < 2; ++nb) {
+    for (int nb = 0; nb < kNB; ++nb) {
       const float mu = m_run[nb] == -INFINITY ? 0.f : m_run[nb];
       float lsum = 0.f;
 #pragma unroll
@@ -253,7 +262,7 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_attn_kernel(
     }
   };
   // O^T (D x this wave's 64 columns) += V^T . P^T
-  auto mma_pv = [&](bf16x8_t (&pb)[2][4], int buf) {
+  auto mma_pv = [&](bf16x8_t (&pb)[kNB][4], int buf) {
     const char* vb = smem + (2 + buf) * TILE;
 #pragma unroll
     for (int sp = 0; sp < 4; ++sp)
@@ -261,8 +270,9 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_attn_kernel(
       for (int md = 0; md < DM; ++md) {
         const int d = md * 32 + l32;
         const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(vb + sp * BLK_BYTES + d * 32 + ((hg ^ sv(d)) * 16));
-        o[md][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[0][sp], o[md][0], 0, 0, 0);
-        o[md][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[1][sp], o[md][1], 0, 0, 0);
+#pragma unroll
+        for (int nb = 0; nb < kNB; ++nb)
+          o[md][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[nb][sp], o[md][nb], 0, 0, 0);
       }
   };
   // keys >= L of the last tile may hold stale bytes (even NaN patterns): zero their V in LDS
@@ -282,8 +292,8 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_attn_kernel(
   // LDS: K(i+1) in K[(i+1)&1], V(i) in V[i&1]; the loads of K(i+2) and V(i+1) fly during step
   // i, and S(i+1) = K(i+1) Q^T is multiplied in the same basic block as the exponentials of
   // tile i, so the scheduler can overlap the MFMAs with the VALU work.
-  f32x16_t sa[2][2], sb[2][2];
-  bf16x8_t pb[2][4];
+  f32x16_t sa[2][kNB], sb[2][kNB];
+  bf16x8_t pb[kNB][4];
   if (ntiles > 0) {
     load_k(0, 0);
     load_v(0, 0);
@@ -292,7 +302,7 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_attn_kernel(
     __syncthreads();
     mma_s(sa, 0);
   }
-  auto step = [&](f32x16_t (&sc)[2][2], f32x16_t (&sn)[2][2], int i) {
+  auto step = [&](f32x16_t (&sc)[2][kNB], f32x16_t (&sn)[2][kNB], int i) {
     const int t0 = kv_lo + i * kBK;
     if (t0 + kBK > L) {  // uniform: only the tile holding the prompt end
       zero_v_tail(i & 1, t0);
@@ -317,10 +327,10 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_attn_kernel(
 
   // ---- epilogue: O^T register r of block md holds dim 32 md + 8 (r / 4) + 4 hg + r % 4 ------
 #pragma unroll
-  for (int nb = 0; nb < 2; ++nb) {
+  for (int nb = 0; nb < kNB; ++nb) {
     const float lt = l_run[nb] + __shfl_xor(l_run[nb], 32);
     const float inv = lt > 0.f ? 1.f / lt : 0.f;
-    const int local = wave * 64 + nb * 32 + l32;
+    const int local = wave * arckv::kWaveCols + nb * 32 + l32;
     if (w.slot < 0) {
       if (!cval[nb]) continue;
       uint16_t* dst = out + qrow[nb] * D;

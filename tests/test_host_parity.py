@@ -183,6 +183,7 @@ def test_error_statuses_match_the_oracle():
 def attention_plan_coverage(cu_q, seq_lens, hq, hkv, d, num_cus):
     ap = ak.attention_plan(cu_q, seq_lens, hq, hkv, d, num_cus)
     g = hq // hkv
+    tc = ak.attention_tile_cols()
     items = ap.work[: ap.n_work]
     comb = ap.work[ap.n_work: ap.n_work + ap.n_combine]
     cover = {}
@@ -195,8 +196,8 @@ def attention_plan_coverage(cu_q, seq_lens, hq, hkv, d, num_cus):
     for r in range(len(seq_lens)):
         S = cu_q[r + 1] - cu_q[r]
         P = seq_lens[r] - S
-        for cs in range(0, S * g, 256):
-            last = min(cs + 256, S * g) - 1
+        for cs in range(0, S * g, tc):
+            last = min(cs + tc, S * g) - 1
             kv_end = P + last // g + 1
             for h in range(hkv):
                 ranges = sorted(cover.pop((r, h, cs)))
