@@ -85,6 +85,12 @@ def load(path: str | None = None):
     if _lib is not None and path is None:
         return _lib
     p = path or LIB_PATH
+    try:
+        # torch ships its own libamdhip64.so.7; loading it first makes libarckv bind to that same
+        # runtime (one HIP runtime per process; two copies do not share devices or streams)
+        import torch  # noqa: F401
+    except ImportError:
+        pass
     if not os.path.exists(p):
         raise RuntimeError(f"libarckv not built: {p} missing; run `python -m paper_2606_21238_amd.build`")
     lib = C.CDLL(p)

@@ -9,10 +9,11 @@
 
 namespace arckv {
 
-// Query columns (token x query head of one KV group) per attention work-group: 4 wave64,
-// each owning kWaveCols columns.  Shared by the host work plan and the kernel.
+// Query columns (token x query head of one KV group) per attention work-group: kTileWaves
+// wave64s, each owning kWaveCols columns.  Shared by the host work plan and the kernel.
 constexpr int kWaveCols = 32;
-constexpr int kTileCols = 4 * kWaveCols;
+constexpr int kTileWaves = 8;
+constexpr int kTileCols = kTileWaves * kWaveCols;
 
 // Records a thread-local message for arckv_last_error() and returns `code`.
 int32_t fail(int32_t code, const char* fmt, ...) __attribute__((format(printf, 2, 3)));

@@ -47,9 +47,10 @@ typedef float f32x2_t __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void lds_void;
 
-constexpr int kThreads = 256;                // 4 wave64
-constexpr int kNB = arckv::kWaveCols / 32;    // 32-column MFMA blocks per wave
-constexpr int kCols = arckv::kTileCols;       // query columns per work-group
+constexpr int kThreads = 64 * arckv::kTileWaves;  // one work-group per CU, two waves per SIMD
+constexpr int kNB = arckv::kWaveCols / 32;         // 32-column MFMA blocks per wave
+constexpr int kCols = arckv::kTileCols;            // query columns per work-group
+constexpr int kStages = 4;                         // K/V tiles resident in LDS (ring)
 constexpr int kBK = 64;        // keys per K/V tile (4 blocks of 16)
 constexpr float kLazy = 8.0f;  // rescale O only when a column max grows by > 2^8
 
@@ -77,7 +78,7 @@ __device__ __forceinline__ void load_lds16(const void* g, lds_void* l) {
 }
 
 template <int D, int G>
-__global__ __launch_bounds__(kThreads, kNB == 1 ? 2 : 1) void prefill_attn_kernel(
+__global__ __launch_bounds__(kThreads, 1) void prefill_attn_kernel(
     const uint16_t* __restrict__ k_pool, const uint16_t* __restrict__ v_pool,
     const uint16_t* __restrict__ q, uint16_t* __restrict__ out,
     const int32_t* __restrict__ block_tables, int bt_stride,
@@ -88,8 +89,10 @@ __global__ __launch_bounds__(kThreads, kNB == 1 ? 2 : 1) void prefill_attn_kerne
   constexpr int DM = D / 32;                     // 32-row blocks of O^T
   constexpr int TILE = kBK * D * 2;              // bytes of one K (or V) tile
   constexpr int NLD = TILE / (kThreads * 16);    // 16-byte direct loads per thread per tile
+  constexpr int LDB = kThreads * 16;             // bytes one load instruction moves per WG
   constexpr int BLK_BYTES = 16 * D * 2;          // one block of one head, K or V
-  __shared__ __attribute__((aligned(1024))) char smem[4 * TILE];  // K0 K1 V0 V1
+  static_assert(NLD >= 1 && TILE % LDB == 0, "tile must be a multiple of one WG-wide load");
+  __shared__ __attribute__((aligned(1024))) char smem[kStages * 2 * TILE];  // stage s: K, then V
 
   const Work w = work[blockIdx.x];
   if (w.req < 0 || w.req >= n_reqs || w.kvh < 0 || w.kvh >= hkv || w.col_start < 0) return;
@@ -130,12 +133,12 @@ __global__ __launch_bounds__(kThreads, kNB == 1 ? 2 : 1) void prefill_attn_kerne
   const int ntiles = kv_hi > kv_lo ? (kv_hi - kv_lo + kBK - 1) / kBK : 0;
 
   // ---- direct global -> LDS tile loads -------------------------------------------------
-  // load i of a thread covers LDS bytes [i*4096 + wave*1024 + lane*16, +16) of the tile; each
+  // load i of a thread covers LDS bytes [i*LDB + wave*1024 + lane*16, +16) of the tile; each
   // wave's 1 KiB lies inside one block, so the block's physical address is wave-uniform.
   int k_off[NLD], v_off[NLD], blk_of[NLD];
 #pragma unroll
   for (int i = 0; i < NLD; ++i) {
-    const int posb = i * 4096 + wave * 1024 + lane * 16;
+    const int posb = i * LDB + wave * 1024 + lane * 16;
     const int r = posb / (2 * D), p = (posb % (2 * D)) / 16;      // K: row r, stored chunk p
     blk_of[i] = posb / BLK_BYTES;
     k_off[i] = (r & 15) * D + ((p ^ fk<D>(r)) * 8);               // elements inside the block
@@ -149,25 +152,22 @@ __global__ __launch_bounds__(kThreads, kNB == 1 ? 2 : 1) void prefill_attn_kerne
     if (ph < 0 || ph >= num_blocks) ph = 0;  // never dereferenced unmasked (see masking)
     return static_cast<int64_t>(ph) * blk_stride + head_k;
   };
-  auto load_k = [&](int tile, int buf) {
+  // tile t (keys kv_lo + 64 t ...) lives in LDS stage t % kStages
+  auto load_tile = [&](int tile) {
     const int b0 = (kv_lo + tile * kBK) >> 4;
+    char* st = smem + (tile % kStages) * 2 * TILE;
 #pragma unroll
-    for (int i = 0; i < NLD; ++i)
-      load_lds16(k_pool + phys_of(b0 + blk_of[i]) + k_off[i],
-                 (lds_void*)(smem + buf * TILE + i * 4096 + wave * 1024));
-  };
-  auto load_v = [&](int tile, int buf) {
-    const int b0 = (kv_lo + tile * kBK) >> 4;
-#pragma unroll
-    for (int i = 0; i < NLD; ++i)
-      load_lds16(v_pool + phys_of(b0 + blk_of[i]) + v_off[i],
-                 (lds_void*)(smem + (2 + buf) * TILE + i * 4096 + wave * 1024));
+    for (int i = 0; i < NLD; ++i) {
+      const int64_t base = phys_of(b0 + blk_of[i]);
+      load_lds16(k_pool + base + k_off[i], (lds_void*)(st + i * LDB + wave * 1024));
+      load_lds16(v_pool + base + v_off[i], (lds_void*)(st + TILE + i * LDB + wave * 1024));
+    }
   };
 
   // ---- MFMA pieces ------------------------------------------------------------------------
   // S^T (64 keys x this wave's 64 columns) = K . Q^T
-  auto mma_s = [&](f32x16_t (&s)[2][kNB], int buf) {
-    const char* kb = smem + buf * TILE;
+  auto mma_s = [&](f32x16_t (&s)[2][kNB], int tile) {
+    const char* kb = smem + (tile % kStages) * 2 * TILE;
 #pragma unroll
     for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
@@ -262,8 +262,8 @@ __global__ __launch_bounds__(kThreads, kNB == 1 ? 2 : 1) void prefill_attn_kerne
     }
   };
   // O^T (D x this wave's 64 columns) += V^T . P^T
-  auto mma_pv = [&](bf16x8_t (&pb)[kNB][4], int buf) {
-    const char* vb = smem + (2 + buf) * TILE;
+  auto mma_pv = [&](bf16x8_t (&pb)[kNB][4], int tile) {
+    const char* vb = smem + (tile % kStages) * 2 * TILE + TILE;
 #pragma unroll
     for (int sp = 0; sp < 4; ++sp)
 #pragma unroll
@@ -276,8 +276,8 @@ __global__ __launch_bounds__(kThreads, kNB == 1 ? 2 : 1) void prefill_attn_kerne
       }
   };
   // keys >= L of the last tile may hold stale bytes (even NaN patterns): zero their V in LDS
-  auto zero_v_tail = [&](int buf, int t0) {
-    uint16_t* vb = reinterpret_cast<uint16_t*>(smem + (2 + buf) * TILE);
+  auto zero_v_tail = [&](int tile, int t0) {
+    uint16_t* vb = reinterpret_cast<uint16_t*>(smem + (tile % kStages) * 2 * TILE + TILE);
     for (int e = tid; e < kBK * D; e += kThreads) {
       const int key = e & (kBK - 1), d = e / kBK;
       if (t0 + key >= L) {
@@ -289,33 +289,37 @@ __global__ __launch_bounds__(kThreads, kNB == 1 ? 2 : 1) void prefill_attn_kerne
   };
 
   // ---- main pipeline ----------------------------------------------------------------------
-  // LDS: K(i+1) in K[(i+1)&1], V(i) in V[i&1]; the loads of K(i+2) and V(i+1) fly during step
-  // i, and S(i+1) = K(i+1) Q^T is multiplied in the same basic block as the exponentials of
-  // tile i, so the scheduler can overlap the MFMAs with the VALU work.
+  // A ring of kStages K/V tiles: step i multiplies S(i+1) = K(i+1) Q^T (in the same basic
+  // block as the exponentials of tile i, so MFMA and VALU work overlap), then O += V(i) P(i),
+  // while tiles i+2 .. i+kStages-1 are in flight.  Tile i+kStages-1 is issued at the start of
+  // step i into the stage tile i-1 used (free once every wave passed the barrier ending step
+  // i-1); the wait ending step i only needs tile i+2, so loads get two steps of latency slack.
+  static_assert(kStages >= 4, "the wait below assumes one tile in flight beyond i+2");
   f32x16_t sa[2][kNB], sb[2][kNB];
   bf16x8_t pb[kNB][4];
   if (ntiles > 0) {
-    load_k(0, 0);
-    load_v(0, 0);
-    if (ntiles > 1) load_k(1, 1);
+    for (int t = 0; t < kStages - 1; ++t)
+      if (t < ntiles) load_tile(t);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
     mma_s(sa, 0);
   }
   auto step = [&](f32x16_t (&sc)[2][kNB], f32x16_t (&sn)[2][kNB], int i) {
     const int t0 = kv_lo + i * kBK;
+    const bool issue = i + kStages - 1 < ntiles;
+    if (issue) load_tile(i + kStages - 1);
     if (t0 + kBK > L) {  // uniform: only the tile holding the prompt end
-      zero_v_tail(i & 1, t0);
+      zero_v_tail(i, t0);
       __syncthreads();
     }
-    if (i + 2 < ntiles) load_k(i + 2, i & 1);
-    if (i + 1 < ntiles) load_v(i + 1, (i + 1) & 1);
     if ((t0 + kBK - 1 > wg_min_pos) || (t0 + kBK > L)) apply_mask(sc, t0);
     update_max(sc);
-    mma_s(sn, (i + 1) & 1);  // on the last tile this multiplies stale LDS; the result is unused
+    mma_s(sn, i + 1);  // on the last tile this multiplies stale LDS; the result is unused
     exp_phase(sc, pb);
-    mma_pv(pb, i & 1);
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    mma_pv(pb, i);
+    // the next step reads tile i+2 (K) and i+1 (V): only the loads just issued may be pending
+    if (issue) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * NLD * (kStages - 3)) : "memory");
+    else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
   };
   int i = 0;
