@@ -207,7 +207,11 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_attn_kernel(
           s[mb][nb][r] = key > pos[nb] ? -INFINITY : s[mb][nb][r];
         }
   };
-  // column maxima (base-2 scaled) and the lazy rescale of O when a maximum grew by > 2^kLazy
+  // Column maxima of a tile (base-2 scaled) and the lazy-rescale decision, without branches:
+  // the running maximum moves only when some column of the wave grew by more than 2^kLazy;
+  // then O and l must be scaled by alpha before the next P.V product (apply_rescale).
+  float alpha[kNB];
+  bool pending = false;  // wave-uniform
   auto update_max = [&](f32x16_t (&s)[2][kNB]) {
     float mx[kNB];
     bool grow = false;
@@ -222,47 +226,59 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_attn_kernel(
       mx[nb] = m * scale_log2;
       grow = grow || (mx[nb] > m_run[nb] + kLazy);
     }
-    if (__builtin_amdgcn_ballot_w64(grow) != 0) {
+    pending = __builtin_amdgcn_ballot_w64(grow) != 0;
+#pragma unroll
+    for (int nb = 0; nb < kNB; ++nb) {
+      const float m_new = pending ? fmaxf(m_run[nb], mx[nb]) : m_run[nb];
+      alpha[nb] = m_new == -INFINITY ? 1.f : fast_exp2(m_run[nb] - m_new);
+      m_run[nb] = m_new;
+    }
+  };
+  auto apply_rescale = [&]() {
+    if (pending) {
 #pragma unroll
       for (int nb = 0; nb < kNB; ++nb) {
-        const float m_new = fmaxf(m_run[nb], mx[nb]);
-        const float alpha = m_new == -INFINITY ? 1.f : fast_exp2(m_run[nb] - m_new);
-        m_run[nb] = m_new;
-        l_run[nb] *= alpha;
+        l_run[nb] *= alpha[nb];
 #pragma unroll
-        for (int md = 0; md < DM; ++md) o[md][nb] *= alpha;
+        for (int md = 0; md < DM; ++md) o[md][nb] *= alpha[nb];
       }
     }
   };
-  // p = 2^(s * scale * log2 e - m) rounded to bf16 (the P^T operands); row sums of the rounded p
-  auto exp_phase = [&](f32x16_t (&s)[2][kNB], bf16x8_t (&pb)[kNB][4]) {
+  // p = 2^(s * scale * log2 e - m) rounded to bf16: the P^T operands of the P.V product, kept
+  // as 32-bit bf16 pairs.  (The row sum reads these scalars; extracting words from the 8-element
+  // vector instead was compiled into four reads of one register.)
+  auto exp_phase = [&](f32x16_t (&s)[2][kNB], uint32_t (&pw)[kNB][4][4]) {
 #pragma unroll
     for (int nb = 0; nb < kNB; ++nb) {
       const float mu = m_run[nb] == -INFINITY ? 0.f : m_run[nb];
-      float lsum = 0.f;
 #pragma unroll
       for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
-        for (int half = 0; half < 2; ++half) {
-          // pairs are converted (and summed) one 32-bit register at a time: the row sum reads
-          // exactly the registers that feed the P.V MFMA
-          uint32_t wd[4];
+        for (int half = 0; half < 2; ++half)
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
             const f32x2_t two = {fast_exp2(fmaf(s[mb][nb][8 * half + 2 * j], scale_log2, -mu)),
                                  fast_exp2(fmaf(s[mb][nb][8 * half + 2 * j + 1], scale_log2, -mu))};
-            const bf16x2_t pr = __builtin_convertvector(two, bf16x2_t);
-            lsum = __builtin_amdgcn_fdot2_f32_bf16(pr, __builtin_bit_cast(bf16x2_t, 0x3F803F80u), lsum, false);
-            wd[j] = __builtin_bit_cast(uint32_t, pr);
+            pw[nb][2 * mb + half][j] = __builtin_bit_cast(uint32_t, __builtin_convertvector(two, bf16x2_t));
           }
-          const u32x4_t w4 = {wd[0], wd[1], wd[2], wd[3]};
-          pb[nb][2 * mb + half] = __builtin_bit_cast(bf16x8_t, w4);
-        }
+    }
+  };
+  // row sums of the bf16-rounded p (exactly what the P.V product weighs V with)
+  auto row_sum = [&](const uint32_t (&pw)[kNB][4][4]) {
+#pragma unroll
+    for (int nb = 0; nb < kNB; ++nb) {
+      float lsum = 0.f;
+#pragma unroll
+      for (int k = 0; k < 4; ++k)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          lsum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, pw[nb][k][j]),
+                                                 __builtin_bit_cast(bf16x2_t, 0x3F803F80u), lsum, false);
       l_run[nb] += lsum;
     }
   };
   // O^T (D x this wave's 64 columns) += V^T . P^T
-  auto mma_pv = [&](bf16x8_t (&pb)[kNB][4], int tile) {
+  auto mma_pv = [&](const uint32_t (&pw)[kNB][4][4], int tile) {
     const char* vb = smem + (tile % kStages) * 2 * TILE + TILE;
 #pragma unroll
     for (int sp = 0; sp < 4; ++sp)
@@ -271,8 +287,10 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_attn_kernel(
         const int d = md * 32 + l32;
         const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(vb + sp * BLK_BYTES + d * 32 + ((hg ^ sv(d)) * 16));
 #pragma unroll
-        for (int nb = 0; nb < kNB; ++nb)
-          o[md][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[nb][sp], o[md][nb], 0, 0, 0);
+        for (int nb = 0; nb < kNB; ++nb) {
+          const u32x4_t w4 = {pw[nb][sp][0], pw[nb][sp][1], pw[nb][sp][2], pw[nb][sp][3]};
+          o[md][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, __builtin_bit_cast(bf16x8_t, w4), o[md][nb], 0, 0, 0);
+        }
       }
   };
   // keys >= L of the last tile may hold stale bytes (even NaN patterns): zero their V in LDS
@@ -289,22 +307,33 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_attn_kernel(
   };
 
   // ---- main pipeline ----------------------------------------------------------------------
-  // A ring of kStages K/V tiles: step i multiplies S(i+1) = K(i+1) Q^T (in the same basic
-  // block as the exponentials of tile i, so MFMA and VALU work overlap), then O += V(i) P(i),
-  // while tiles i+2 .. i+kStages-1 are in flight.  Tile i+kStages-1 is issued at the start of
-  // step i into the stage tile i-1 used (free once every wave passed the barrier ending step
-  // i-1); the wait ending step i only needs tile i+2, so loads get two steps of latency slack.
+  // A ring of kStages K/V tiles; tile i+kStages-1 is issued at the start of step i into the
+  // stage tile i-1 used (free once every wave passed the barrier ending step i-1), and the
+  // wait ending step i only needs tile i+2: loads get two steps of latency slack.
+  // Step i is two MFMA phases, each in one basic block with VALU work to overlap:
+  //   A: S(i+1) = K(i+1) Q^T            || exponentials of tile i (max of tile i known)
+  //   B: O += V(i) P(i)                  || row sums of tile i, mask + max of tile i+1
+  // A rescale of O decided in B of step i is applied at the start of step i+1.  Steps whose
+  // next tile needs masking (diagonal tiles, prompt end) run in a second, peeled loop, so the
+  // main loop carries no mask code.
   static_assert(kStages >= 4, "the wait below assumes one tile in flight beyond i+2");
+  auto tile_masked = [&](int t) {
+    const int t0 = kv_lo + t * kBK;
+    return (t0 + kBK - 1 > wg_min_pos) || (t0 + kBK > L);
+  };
   f32x16_t sa[2][kNB], sb[2][kNB];
-  bf16x8_t pb[kNB][4];
+  uint32_t pb[kNB][4][4];
   if (ntiles > 0) {
     for (int t = 0; t < kStages - 1; ++t)
       if (t < ntiles) load_tile(t);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
     mma_s(sa, 0);
+    if (tile_masked(0)) apply_mask(sa, kv_lo);
+    update_max(sa);
   }
-  auto step = [&](f32x16_t (&sc)[2][kNB], f32x16_t (&sn)[2][kNB], int i) {
+  auto step = [&](auto mask_next, f32x16_t (&sc)[2][kNB], f32x16_t (&sn)[2][kNB], int i) {
+    constexpr bool MASK_NEXT = decltype(mask_next)::value;
     const int t0 = kv_lo + i * kBK;
     const bool issue = i + kStages - 1 < ntiles;
     if (issue) load_tile(i + kStages - 1);
@@ -312,22 +341,56 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_attn_kernel(
       zero_v_tail(i, t0);
       __syncthreads();
     }
-    if ((t0 + kBK - 1 > wg_min_pos) || (t0 + kBK > L)) apply_mask(sc, t0);
-    update_max(sc);
+    apply_rescale();
+    // phase A
     mma_s(sn, i + 1);  // on the last tile this multiplies stale LDS; the result is unused
     exp_phase(sc, pb);
+    // phase B
     mma_pv(pb, i);
+    row_sum(pb);
+    if constexpr (MASK_NEXT) {
+      if (i + 1 < ntiles) {  // past the key range S(i+1) is stale LDS: never feed it to the max
+        apply_mask(sn, t0 + kBK);
+        update_max(sn);
+      }
+    } else {
+      update_max(sn);  // main-loop steps always have a next tile
+    }
     // the next step reads tile i+2 (K) and i+1 (V): only the loads just issued may be pending
     if (issue) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * NLD * (kStages - 3)) : "memory");
     else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
   };
-  int i = 0;
-  for (; i + 1 < ntiles; i += 2) {
-    step(sa, sb, i);
-    step(sb, sa, i + 1);
+  // first step whose next tile is masked (tile_masked is monotone in the tile index)
+  int n_main = ntiles > 0 ? ntiles - 1 : 0;
+  {
+    int lo = 0, hi = n_main;  // smallest i in [0, n_main) with tile_masked(i + 1), else n_main
+    while (lo < hi) {
+      const int mid = (lo + hi) >> 1;
+      if (tile_masked(mid + 1)) hi = mid; else lo = mid + 1;
+    }
+    n_main = lo;
   }
-  if (i < ntiles) step(sa, sb, i);
+  int i = 0;
+  for (; i + 1 < n_main; i += 2) {
+    step(std::false_type{}, sa, sb, i);
+    step(std::false_type{}, sb, sa, i + 1);
+  }
+  if (i < n_main) {
+    step(std::false_type{}, sa, sb, i);
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+      for (int nb = 0; nb < kNB; ++nb) sa[mb][nb] = sb[mb][nb];
+    ++i;
+  }
+  for (; i < ntiles; ++i) {
+    step(std::true_type{}, sa, sb, i);
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+      for (int nb = 0; nb < kNB; ++nb) sa[mb][nb] = sb[mb][nb];
+  }
 
   // ---- epilogue: O^T register r of block md holds dim 32 md + 8 (r / 4) + 4 hg + r % 4 ------
 #pragma unroll
