@@ -181,10 +181,15 @@ def main():
 
     eng = PrefillEngine(hq, hkv, d, cfg.capacity, cfg.num_phys, cfg.scratch, args.policy, order)
 
+    host_t = {"plan": 0.0, "upload": 0.0, "launch": 0.0, "release": 0.0}
+
     def step(i, ev=None):
         q, kn, vn, out = staged[i]
+        h0 = time.perf_counter()
         plan = eng.plan(tokens[i])
+        h1 = time.perf_counter()
         db = eng.upload(plan)
+        h2 = time.perf_counter()
         if ev is not None:
             ev[0].record()
         eng.scatter(db, kn, vn)
@@ -193,7 +198,14 @@ def main():
         eng.attention(db, q, out)
         if ev is not None:
             ev[2].record()
+        h3 = time.perf_counter()
         eng.release()
+        h4 = time.perf_counter()
+        if ev is not None:
+            host_t["plan"] += h1 - h0
+            host_t["upload"] += h2 - h1
+            host_t["launch"] += h3 - h2
+            host_t["release"] += h4 - h3
         return plan, db
 
     for i in range(n_untimed):
@@ -272,6 +284,7 @@ def main():
             "step_wall": round(wall / steps * 1e3, 4),
             "scatter_gbs": round(scatter_bytes(np.concatenate(S_list), hkv, d)
                                  / max(float(np.sum(t_scatter)), 1e-12) / 1e9, 1),
+            "host_ms": {k: round(v / steps * 1e3, 4) for k, v in host_t.items()},
         },
         "cache": {
             "policy": args.policy,

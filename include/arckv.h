@@ -89,6 +89,13 @@ int32_t arckv_version(void);
  * ------------------------------------------------------------------------------------- */
 int32_t arckv_hash_blocks(const int32_t* tokens, int64_t n_tokens, uint64_t root,
                           uint64_t* out, int64_t out_cap, int64_t* n_full);
+/* The same for n_seqs sequences at once (several chains advance together, which hides the
+ * serial multiply latency).  tokens[r]: n_tokens[r] ids.  out: all identities, sequence after
+ * sequence; offsets (n_seqs + 1 entries, host) receives where each sequence's run starts.
+ * ENOSPC if the total exceeds out_cap (offsets are still filled). */
+int32_t arckv_hash_blocks_batch(const int32_t* const* tokens, const int64_t* n_tokens,
+                                int32_t n_seqs, uint64_t root, uint64_t* out, int64_t out_cap,
+                                int64_t* offsets);
 
 /* ---------------------------------------------------------------------------------------
  * Block cache: ARC(c) or LRU over block identities, with physical placement (host).

@@ -43,6 +43,21 @@ def hash_blocks(tokens, root: int = 0) -> np.ndarray:
     return out
 
 
+def hash_blocks_batch(token_lists, root: int = 0):
+    """Chained identities of several sequences in one call -> list of uint64 arrays (views)."""
+    toks = [np.ascontiguousarray(t, dtype=np.int32) for t in token_lists]
+    n = len(toks)
+    lens = np.array([len(t) for t in toks], dtype=np.int64)
+    ptrs = (_lib.P_i32 * max(n, 1))(*[_ptr(t, _lib.i32) for t in toks])
+    total = int(np.sum(lens // BLOCK_TOKENS))
+    out = np.empty(max(total, 1), dtype=np.uint64)
+    offs = np.empty(n + 1, dtype=np.int64)
+    _lib.check(lib().arckv_hash_blocks_batch(ptrs, _ptr(lens, _lib.i64), n, C.c_uint64(root),
+                                             _ptr(out, _lib.u64), len(out), _ptr(offs, _lib.i64)),
+               "arckv_hash_blocks_batch")
+    return [out[offs[r]:offs[r + 1]] for r in range(n)]
+
+
 def next_batch(n_tokens, max_batch: int, capacity: int, scratch: int) -> int:
     a = np.ascontiguousarray(n_tokens, dtype=np.int64)
     n = _lib.i32()

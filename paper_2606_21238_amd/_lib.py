@@ -49,6 +49,7 @@ _SIGS = {
     "arckv_last_error": (C.c_char_p, []),
     "arckv_version": (i32, []),
     "arckv_hash_blocks": (i32, [P_i32, i64, u64, P_u64, i64, P_i64]),
+    "arckv_hash_blocks_batch": (i32, [C.POINTER(P_i32), P_i64, i32, u64, P_u64, i64, P_i64]),
     "arckv_cache_create": (i32, [C.POINTER(CacheCfg), C.POINTER(vp)]),
     "arckv_cache_destroy": (i32, [vp]),
     "arckv_next_batch": (i32, [P_i64, i32, i32, i64, i64, P_i32]),

@@ -44,3 +44,56 @@ extern "C" int32_t arckv_hash_blocks(const int32_t* tokens, int64_t n_tokens, ui
   }
   return ARCKV_OK;
 }
+
+// Many sequences at once: up to kLanes independent chains advance in lock-step, so the serial
+// xor-multiply latency of one chain overlaps with the others.  Same definition, same result.
+extern "C" int32_t arckv_hash_blocks_batch(const int32_t* const* tokens, const int64_t* n_tokens,
+                                           int32_t n_seqs, uint64_t root, uint64_t* out,
+                                           int64_t out_cap, int64_t* offsets) {
+  constexpr int kLanes = 8;
+  if (n_seqs < 0 || offsets == nullptr || (n_seqs > 0 && (tokens == nullptr || n_tokens == nullptr)))
+    return arckv::fail(ARCKV_EINVAL, "hash_blocks_batch: bad arguments");
+  offsets[0] = 0;
+  for (int32_t r = 0; r < n_seqs; ++r) {
+    if (n_tokens[r] < 0 || (n_tokens[r] > 0 && tokens[r] == nullptr))
+      return arckv::fail(ARCKV_EINVAL, "hash_blocks_batch: sequence %d", r);
+    offsets[r + 1] = offsets[r] + n_tokens[r] / ARCKV_BLOCK_TOKENS;
+  }
+  if (offsets[n_seqs] > out_cap || (offsets[n_seqs] > 0 && out == nullptr))
+    return arckv::fail(ARCKV_ENOSPC, "hash_blocks_batch: %lld blocks, capacity %lld",
+                       (long long)offsets[n_seqs], (long long)out_cap);
+  for (int32_t g = 0; g < n_seqs; g += kLanes) {
+    const int lanes = n_seqs - g < kLanes ? n_seqs - g : kLanes;
+    uint64_t h[kLanes];
+    int64_t nf[kLanes];
+    int64_t most = 0;
+    for (int l = 0; l < kLanes; ++l) {
+      h[l] = root;
+      nf[l] = 0;
+    }
+    for (int l = 0; l < lanes; ++l) {
+      h[l] = root;
+      nf[l] = n_tokens[g + l] / ARCKV_BLOCK_TOKENS;
+      most = nf[l] > most ? nf[l] : most;
+    }
+    for (int64_t i = 0; i < most; ++i) {
+      uint64_t x[kLanes];
+      for (int l = 0; l < kLanes; ++l) x[l] = kFnvOffset;
+      for (int byte = 0; byte < 8; ++byte)
+        for (int l = 0; l < kLanes; ++l) x[l] = mix_byte(x[l], static_cast<uint8_t>(h[l] >> (8 * byte)));
+      for (int t = 0; t < ARCKV_BLOCK_TOKENS; ++t) {
+        uint32_t v[kLanes];
+        for (int l = 0; l < kLanes; ++l)
+          v[l] = (l < lanes && i < nf[l]) ? static_cast<uint32_t>(tokens[g + l][i * ARCKV_BLOCK_TOKENS + t]) : 0u;
+        for (int byte = 0; byte < 4; ++byte)
+          for (int l = 0; l < kLanes; ++l) x[l] = mix_byte(x[l], static_cast<uint8_t>(v[l] >> (8 * byte)));
+      }
+      for (int l = 0; l < lanes; ++l)
+        if (i < nf[l]) {
+          h[l] = x[l];
+          out[offsets[g + l] + i] = x[l];
+        }
+    }
+  }
+  return ARCKV_OK;
+}

@@ -18,12 +18,12 @@
 // ghost list then receives the page); a new page takes the evicted page's physical block or
 // the head of a FIFO free list; partial last blocks use a separate scratch FIFO.
 //
-// Lists are intrusive doubly linked lists over a node array (head = LRU, tail = MRU) with a
-// hash index from identity to node, so every reference is O(1) apart from skipping pinned
-// pages at the LRU end.
+// Lists are intrusive doubly linked lists over a node array (head = LRU, tail = MRU) with an
+// open-addressing index from identity to node (linear probing, backward-shift deletion, no
+// per-entry allocation), so every reference is O(1) apart from skipping pinned pages at the
+// LRU end.
 #include <algorithm>
 #include <deque>
-#include <unordered_map>
 #include <vector>
 
 #include "internal.hpp"
@@ -41,6 +41,52 @@ struct Node {
 struct List {
   int32_t head = -1, tail = -1;  // head = LRU end, tail = MRU end
   int64_t size = 0;
+};
+
+// identity -> node index; at most 2c + 1 live entries, table at least 4x that (power of two)
+class NodeIndex {
+ public:
+  void init(int64_t max_entries) {
+    size_t cap = 16;
+    while (cap < static_cast<size_t>(4 * max_entries + 16)) cap <<= 1;
+    keys_.assign(cap, 0);
+    vals_.assign(cap, -1);
+    mask_ = cap - 1;
+  }
+  int32_t find(uint64_t key) const {
+    for (size_t i = slot(key);; i = (i + 1) & mask_) {
+      if (vals_[i] < 0) return -1;
+      if (keys_[i] == key) return vals_[i];
+    }
+  }
+  void insert(uint64_t key, int32_t val) {  // key absent
+    size_t i = slot(key);
+    while (vals_[i] >= 0) i = (i + 1) & mask_;
+    keys_[i] = key;
+    vals_[i] = val;
+  }
+  void erase(uint64_t key) {  // key present
+    size_t i = slot(key);
+    while (keys_[i] != key || vals_[i] < 0) i = (i + 1) & mask_;
+    // backward-shift: pull later entries of the probe run into the hole
+    for (size_t j = (i + 1) & mask_; vals_[j] >= 0; j = (j + 1) & mask_) {
+      const size_t home = slot(keys_[j]);
+      // entry j may move to the hole i iff its home is not cyclically in (i, j]
+      const bool between = i <= j ? (home > i && home <= j) : (home > i || home <= j);
+      if (!between) {
+        keys_[i] = keys_[j];
+        vals_[i] = vals_[j];
+        i = j;
+      }
+    }
+    vals_[i] = -1;
+  }
+
+ private:
+  size_t slot(uint64_t key) const { return static_cast<size_t>((key * 0x9E3779B97F4A7C15ull) >> 20) & mask_; }
+  std::vector<uint64_t> keys_;
+  std::vector<int32_t> vals_;
+  size_t mask_ = 0;
 };
 
 struct Victim {
@@ -62,7 +108,7 @@ struct arckv_cache {
   List lists[5];
   std::vector<Node> nodes;
   std::vector<int32_t> free_nodes;
-  std::unordered_map<uint64_t, int32_t> index;
+  NodeIndex index;
   std::deque<int32_t> free_blocks;
   std::deque<int32_t> scratch_fifo;
   std::vector<int32_t> batch_scratch;
@@ -106,7 +152,7 @@ struct arckv_cache {
     x = Node();
     x.key = key;
     x.phys = phys;
-    index[key] = n;
+    index.insert(key, n);
     return n;
   }
   void erase_node(int32_t n) {
@@ -121,8 +167,7 @@ struct arckv_cache {
     return -1;
   }
   int32_t find(uint64_t key) const {
-    auto it = index.find(key);
-    return it == index.end() ? -1 : it->second;
+    return index.find(key);
   }
   bool resident(uint64_t key) const {
     const int32_t n = find(key);
@@ -317,7 +362,7 @@ extern "C" int32_t arckv_cache_create(const arckv_cache_cfg* cfg, arckv_cache** 
   c->free_blocks.assign(order.begin(), order.begin() + n_pages);
   c->scratch_fifo.assign(order.begin() + n_pages, order.end());
   c->nodes.reserve(static_cast<size_t>(2 * c->c + 8));
-  c->index.reserve(static_cast<size_t>(2 * c->c + 8));
+  c->index.init(2 * c->c + 8);
   *out = c;
   return ARCKV_OK;
 }

@@ -12,7 +12,7 @@ from dataclasses import dataclass
 
 import numpy as np
 
-from . import (BlockCache, BatchPlan, attention_plan, hash_blocks, kv_scatter, prefill_attention)
+from . import (BlockCache, BatchPlan, attention_plan, hash_blocks_batch, kv_scatter, prefill_attention)
 
 
 @dataclass
@@ -48,11 +48,17 @@ class PrefillEngine:
             num_cus = torch.cuda.get_device_properties(self.device).multi_processor_count
         self.num_cus = int(num_cus)
         self._ws = torch.empty(0, dtype=torch.uint8, device=self.device)
+        # two reusable pinned staging buffers (one may still feed an in-flight copy) and the
+        # events that mark their copies done; allocating pinned memory per batch would stall
+        self._stage = [None, None]
+        self._stage_ev = [None, None]
+        self._dev_meta = [None, None]
+        self._turn = 0
 
     # ---- host steps ----------------------------------------------------------------------
     def plan(self, token_lists) -> BatchPlan:
-        reqs = [(hash_blocks(t), len(t)) for t in token_lists]
-        return self.cache.plan_batch(reqs)
+        hashes = hash_blocks_batch(token_lists)
+        return self.cache.plan_batch([(h, len(t)) for h, t in zip(hashes, token_lists)])
 
     def release(self):
         self.cache.release_batch()
@@ -60,10 +66,26 @@ class PrefillEngine:
     def upload(self, plan: BatchPlan, stream=None) -> DeviceBatch:
         import torch
         ap = attention_plan(plan.cu_q, plan.seq_lens, self.hq, self.hkv, self.d, self.num_cus)
-        host = np.concatenate([plan.block_tables.ravel(), plan.cu_q, plan.seq_lens, plan.slot_mapping,
-                               ap.work.ravel()]).astype(np.int32)
-        pinned = torch.from_numpy(host).pin_memory()
-        dev = pinned.to(self.device, non_blocking=True)
+        parts = [plan.block_tables.ravel(), plan.cu_q, plan.seq_lens, plan.slot_mapping, ap.work.ravel()]
+        n_int = sum(p.size for p in parts)
+        t = self._turn
+        self._turn ^= 1
+        if self._stage_ev[t] is not None:
+            self._stage_ev[t].synchronize()          # the copy that last read this buffer is done
+        if self._stage[t] is None or self._stage[t].numel() < n_int:
+            cap = max(n_int, 1 << 16) * 2
+            self._stage[t] = torch.empty(cap, dtype=torch.int32, pin_memory=True)
+            self._dev_meta[t] = torch.empty(cap, dtype=torch.int32, device=self.device)
+        host = self._stage[t].numpy()
+        o = 0
+        for p in parts:
+            host[o:o + p.size] = p
+            o += p.size
+        dev = self._dev_meta[t][:n_int]
+        dev.copy_(self._stage[t][:n_int], non_blocking=True)
+        ev = torch.cuda.Event()
+        ev.record()
+        self._stage_ev[t] = ev
         n = plan.n_reqs
         o = 0
         bt = dev[o:o + plan.block_tables.size].view(n, plan.block_tables.shape[1]); o += plan.block_tables.size

@@ -25,6 +25,10 @@ def test_hash_matches_oracle():
         assert [int(x) for x in ak.hash_blocks(s, root=12345)] == obh.hash_blocks(s, root=12345)
     neg = np.array([-1, -(2 ** 31)] + [7] * 14, dtype=np.int32)
     assert [int(x) for x in ak.hash_blocks(neg)] == obh.hash_blocks(neg)
+    # the multi-sequence entry point (lock-step chains) gives the same identities
+    many = seqs + [neg] + [rng.integers(0, 128256, n).astype(np.int32) for n in range(0, 400, 37)]
+    got = ak.hash_blocks_batch(many, root=5)
+    assert [[int(x) for x in g] for g in got] == [obh.hash_blocks(s, root=5) for s in many]
 
 
 class Pair:
