@@ -227,36 +227,38 @@ int32_t arckv_kv_scatter(void* k_pool, void* v_pool, const void* k_new, const vo
  * num_kv_heads); K/V read through the block table.  bf16 in, fp32 accumulate, bf16 out.
  * ------------------------------------------------------------------------------------- */
 
-/* Work decomposition (host): one work item is a query tile of arckv_attention_tile_cols() (column = token x
+/* Work decomposition (host): one work item is a query tile of *tile_cols (column = token x
  * query head of one KV group, token-major) of one (request, KV head) over a key range.
  * Long key ranges are split when the batch has too few tiles to fill num_cus compute units;
  * split tiles are merged by a log-sum-exp combine pass.
  * cu_q, seq_lens: HOST copies of the plan's arrays.  work: host int32 buffer of
  * ARCKV_WORK_INTS * work_cap entries or NULL to query sizes.
  * Outputs: *n_work attention items, *n_combine combine items (both stored in work, the
- * combine items after the attention items), *ws_bytes device workspace needed.
+ * combine items after the attention items), *ws_bytes device workspace needed, *tile_cols
+ * the tile width (256, or 128 when every request has at most 128 columns).
  * ENOSPC if n_work + n_combine > work_cap (sizes still reported). */
 #define ARCKV_WORK_INTS 8
-/* Query columns per attention work item (the tile width the plan and the kernel share). */
-int32_t arckv_attention_tile_cols(void);
 int32_t arckv_attention_plan(const int32_t* cu_q, const int32_t* seq_lens, int32_t n_reqs,
                              int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
                              int32_t num_cus, int32_t* work, int64_t work_cap,
-                             int64_t* n_work, int64_t* n_combine, int64_t* ws_bytes);
+                             int64_t* n_work, int64_t* n_combine, int64_t* ws_bytes,
+                             int32_t* tile_cols);
 
 /* Runs attention for one planned batch.
  * k_pool, v_pool: device, layout V1 (num_blocks blocks).  q: device bf16
  * [n_q][num_q_heads][head_dim], rows ordered by cu_q.  out: device bf16, same shape.
  * block_tables: device int32 [n_reqs][bt_stride]; cu_q: device [n_reqs + 1]; seq_lens:
  * device [n_reqs] (the same values given to arckv_attention_plan).  work: device copy of
- * the plan's items.  workspace: device, >= the planned ws_bytes (may be NULL if 0).
+ * the plan's items, tile_cols: the plan's tile width.  workspace: device, >= the planned
+ * ws_bytes (may be NULL if 0).
  * Block-table entries outside [0, num_blocks) are read as zero keys/values.
  * head_dim in {64, 128}; num_q_heads / num_kv_heads in {1, 2, 4, 8}. */
 int32_t arckv_prefill_attention(const void* k_pool, const void* v_pool, const void* q, void* out,
                                 const int32_t* block_tables, int32_t bt_stride,
                                 const int32_t* cu_q, const int32_t* seq_lens, int32_t n_reqs,
                                 int64_t n_q, int64_t num_blocks, const int32_t* work,
-                                int64_t n_work, int64_t n_combine, int32_t num_q_heads,
+                                int64_t n_work, int64_t n_combine, int32_t tile_cols,
+                                int32_t num_q_heads,
                                 int32_t num_kv_heads, int32_t head_dim, float scale,
                                 void* workspace, int64_t ws_bytes, void* stream);
 

@@ -221,30 +221,29 @@ class AttnPlan:
     n_work: int
     n_combine: int
     ws_bytes: int
-
-
-def attention_tile_cols() -> int:
-    return int(lib().arckv_attention_tile_cols())
+    tile_cols: int       # query columns per work item (256, or 128 for short suffixes)
 
 
 def attention_plan(cu_q, seq_lens, num_q_heads: int, num_kv_heads: int, head_dim: int,
                    num_cus: int = 256) -> AttnPlan:
     cu = np.ascontiguousarray(cu_q, dtype=np.int32)
     sl = np.ascontiguousarray(seq_lens, dtype=np.int32)
-    nw, nc, ws = _lib.i64(), _lib.i64(), _lib.i64()
+    nw, nc, ws, tc = _lib.i64(), _lib.i64(), _lib.i64(), _lib.i32()
     L = lib()
     _lib.check(L.arckv_attention_plan(_ptr(cu, _lib.i32), _ptr(sl, _lib.i32), len(sl), num_q_heads,
                                       num_kv_heads, head_dim, num_cus, None, 0, C.byref(nw), C.byref(nc),
-                                      C.byref(ws)), "arckv_attention_plan")
+                                      C.byref(ws), C.byref(tc)), "arckv_attention_plan")
     work = np.zeros((max(nw.value + nc.value, 1), WORK_INTS), dtype=np.int32)
     _lib.check(L.arckv_attention_plan(_ptr(cu, _lib.i32), _ptr(sl, _lib.i32), len(sl), num_q_heads,
                                       num_kv_heads, head_dim, num_cus, _ptr(work, _lib.i32), len(work),
-                                      C.byref(nw), C.byref(nc), C.byref(ws)), "arckv_attention_plan")
-    return AttnPlan(work, int(nw.value), int(nc.value), int(ws.value))
+                                      C.byref(nw), C.byref(nc), C.byref(ws), C.byref(tc)),
+               "arckv_attention_plan")
+    return AttnPlan(work, int(nw.value), int(nc.value), int(ws.value), int(tc.value))
 
 
 def prefill_attention(k_pool, v_pool, q, out, block_tables, cu_q, seq_lens, work, n_work: int,
-                      n_combine: int, scale: float, workspace=None, ws_bytes: int = 0, stream=None):
+                      n_combine: int, tile_cols: int, scale: float, workspace=None, ws_bytes: int = 0,
+                      stream=None):
     """Device tensors: pools (layout V1), q/out [n_q, Hq, D] bf16, block_tables [n, stride] int32,
     cu_q [n+1], seq_lens [n], work [n_work + n_combine, 8] int32, workspace (bytes >= ws_bytes)."""
     n_q, hq, d = int(q.shape[0]), int(q.shape[1]), int(q.shape[2])
@@ -265,5 +264,6 @@ def prefill_attention(k_pool, v_pool, q, out, block_tables, cu_q, seq_lens, work
         _dev(k_pool, 16, "k_pool"), _dev(v_pool, 16, "v_pool"), _dev(q, 16, "q"), _dev(out, 16, "out"),
         _dev(block_tables, 32, "block_tables"), int(block_tables.shape[1]), _dev(cu_q, 32, "cu_q"),
         _dev(seq_lens, 32, "seq_lens"), int(seq_lens.shape[0]), n_q, int(k_pool.shape[0]),
-        _dev(work, 32, "work"), n_work, n_combine, hq, hkv, d, float(scale), ws, int(ws_bytes),
+        _dev(work, 32, "work"), n_work, n_combine, int(tile_cols), hq, hkv, d, float(scale), ws,
+        int(ws_bytes),
         C.c_void_p(_stream(stream))), "arckv_prefill_attention")

@@ -1,13 +1,15 @@
 // Work decomposition of prefix-cached prefill attention (host side).
 //
-// A work item covers one query tile of kTileCols "columns" of one (request, KV head): column
+// A work item covers one query tile of `cols` "columns" of one (request, KV head): column
 // c = token * G + g (G query heads share a KV head, token-major), so the K/V tiles a work
 // item streams serve all G heads of its group at once.  The key range of a tile ends at the
 // last visible key of its last column (causal: suffix token i of a request with P cached
-// tokens sees keys 0..P+i).  When a batch has too few tiles to give every compute unit a
-// couple of work items (short suffixes over long cached prefixes), tiles are split along the
-// key range into chunks of >= 256 keys; split tiles write fp32 partials plus a base-2
-// log-sum-exp, merged afterwards by one combine item per tile.
+// tokens sees keys 0..P+i).  Tiles are 256 columns wide, or 128 when no request of the batch
+// has more than 128 columns (short suffixes), so that no work-group computes on empty
+// columns.  When a batch has fewer tiles than compute units (short suffixes over long cached
+// prefixes), tiles are split along the key range into about one item per compute unit, at
+// least 512 keys each; split tiles write fp32 partials plus a base-2 log-sum-exp, merged
+// afterwards by one combine item per tile.
 //
 // Items are ordered longest key range first so the longest ones start first, and the order
 // is interleaved over the 8 XCDs (work-groups are dispatched round-robin over XCDs, each with
@@ -21,7 +23,6 @@
 
 namespace {
 
-constexpr int kCols = arckv::kTileCols;  // query columns per work-group
 constexpr int kKeyTile = 64;  // keys per K/V tile (split boundaries are multiples of this)
 constexpr int kXcds = 8;      // MI355X: 8 XCDs; dispatch round-robins work-groups over them
 
@@ -33,14 +34,13 @@ struct Item {
 
 }  // namespace
 
-extern "C" int32_t arckv_attention_tile_cols(void) { return kCols; }
-
 extern "C" int32_t arckv_attention_plan(const int32_t* cu_q, const int32_t* seq_lens,
                                         int32_t n_reqs, int32_t num_q_heads, int32_t num_kv_heads,
                                         int32_t head_dim, int32_t num_cus, int32_t* work,
                                         int64_t work_cap, int64_t* n_work, int64_t* n_combine,
-                                        int64_t* ws_bytes) {
-  if (n_work == nullptr || n_combine == nullptr || ws_bytes == nullptr || n_reqs < 0 ||
+                                        int64_t* ws_bytes, int32_t* tile_cols) {
+  if (n_work == nullptr || n_combine == nullptr || ws_bytes == nullptr || tile_cols == nullptr ||
+      n_reqs < 0 ||
       (n_reqs > 0 && (cu_q == nullptr || seq_lens == nullptr)) || num_cus < 1 ||
       num_kv_heads < 1 || num_q_heads < 1)
     return arckv::fail(ARCKV_EINVAL, "attention_plan: bad arguments");
@@ -52,6 +52,12 @@ extern "C" int32_t arckv_attention_plan(const int32_t* cu_q, const int32_t* seq_
   if (head_dim != 64 && head_dim != 128)
     return arckv::fail(ARCKV_EUNSUPPORTED, "attention_plan: head_dim %d not in {64,128}", head_dim);
   if (n_reqs > 0 && cu_q[0] != 0) return arckv::fail(ARCKV_EINVAL, "attention_plan: cu_q[0] != 0");
+
+  int64_t max_cols = 0;
+  for (int32_t r = 0; r < n_reqs; ++r)
+    max_cols = std::max<int64_t>(max_cols, (static_cast<int64_t>(cu_q[r + 1]) - cu_q[r]) * G);
+  const int kCols = max_cols <= arckv::kNarrowCols ? arckv::kNarrowCols : arckv::kWideCols;
+  *tile_cols = kCols;
 
   struct Tile { int32_t req, kvh, col_start, kv_end; };
   std::vector<Tile> tiles;
@@ -72,11 +78,11 @@ extern "C" int32_t arckv_attention_plan(const int32_t* cu_q, const int32_t* seq_
     }
   }
   const int64_t base = static_cast<int64_t>(tiles.size());
-  const int64_t target = 2 * static_cast<int64_t>(num_cus);
+  const int64_t target = static_cast<int64_t>(num_cus);  // one work-group per CU at a time
   int64_t chunk = INT32_MAX;
   if (base > 0 && base < target) {
     const int64_t want = (total_keys + target - 1) / target;
-    chunk = std::max<int64_t>(256, (want + kKeyTile - 1) / kKeyTile * kKeyTile);
+    chunk = std::max<int64_t>(512, (want + kKeyTile - 1) / kKeyTile * kKeyTile);
   }
 
   std::vector<Item> items, combines;

@@ -8,7 +8,8 @@
 // Sec. 4; layout V1: K [blk][kvh][16][D], V [blk][kvh][D][16]).
 //
 // Design (MI355X-first):
-//  * One work-group = 4 wave64s = one kTileCols-column query tile of one (request, KV head); a
+//  * One work-group = 8 (or, for short suffixes, 4) wave64s = one query tile of one (request,
+//    KV head); a
 //    column is (token, head-of-group), token-major, so every K/V tile a work-group loads
 //    serves all G query heads of its KV head (GQA packed into the MFMA N dimension).
 //  * Transposed formulation: S^T = K . Q^T and O^T = V^T . P^T with v_mfma_f32_32x32x16_bf16.
@@ -47,9 +48,7 @@ typedef float f32x2_t __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void lds_void;
 
-constexpr int kThreads = 64 * arckv::kTileWaves;  // one work-group per CU, two waves per SIMD
 constexpr int kNB = arckv::kWaveCols / 32;         // 32-column MFMA blocks per wave
-constexpr int kCols = arckv::kTileCols;            // query columns per work-group
 constexpr int kStages = 4;                         // K/V tiles resident in LDS (ring)
 constexpr int kBK = 64;        // keys per K/V tile (4 blocks of 16)
 constexpr float kLazy = 8.0f;  // rescale O only when a column max grows by > 2^8
@@ -77,14 +76,18 @@ __device__ __forceinline__ void load_lds16(const void* g, lds_void* l) {
   __builtin_amdgcn_global_load_lds(g, l, 16, 0, 0);
 }
 
-template <int D, int G>
-__global__ __launch_bounds__(kThreads, 1) void prefill_attn_kernel(
+// NW waves (32 query columns each) per work-group: 8 (wide tiles, two waves per SIMD) or 4
+// (narrow tiles for short suffixes); one work-group per CU either way (the K/V ring fills LDS).
+template <int D, int G, int NW>
+__global__ __launch_bounds__(64 * NW, 1) void prefill_attn_kernel(
     const uint16_t* __restrict__ k_pool, const uint16_t* __restrict__ v_pool,
     const uint16_t* __restrict__ q, uint16_t* __restrict__ out,
     const int32_t* __restrict__ block_tables, int bt_stride,
     const int32_t* __restrict__ cu_q, const int32_t* __restrict__ seq_lens, int n_reqs,
     const Work* __restrict__ work, int64_t n_q, int64_t num_blocks, int hq, int hkv,
     float scale_log2, float* __restrict__ ws_o, float* __restrict__ ws_lse, int64_t ws_slots) {
+  constexpr int kThreads = 64 * NW;
+  constexpr int kCols = NW * arckv::kWaveCols;   // query columns of the work-group
   constexpr int KSTEPS = D / 16;                 // k-steps of Q.K^T
   constexpr int DM = D / 32;                     // 32-row blocks of O^T
   constexpr int TILE = kBK * D * 2;              // bytes of one K (or V) tile
@@ -410,7 +413,7 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_attn_kernel(
           for (int j = 0; j < 4; ++j) v[j] = o[md][nb][4 * r4 + j] * inv;
           *reinterpret_cast<bf16x4_t*>(dst + md * 32 + 8 * r4 + 4 * hg) = __builtin_convertvector(v, bf16x4_t);
         }
-    } else if (w.slot < ws_slots) {
+    } else if (w.slot < ws_slots && cval[nb]) {
       float* po = ws_o + (static_cast<int64_t>(w.slot) * kCols + local) * D;
 #pragma unroll
       for (int md = 0; md < DM; ++md)
@@ -429,10 +432,13 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_attn_kernel(
 }
 
 // Merges the key-range splits of one query tile: o = sum_s 2^lse_s O_s / sum_s 2^lse_s.
+// Grid: (combine items, kCombineSplit); block y handles every kCombineSplit-th column.
+constexpr int kCombineThreads = 256;
+constexpr int kCombineSplit = 8;
 template <int D>
-__global__ __launch_bounds__(kThreads) void attn_combine_kernel(
+__global__ __launch_bounds__(kCombineThreads) void attn_combine_kernel(
     uint16_t* __restrict__ out, const Work* __restrict__ items, const int32_t* __restrict__ cu_q,
-    int n_reqs, int64_t n_q, int hq, int G, const float* __restrict__ ws_o,
+    int n_reqs, int64_t n_q, int hq, int G, int tile_cols, const float* __restrict__ ws_o,
     const float* __restrict__ ws_lse, int64_t ws_slots) {
   const Work w = items[blockIdx.x];  // {req, kvh, col_start, slot0, n_splits}
   const int slot0 = w.kv_start, ns = w.kv_end;
@@ -442,23 +448,26 @@ __global__ __launch_bounds__(kThreads) void attn_combine_kernel(
   const int q0 = cu_q[w.req];
   const int ncols = (cu_q[w.req + 1] - q0) * G;
   constexpr int D4 = D / 4;
-  for (int e = threadIdx.x; e < kCols * D4; e += kThreads) {
-    const int local = e / D4, d4 = e % D4;
+  const int my_cols = (tile_cols + kCombineSplit - 1) / kCombineSplit;
+  for (int e = threadIdx.x; e < my_cols * D4; e += kCombineThreads) {
+    const int local = (e / D4) * kCombineSplit + blockIdx.y, d4 = e % D4;
     const int col = w.col_start + local;
-    if (col >= ncols) continue;
+    if (local >= tile_cols || col >= ncols) continue;
     const int tok = col / G, g = col % G;
     if (q0 + tok >= n_q) continue;
     float m = -INFINITY;
-    for (int s = 0; s < ns; ++s) m = fmaxf(m, ws_lse[static_cast<int64_t>(slot0 + s) * kCols + local]);
+    for (int s = 0; s < ns; ++s) m = fmaxf(m, ws_lse[static_cast<int64_t>(slot0 + s) * tile_cols + local]);
     f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
     float wsum = 0.f;
     for (int s = 0; s < ns; ++s) {
-      const float lse = ws_lse[static_cast<int64_t>(slot0 + s) * kCols + local];
+      const float lse = ws_lse[static_cast<int64_t>(slot0 + s) * tile_cols + local];
       const float wt = lse == -INFINITY ? 0.f : fast_exp2(lse - m);
       wsum += wt;
-      const f32x4_t v = *reinterpret_cast<const f32x4_t*>(
-          ws_o + (static_cast<int64_t>(slot0 + s) * kCols + local) * D + 4 * d4);
-      acc += wt * v;
+      if (wt > 0.f) {
+        const f32x4_t v = *reinterpret_cast<const f32x4_t*>(
+            ws_o + (static_cast<int64_t>(slot0 + s) * tile_cols + local) * D + 4 * d4);
+        acc += wt * v;
+      }
     }
     const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
     const bf16x4_t b = __builtin_convertvector(acc * inv, bf16x4_t);
@@ -466,13 +475,13 @@ __global__ __launch_bounds__(kThreads) void attn_combine_kernel(
   }
 }
 
-template <int D, int G>
+template <int D, int G, int NW>
 void launch_attn(dim3 grid, hipStream_t st, const uint16_t* kp, const uint16_t* vp,
                  const uint16_t* q, uint16_t* out, const int32_t* bt, int bt_stride,
                  const int32_t* cu_q, const int32_t* seq_lens, int n_reqs, const Work* work,
                  int64_t n_q, int64_t num_blocks, int hq, int hkv, float scale_log2, float* ws_o,
                  float* ws_lse, int64_t ws_slots) {
-  hipLaunchKernelGGL((prefill_attn_kernel<D, G>), grid, dim3(kThreads), 0, st, kp, vp, q, out,
+  hipLaunchKernelGGL((prefill_attn_kernel<D, G, NW>), grid, dim3(64 * NW), 0, st, kp, vp, q, out,
                      bt, bt_stride, cu_q, seq_lens, n_reqs, work, n_q, num_blocks, hq, hkv,
                      scale_log2, ws_o, ws_lse, ws_slots);
 }
@@ -484,7 +493,7 @@ extern "C" int32_t arckv_prefill_attention(const void* k_pool, const void* v_poo
                                            int32_t bt_stride, const int32_t* cu_q,
                                            const int32_t* seq_lens, int32_t n_reqs, int64_t n_q,
                                            int64_t num_blocks, const int32_t* work,
-                                           int64_t n_work, int64_t n_combine,
+                                           int64_t n_work, int64_t n_combine, int32_t tile_cols,
                                            int32_t num_q_heads, int32_t num_kv_heads,
                                            int32_t head_dim, float scale, void* workspace,
                                            int64_t ws_bytes, void* stream) {
@@ -497,18 +506,20 @@ extern "C" int32_t arckv_prefill_attention(const void* k_pool, const void* v_poo
     return arckv::fail(ARCKV_EUNSUPPORTED, "prefill_attention: head_dim %d not in {64,128}", head_dim);
   if (G != 1 && G != 2 && G != 4 && G != 8)
     return arckv::fail(ARCKV_EUNSUPPORTED, "prefill_attention: group size %d not in {1,2,4,8}", G);
+  if (tile_cols != arckv::kWideCols && tile_cols != arckv::kNarrowCols)
+    return arckv::fail(ARCKV_EINVAL, "prefill_attention: tile_cols %d is not a planned width", tile_cols);
   if (n_work == 0 && n_combine == 0) return ARCKV_OK;
   if (k_pool == nullptr || v_pool == nullptr || q == nullptr || out == nullptr ||
       block_tables == nullptr || cu_q == nullptr || seq_lens == nullptr || work == nullptr)
     return arckv::fail(ARCKV_EINVAL, "prefill_attention: NULL pointer");
   if (n_work > INT32_MAX || n_combine > INT32_MAX)
     return arckv::fail(ARCKV_EINVAL, "prefill_attention: too many work items");
-  const int64_t slot_bytes = static_cast<int64_t>(kCols) * (head_dim + 1) * 4;
+  const int64_t slot_bytes = static_cast<int64_t>(tile_cols) * (head_dim + 1) * 4;
   const int64_t ws_slots = workspace != nullptr ? ws_bytes / slot_bytes : 0;
   if (n_combine > 0 && ws_slots == 0)
     return arckv::fail(ARCKV_EINVAL, "prefill_attention: split plan needs a workspace");
   float* ws_o = static_cast<float*>(workspace);
-  float* ws_lse = ws_o == nullptr ? nullptr : ws_o + ws_slots * kCols * head_dim;
+  float* ws_lse = ws_o == nullptr ? nullptr : ws_o + ws_slots * tile_cols * head_dim;
   auto* st = static_cast<hipStream_t>(stream);
   auto* kp = static_cast<const uint16_t*>(k_pool);
   auto* vp = static_cast<const uint16_t*>(v_pool);
@@ -520,9 +531,16 @@ extern "C" int32_t arckv_prefill_attention(const void* k_pool, const void* v_poo
   if (n_work > 0) {
     const dim3 grid(static_cast<unsigned>(n_work));
 #define ARCKV_LAUNCH(DD, GG)                                                                   \
-  launch_attn<DD, GG>(grid, st, kp, vp, qp, op, block_tables, bt_stride, cu_q, seq_lens,       \
-                      n_reqs, wk, n_q, num_blocks, num_q_heads, num_kv_heads, scale_log2,      \
-                      ws_o, ws_lse, ws_slots)
+  do {                                                                                         \
+    if (tile_cols == arckv::kWideCols)                                                         \
+      launch_attn<DD, GG, 8>(grid, st, kp, vp, qp, op, block_tables, bt_stride, cu_q, seq_lens, \
+                             n_reqs, wk, n_q, num_blocks, num_q_heads, num_kv_heads,           \
+                             scale_log2, ws_o, ws_lse, ws_slots);                              \
+    else                                                                                       \
+      launch_attn<DD, GG, 4>(grid, st, kp, vp, qp, op, block_tables, bt_stride, cu_q, seq_lens, \
+                             n_reqs, wk, n_q, num_blocks, num_q_heads, num_kv_heads,           \
+                             scale_log2, ws_o, ws_lse, ws_slots);                              \
+  } while (0)
     if (head_dim == 64) {
       switch (G) {
         case 1: ARCKV_LAUNCH(64, 1); break;
@@ -544,14 +562,14 @@ extern "C" int32_t arckv_prefill_attention(const void* k_pool, const void* v_poo
       return arckv::fail(ARCKV_EDEVICE, "prefill_attention: %s", hipGetErrorString(e));
   }
   if (n_combine > 0) {
-    const dim3 grid(static_cast<unsigned>(n_combine));
+    const dim3 grid(static_cast<unsigned>(n_combine), kCombineSplit);
     const Work* items = wk + n_work;
     if (head_dim == 64)
-      hipLaunchKernelGGL(attn_combine_kernel<64>, grid, dim3(kThreads), 0, st, op, items, cu_q,
-                         n_reqs, n_q, num_q_heads, G, ws_o, ws_lse, ws_slots);
+      hipLaunchKernelGGL(attn_combine_kernel<64>, grid, dim3(kCombineThreads), 0, st, op, items,
+                         cu_q, n_reqs, n_q, num_q_heads, G, tile_cols, ws_o, ws_lse, ws_slots);
     else
-      hipLaunchKernelGGL(attn_combine_kernel<128>, grid, dim3(kThreads), 0, st, op, items, cu_q,
-                         n_reqs, n_q, num_q_heads, G, ws_o, ws_lse, ws_slots);
+      hipLaunchKernelGGL(attn_combine_kernel<128>, grid, dim3(kCombineThreads), 0, st, op, items,
+                         cu_q, n_reqs, n_q, num_q_heads, G, tile_cols, ws_o, ws_lse, ws_slots);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess)
       return arckv::fail(ARCKV_EDEVICE, "attn_combine: %s", hipGetErrorString(e));

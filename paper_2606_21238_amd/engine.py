@@ -26,6 +26,7 @@ class DeviceBatch:
     n_work: int
     n_combine: int
     ws_bytes: int
+    tile_cols: int
 
 
 class PrefillEngine:
@@ -95,7 +96,7 @@ class PrefillEngine:
         wk = dev[o:o + ap.work.size].view(-1, 8)
         if ap.ws_bytes > self._ws.numel():
             self._ws = torch.empty(ap.ws_bytes, dtype=torch.uint8, device=self.device)
-        return DeviceBatch(plan, bt, cu, sl, sm, wk, ap.n_work, ap.n_combine, ap.ws_bytes)
+        return DeviceBatch(plan, bt, cu, sl, sm, wk, ap.n_work, ap.n_combine, ap.ws_bytes, ap.tile_cols)
 
     # ---- device steps --------------------------------------------------------------------
     def scatter(self, db: DeviceBatch, k_new, v_new, stream=None):
@@ -103,7 +104,7 @@ class PrefillEngine:
 
     def attention(self, db: DeviceBatch, q, out, stream=None):
         prefill_attention(self.k_pool, self.v_pool, q, out, db.block_tables, db.cu_q, db.seq_lens,
-                          db.work, db.n_work, db.n_combine, self.scale,
+                          db.work, db.n_work, db.n_combine, db.tile_cols, self.scale,
                           self._ws if db.ws_bytes else None, db.ws_bytes, stream)
 
     def step(self, token_lists, qkv_for_plan, stream=None):

@@ -40,10 +40,13 @@ def test_device_calls_validate_arguments_without_touching_a_device():
     # unsupported head_dim / group size are refused before any launch
     assert L.arckv_kv_scatter(None, None, None, None, None, 4, 4, 2, 96, None) == _lib.EUNSUPPORTED
     assert L.arckv_prefill_attention(None, None, None, None, None, 1, None, None, 1, 1, 1, None, 1, 0,
-                                     12, 4, 128, 0.1, None, 0, None) == _lib.EUNSUPPORTED
+                                     256, 12, 4, 128, 0.1, None, 0, None) == _lib.EUNSUPPORTED
     assert L.arckv_prefill_attention(None, None, None, None, None, 1, None, None, 1, 1, 1, None, 1, 0,
-                                     8, 4, 128, 0.1, None, 0, None) == _lib.EINVAL
+                                     256, 8, 4, 128, 0.1, None, 0, None) == _lib.EINVAL
     assert b"NULL" in L.arckv_last_error()
+    assert L.arckv_prefill_attention(None, None, None, None, None, 1, None, None, 1, 1, 1, None, 1, 0,
+                                     200, 8, 4, 128, 0.1, None, 0, None) == _lib.EINVAL
+    assert b"tile_cols" in L.arckv_last_error()
     # nothing to do is a no-op
     assert L.arckv_kv_scatter(None, None, None, None, None, 0, 4, 2, 64, None) == _lib.OK
 

@@ -110,7 +110,7 @@ def run_attention(b, hq, hkv, d, num_cus=256, table_override=None, kp=None, vp=N
     ak.prefill_attention(b["kp"] if kp is None else kp, b["vp"] if vp is None else vp, b["q"], out,
                          torch.from_numpy(bt).to(DEV), torch.from_numpy(b["cu"]).to(DEV),
                          torch.from_numpy(b["seq"]).to(DEV), torch.from_numpy(ap.work).to(DEV),
-                         ap.n_work, ap.n_combine, d ** -0.5, ws, ap.ws_bytes)
+                         ap.n_work, ap.n_combine, ap.tile_cols, d ** -0.5, ws, ap.ws_bytes)
     torch.cuda.synchronize()
     return bits(out), ap
 
@@ -142,7 +142,7 @@ def test_attention_sweep(case, num_cus):
     got, ap = run_attention(b, hq, hkv, d, num_cus)
     ref = oracle_out(b, hq, hkv, d)
     compare(got, ref, f"case {case}")
-    if num_cus > 1000 and max(L for L, _ in reqs) > 256:
+    if num_cus > 1000 and max(L for L, _ in reqs) > 512:   # splits are >= 512 keys
         assert ap.n_combine > 0
 
 
@@ -281,6 +281,6 @@ def test_empty_work_is_a_noop():
     out = torch.zeros_like(b["q"])
     ak.prefill_attention(b["kp"], b["vp"], b["q"], out, torch.from_numpy(b["bt"]).to(DEV),
                          torch.from_numpy(b["cu"]).to(DEV), torch.from_numpy(b["seq"]).to(DEV),
-                         torch.zeros((1, 8), dtype=torch.int32, device=DEV), 0, 0, 0.125)
+                         torch.zeros((1, 8), dtype=torch.int32, device=DEV), 0, 0, 256, 0.125)
     torch.cuda.synchronize()
     assert int(out.abs().sum()) == 0

@@ -187,7 +187,9 @@ def test_error_statuses_match_the_oracle():
 def attention_plan_coverage(cu_q, seq_lens, hq, hkv, d, num_cus):
     ap = ak.attention_plan(cu_q, seq_lens, hq, hkv, d, num_cus)
     g = hq // hkv
-    tc = ak.attention_tile_cols()
+    tc = ap.tile_cols
+    max_cols = max(int(cu_q[r + 1] - cu_q[r]) * g for r in range(len(seq_lens)))
+    assert tc == (128 if max_cols <= 128 else 256)
     items = ap.work[: ap.n_work]
     comb = ap.work[ap.n_work: ap.n_work + ap.n_combine]
     cover = {}
