@@ -29,25 +29,30 @@ def new_pool(num_blocks: int, num_kv_heads: int, head_dim: int, fill: int = 0xFF
 
 
 def scatter(k_pool, v_pool, k_new, v_new, slots) -> None:
-    """Write token t's K/V rows ([Hkv, D] bf16 bits) into slot ``slots[t]`` (in place)."""
+    """Write token t's K/V rows ([Hkv, D] bf16 bits) into slot ``slots[t]`` (in place).
+
+    blk = slot // 16, off = slot % 16; K goes to k_pool[blk, :, off, :], V to
+    v_pool[blk, :, :, off] (numpy fancy-index assignment, one element per token and head)."""
     k_new = np.asarray(k_new, dtype=np.uint16)
     v_new = np.asarray(v_new, dtype=np.uint16)
-    for t, s in enumerate(slots):
-        blk, off = divmod(int(s), BLOCK_TOKENS)
-        k_pool[blk, :, off, :] = k_new[t]
-        v_pool[blk, :, :, off] = v_new[t]
+    slots = np.asarray(slots, dtype=np.int64)
+    if slots.size == 0:
+        return
+    blk, off = slots // BLOCK_TOKENS, slots % BLOCK_TOKENS
+    k_pool[blk, :, off, :] = k_new
+    # advanced indices (blk, off) separated by slices put the token axis first: [T, Hkv, D]
+    v_pool[blk, :, :, off] = v_new
 
 
 def gather(k_pool, v_pool, table_row, n_tokens: int):
-    """Contiguous K, V ([n_tokens, Hkv, D] bf16 bits) of one request through its block table."""
-    hkv, d = k_pool.shape[1], k_pool.shape[3]
-    k = np.empty((n_tokens, hkv, d), dtype=np.uint16)
-    v = np.empty((n_tokens, hkv, d), dtype=np.uint16)
-    for j in range(n_tokens):
-        blk, off = int(table_row[j // BLOCK_TOKENS]), j % BLOCK_TOKENS
-        k[j] = k_pool[blk, :, off, :]
-        v[j] = v_pool[blk, :, :, off]
-    return k, v
+    """Contiguous K, V ([n_tokens, Hkv, D] bf16 bits) of one request through its block table:
+    token j comes from physical block table_row[j // 16] at offset j % 16."""
+    j = np.arange(n_tokens)
+    blk = np.asarray(table_row, dtype=np.int64)[j // BLOCK_TOKENS]
+    off = j % BLOCK_TOKENS
+    k = k_pool[blk, :, off, :]
+    v = v_pool[blk, :, :, off]
+    return np.ascontiguousarray(k), np.ascontiguousarray(v)
 
 
 def touched_blocks(slots) -> set[int]:

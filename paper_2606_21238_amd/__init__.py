@@ -158,6 +158,13 @@ class BlockCache:
         return [(e.key, e.kase, e.evicted, e.evicted_from, e.dropped, e.dropped_from, e.phys_block,
                  e.p_after) for e in self._log[:m]]
 
+    def log_array(self) -> np.ndarray:
+        """Recorded decisions as one numpy structured array (fields of ``arckv_event``)."""
+        if self._log is None:
+            return np.ctypeslib.as_array((_lib.Event * 1)())[:0].copy()
+        m = min(self.log_count(), len(self._log))
+        return np.ctypeslib.as_array(self._log)[:m].copy()
+
     def log_count(self) -> int:
         n = _lib.i64()
         _lib.check(lib().arckv_cache_log_count(self._h, C.byref(n)), "arckv_cache_log_count")

@@ -262,3 +262,97 @@ def steps_short(cfg: Config, n_steps: int, suffix: int, batch: int = 16, n_sessi
                                          (Source(KIND_QUESTION, 400000 + k * batch + j, suffix), 0, suffix)])
                       for j, s in enumerate(range(g * batch, (g + 1) * batch))])
     return warm, steps
+
+
+# ---------------------------------------------------------------------------------------------
+# configuration 3: multi-turn conversations; configuration 5: trace replay
+# ---------------------------------------------------------------------------------------------
+
+def stream_multiturn(cfg: Config, n_requests: int | None = None):
+    """Requests of 64 conversation sessions, merged in arrival order.
+
+    Session s starts with a history of h_s tokens, h_s = clip(round(exp(N(mu, sigma^2))),
+    [hist_min, hist_max]).  Each request of the session is its whole history plus a new turn
+    of U{turn_min..turn_max} tokens; the turn is then appended to the history.  A session
+    whose next prompt would exceed hist_max tokens starts over with a fresh history (a new
+    conversation of the same user).  Session activity w_s ~ Zipf(activity_s) over a seeded
+    permutation; each session's requests arrive with exponential gaps of mean 1/w_s.
+    Returns (requests, capacity in blocks = floor(cache_frac * sum_s h_s / 16)).
+    """
+    e = cfg.extra
+    n_requests = e["n_requests"] if n_requests is None else n_requests
+    n = e["n_sessions"]
+    rng = np.random.default_rng(derive_seed(cfg.seed, KIND_STREAM, 3, 0))
+    hist0 = np.clip(np.round(np.exp(rng.normal(e["hist_mu"], e["hist_sigma"], n))), e["hist_min"],
+                    e["hist_max"]).astype(np.int64)
+    perm = rng.permutation(n)
+    w = np.empty(n)
+    w[perm] = zipf_probs(n, e["activity_s"])
+    # arrival times: per session a Poisson process of rate w_s; merge the first n_requests
+    events = []
+    for s in range(n):
+        t = 0.0
+        k = 0
+        while True:
+            t += rng.exponential(1.0 / w[s])
+            events.append((t, s, k))
+            k += 1
+            if k > n_requests:
+                break
+    events.sort()
+    events = events[:n_requests]
+    turns = rng.integers(e["turn_min"], e["turn_max"] + 1, size=len(events))
+    gen = np.zeros(n, dtype=np.int64)
+    hist = hist0.copy()
+    out = []
+    max_len = e["hist_max"] + e["turn_max"]
+    for (t, s, k), turn in zip(events, turns):
+        if hist[s] + turn > max_len:                       # the conversation starts over
+            gen[s] += 1
+            hist[s] = hist0[s]
+        src = Source(KIND_SESSION, int(s * 100000 + gen[s]), max_len)
+        L = int(hist[s] + turn)
+        out.append(make_request(cfg, [(src, 0, L)]))
+        hist[s] = L
+    capacity = int(e["cache_frac"] * hist0.sum() // 16)
+    return out, capacity
+
+
+def trace_docs(cfg: Config):
+    """Lengths of the recurring documents of the trace (seeded)."""
+    e = cfg.extra
+    rng = np.random.default_rng(derive_seed(cfg.seed, KIND_STREAM, 5, 1))
+    return rng.integers(e["doc_min"], e["doc_max"] + 1, size=e["n_docs"])
+
+
+def stream_trace(cfg: Config, n_requests: int | None = None):
+    """Trace replay: a recurring document drawn Zipf(s) (seeded rank permutation) with
+    probability 1 - oneoff_frac, else a one-off fresh document (same length law); each request
+    adds a fresh question of question_tokens tokens.
+    Returns (requests, capacity = floor(cache_frac * sum of recurring document tokens / 16))."""
+    e = cfg.extra
+    n_requests = e["n_requests"] if n_requests is None else n_requests
+    lens = trace_docs(cfg)
+    rng = np.random.default_rng(derive_seed(cfg.seed, KIND_STREAM, 5, 2))
+    rank_to_doc = rng.permutation(e["n_docs"])
+    p = zipf_probs(e["n_docs"], e["zipf_s"])
+    out = []
+    n_oneoff = 0
+    for i in range(n_requests):
+        if rng.random() < e["oneoff_frac"]:
+            L = int(rng.integers(e["doc_min"], e["doc_max"] + 1))
+            doc = Source(KIND_ONEOFF, n_oneoff, L)
+            n_oneoff += 1
+        else:
+            d = int(rank_to_doc[rng.choice(e["n_docs"], p=p)])
+            doc = Source(KIND_DOC, d, int(lens[d]))
+        q = Source(KIND_QUESTION, 500000 + i, e["question_tokens"])
+        out.append(make_request(cfg, [(doc, 0, doc.length), (q, 0, q.length)]))
+    capacity = int(e["cache_frac"] * lens.sum() // 16)
+    return out, capacity
+
+
+def sized(cfg: Config, capacity: int) -> Config:
+    """The configuration with a stream-derived cache capacity and a pool of capacity + scratch."""
+    import dataclasses
+    return dataclasses.replace(cfg, capacity=int(capacity), num_phys=int(capacity) + cfg.scratch)
