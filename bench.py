@@ -11,7 +11,12 @@ continues across warm-up and timed steps).
 Other workloads (`--workload`): `docqa_hit` (8 cached 8192-token documents + fresh 128-token
 questions), `longctx` (70B-shaped layer, 64/8 heads: 4 cached 32768-token documents + fresh
 2048-token suffixes), `short32|short48|short64` (16 sessions per batch adding S new tokens to
-fully cached lognormal histories; KV-read bound).
+fully cached lognormal histories; KV-read bound), `multiturn` (64 conversation sessions,
+lognormal histories, new turns of 32..512 tokens, cache 40 % of the histories; the first 256
+requests warm up) and `trace` (10,000-request replay over 500 Zipf(1.1) documents with 30 %
+one-off documents, cache 20 % of the recurring documents; the first 2,000 requests warm up, the
+next `--steps` batches are timed, and the host replays the whole stream for ARC and LRU hit
+rates).
 
 One step = one batch through the whole path: block hashing -> ARC plan -> metadata H2D ->
 KV scatter -> prefill attention -> release.  Each batch's computed-token Q/K/V are staged in
@@ -38,7 +43,7 @@ PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA (published)
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E (published)
 
 DEFAULT_STEPS = {"docqa": (48, 16), "docqa_hit": (20, 3), "longctx": (8, 2), "short32": (40, 4),
-                 "short48": (40, 4), "short64": (40, 4)}
+                 "short48": (40, 4), "short64": (40, 4), "multiturn": (None, None), "trace": (40, None)}
 
 
 def attn_flops(S, L, hq, d):
@@ -78,10 +83,45 @@ def cpu_baseline(cfg, sample, budget_s: float):
     return rows_done, flops, t_used
 
 
-def make_workload(name: str, steps: int, warmup: int):
-    """-> (cfg, untimed batches, timed batches, description, bound)"""
+def split_stream(reqs, cfg, warm_requests: int):
+    """Consecutive batches of a request stream (the library's batch formation) and the number of
+    batches that start before request `warm_requests`."""
+    import paper_2606_21238_amd as ak
+    lens = [r.n_tokens for r in reqs]
+    out, i = [], 0
+    while i < len(lens):
+        n = ak.next_batch(lens[i:i + 4 * cfg.max_batch], cfg.max_batch, cfg.capacity, cfg.scratch)
+        out.append((i, i + n))
+        i += n
+    n_warm = sum(1 for a, _ in out if a < warm_requests)
+    return [reqs[a:b] for a, b in out], n_warm
+
+
+def make_workload(name: str, steps, warmup):
+    """-> (cfg, untimed batches, timed batches, description, bound, host-only tail batches)"""
     from workloads import get_config
     from workloads import streams as st
+    if name in ("multiturn", "trace"):
+        base = get_config(name)
+        reqs, cap = st.stream_multiturn(base) if name == "multiturn" else st.stream_trace(base)
+        cfg = st.sized(base, cap)
+        batches, n_warm = split_stream(reqs, cfg, base.extra["warmup_requests"])
+        warmup = n_warm if warmup is None else warmup
+        steps = len(batches) - warmup if steps is None else steps
+        if steps <= 0 or warmup + steps > len(batches):
+            raise SystemExit(f"{name}: {len(batches)} batches in the stream, asked for {warmup} + {steps}")
+        e = base.extra
+        if name == "multiturn":
+            desc = (f"multiturn: {len(reqs)} requests of 64 sessions (history lognormal(7.5, 0.8) clipped "
+                    f"to [256, 16384], turns U[32, 512], Zipf(1.0) activity, Poisson arrivals) in batches "
+                    f"of <= 16; cache {cap} blocks (40% of the histories); 32 q / 8 kv heads, head_dim 128")
+        else:
+            desc = (f"trace: {len(reqs)}-request replay, 500 documents U[4096, 16384] tokens with Zipf(1.1) "
+                    f"popularity + 30% one-off documents, 128-token questions, batches of <= 16; cache "
+                    f"{cap} blocks (20% of the recurring documents); 32 q / 8 kv heads, head_dim 128; "
+                    f"GPU runs batches 0..{warmup + steps - 1}, timed {warmup}..{warmup + steps - 1}")
+        return (cfg, batches[:warmup], batches[warmup:warmup + steps], desc, None,
+                batches[warmup + steps:], e["warmup_requests"])
     if name == "docqa":
         cfg = get_config("docqa")
         stream = st.stream_docqa(cfg, n_batches=warmup + steps)
@@ -89,19 +129,19 @@ def make_workload(name: str, steps: int, warmup: int):
         desc = ("docqa: 8 requests/batch, 8192-token documents drawn Zipf(1.1) from 64 + 128-token "
                 "question; 32 q / 8 kv heads, head_dim 128, block 16; KV pool 25% of document tokens "
                 "(8192 blocks)")
-        return cfg, b[:warmup], b[warmup:], desc, "mfma"
+        return cfg, b[:warmup], b[warmup:], desc, "mfma", [], None
     if name == "docqa_hit":
         cfg = get_config("docqa")
         warm, st_b = st.steps_docqa_hit(cfg, warmup + steps)
         desc = ("docqa_hit: 8 cached 8192-token documents + fresh 128-token questions per step; 32 q / "
                 "8 kv heads, head_dim 128, block 16")
-        return cfg, warm + st_b[:warmup], st_b[warmup:], desc, "mfma"
+        return cfg, warm + st_b[:warmup], st_b[warmup:], desc, "mfma", [], None
     if name == "longctx":
         cfg = get_config("longctx")
         warm, st_b = st.steps_longctx(cfg, warmup + steps)
         desc = ("longctx: 70B-shaped layer, 64 q / 8 kv heads, head_dim 128, block 16; 4 cached "
                 "32768-token documents scattered over a 16384-block pool + fresh 2048-token suffixes")
-        return cfg, warm + st_b[:warmup], st_b[warmup:], desc, "mfma"
+        return cfg, warm + st_b[:warmup], st_b[warmup:], desc, "mfma", [], None
     if name.startswith("short"):
         S = int(name[5:])
         cfg = get_config("short")
@@ -109,7 +149,7 @@ def make_workload(name: str, steps: int, warmup: int):
         desc = (f"short{S}: 16 sessions/batch rotating over 64, each adding {S} new tokens to a fully "
                 f"cached lognormal(7.5, 0.8) history (block-aligned, clipped to [256, 16384]); 32 q / "
                 f"8 kv heads, head_dim 128, block 16")
-        return cfg, warm + st_b[:warmup], st_b[warmup:], desc, "hbm"
+        return cfg, warm + st_b[:warmup], st_b[warmup:], desc, "hbm", [], None
     raise SystemExit(f"unknown workload {name}")
 
 
@@ -139,35 +179,46 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     ak.lib()
-    cfg, untimed, timed, desc, bound = make_workload(args.workload, steps, warmup)
+    cfg, untimed, timed, desc, bound, host_tail, warm_requests = make_workload(args.workload, steps, warmup)
+    steps, warmup = len(timed), len(untimed)
     hq, hkv, d = cfg.num_q_heads, cfg.num_kv_heads, cfg.head_dim
     order = free_order(cfg.seed, cfg.num_phys)
     batches = untimed + timed
     n_untimed = len(untimed)
     tokens = [[r.tokens for r in b] for b in batches]
 
-    # ---- staging (untimed): plans on a shadow cache, then every batch's Q/K/V in HBM ----
+    # ---- staging (untimed): plans on a shadow cache, then the timed batches' Q/K/V in HBM ----
     shadow = ak.BlockCache(args.policy, cfg.capacity, cfg.num_phys, cfg.scratch, order)
     other = ak.BlockCache("lru" if args.policy == "arc" else "arc", cfg.capacity, cfg.num_phys,
                           cfg.scratch, order)
     prefix = []
-    s_w = l_w = {"prefix_hit_tokens": 0, "prompt_tokens": 0}
-    for bi, tl in enumerate(tokens):
+    zero = {"prefix_hit_tokens": 0, "prompt_tokens": 0}
+    s_w = l_w = s_e = l_e = s_sw = l_sw = zero
+    seen = 0
+    all_batches = batches + host_tail
+    for bi, b in enumerate(all_batches):
         if bi == n_untimed:
             s_w, l_w = shadow.stats(), other.stats()
-        reqs = [(ak.hash_blocks(t), len(t)) for t in tl]
+        if warm_requests is not None and s_sw is zero and seen >= warm_requests:
+            s_sw, l_sw = shadow.stats(), other.stats()
+        seen += len(b)
+        reqs = list(zip(ak.hash_blocks_batch([r.tokens for r in b]), (r.n_tokens for r in b)))
         p = shadow.plan_batch(reqs)
         shadow.release_batch()
-        prefix.append(p.prefix_lens.copy())
+        if bi < len(batches):
+            prefix.append(p.prefix_lens.copy())
         other.plan_batch(reqs)
         other.release_batch()
-    s_e, l_e = shadow.stats(), other.stats()
+        if bi + 1 == len(batches):
+            s_e, l_e = shadow.stats(), other.stats()
+    s_end, l_end = shadow.stats(), other.stats()
 
-    bank = TensorBank(cfg, "cuda")
-    staged = []
-    for b, pl in zip(batches, prefix):
-        q, kn, vn = bank.batch_suffix(b, pl)
-        staged.append((q, kn, vn, torch.empty_like(q)))
+    # stream workloads touch far more distinct sources than fit in HBM at once
+    bank = TensorBank(cfg, "cuda", max_sources=64 if host_tail or warm_requests is not None else 1 << 30)
+    staged = [None] * len(batches)
+    for i in range(n_untimed, len(batches)):
+        q, kn, vn = bank.batch_suffix(batches[i], prefix[i])
+        staged[i] = (q, kn, vn, torch.empty_like(q))
     torch.cuda.synchronize()
 
     if args.copy_calibration_mib:
@@ -184,6 +235,9 @@ def main():
     host_t = {"plan": 0.0, "upload": 0.0, "launch": 0.0, "release": 0.0}
 
     def step(i, ev=None):
+        if staged[i] is None:                       # untimed batches are staged just in time
+            q, kn, vn = bank.batch_suffix(batches[i], prefix[i])
+            staged[i] = (q, kn, vn, torch.empty_like(q))
         q, kn, vn, out = staged[i]
         h0 = time.perf_counter()
         plan = eng.plan(tokens[i])
@@ -210,6 +264,7 @@ def main():
 
     for i in range(n_untimed):
         step(i)
+        staged[i] = None
     torch.cuda.synchronize()
 
     events = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(steps)]
@@ -235,6 +290,8 @@ def main():
     total_f = float(np.sum(F))
     suffix_tokens = int(sum(int(s.sum()) for s in S_list))
     roof_t = [max(f / (PEAK_BF16_TFLOPS * 1e12), b / (PEAK_HBM_GBS * 1e9)) for f, b in zip(F, B)]
+    if bound is None:            # mixed hit/miss stream: the resource the whole window needs most of
+        bound = "mfma" if total_f / (PEAK_BF16_TFLOPS * 1e12) >= np.sum(B) / (PEAK_HBM_GBS * 1e9) else "hbm"
     if bound == "mfma":
         achieved, peak, unit = total_f / np.sum(t_attn) / 1e12, PEAK_BF16_TFLOPS, "TFLOP/s"
         per_launch = float(np.mean(F))
@@ -294,6 +351,14 @@ def main():
         },
         "work_items_per_step": [int(np.mean([w for w, _ in n_work])), int(np.mean([c for _, c in n_work]))],
     }
+
+    if warm_requests is not None:
+        # the whole stream after its warm-up requests, replayed on the host for both policies
+        result["cache"]["hit_rate_stream_after_warmup"] = {
+            args.policy: round(hit(s_end, s_sw), 4),
+            ("lru" if args.policy == "arc" else "arc"): round(hit(l_end, l_sw), 4),
+            "requests": int(s_end["requests"] - s_sw["requests"]),
+        }
 
     if not args.no_cpu_baseline:
         # bounded oracle sample: the first timed batch's requests, 16 query rows at a time
