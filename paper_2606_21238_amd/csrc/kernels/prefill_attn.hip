@@ -48,7 +48,6 @@ typedef float f32x2_t __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void lds_void;
 
-constexpr int kNB = arckv::kWaveCols / 32;         // 32-column MFMA blocks per wave
 constexpr int kStages = 4;                         // K/V tiles resident in LDS (ring)
 constexpr int kBK = 64;        // keys per K/V tile (4 blocks of 16)
 constexpr float kLazy = 8.0f;  // rescale O only when a column max grows by > 2^8
@@ -72,13 +71,43 @@ __device__ __forceinline__ int sv(int d) { return (d >> 3) & 1; }
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// v_permlane32_swap(a, b) exchanges the upper half of a with the lower half of b.  With b = a,
+// one result holds lanes 0..31 of x in both halves and the other lanes 32..63, so the max / sum
+// of the pair combines lanes l and l ^ 32 in every lane with no LDS round trip.  (The results
+// are copied to scalars before the bit casts: a bit cast of a vector element subscript was
+// compiled as a cast of element 0.)
+__device__ __forceinline__ void halves(float x, float& lo, float& hi) {
+  const uint32_t a = __builtin_bit_cast(uint32_t, x);
+  const auto r = __builtin_amdgcn_permlane32_swap(a, a, false, false);
+  const uint32_t r0 = r[0], r1 = r[1];
+  lo = __builtin_bit_cast(float, r0);
+  hi = __builtin_bit_cast(float, r1);
+}
+__device__ __forceinline__ float max_halves(float x) {
+  float lo, hi;
+  halves(x, lo, hi);
+  return fmaxf(lo, hi);
+}
+__device__ __forceinline__ float sum_halves(float x) {
+  float lo, hi;
+  halves(x, lo, hi);
+  return lo + hi;
+}
+
+// 16 bytes per lane from global memory straight into LDS (lane l writes LDS bytes
+// [M0 + 16 l, M0 + 16 l + 16)).  Written as inline assembly on purpose: the compiler's wait
+// insertion treats its own LDS-DMA loads as pending LDS traffic and then waits for every LDS
+// read to return before each MFMA; the kernel does its own vmcnt accounting for these loads
+// (every compiler-visible vector load has completed before the first one is issued).
 __device__ __forceinline__ void load_lds16(const void* g, lds_void* l) {
-  __builtin_amdgcn_global_load_lds(g, l, 16, 0, 0);
+  const uint32_t m = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(l));
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(m)
+               : "memory", "m0");
 }
 
 // NW waves (32 query columns each) per work-group: 8 (wide tiles, two waves per SIMD) or 4
 // (narrow tiles for short suffixes); one work-group per CU either way (the K/V ring fills LDS).
-template <int D, int G, int NW>
+template <int D, int G, int NW, int NB>
 __global__ __launch_bounds__(64 * NW, 1) void prefill_attn_kernel(
     const uint16_t* __restrict__ k_pool, const uint16_t* __restrict__ v_pool,
     const uint16_t* __restrict__ q, uint16_t* __restrict__ out,
@@ -87,7 +116,9 @@ __global__ __launch_bounds__(64 * NW, 1) void prefill_attn_kernel(
     const Work* __restrict__ work, int64_t n_q, int64_t num_blocks, int hq, int hkv,
     float scale_log2, float* __restrict__ ws_o, float* __restrict__ ws_lse, int64_t ws_slots) {
   constexpr int kThreads = 64 * NW;
-  constexpr int kCols = NW * arckv::kWaveCols;   // query columns of the work-group
+  constexpr int kNB = NB;                        // 32-column MFMA blocks per wave
+  constexpr int kWC = 32 * NB;                   // query columns per wave
+  constexpr int kCols = NW * kWC;                // query columns of the work-group
   constexpr int KSTEPS = D / 16;                 // k-steps of Q.K^T
   constexpr int DM = D / 32;                     // 32-row blocks of O^T
   constexpr int TILE = kBK * D * 2;              // bytes of one K (or V) tile
@@ -113,20 +144,23 @@ __global__ __launch_bounds__(64 * NW, 1) void prefill_attn_kernel(
   // ---- this lane's two query columns and their Q^T operands ----------------------------
   int pos[kNB];
   bool cval[kNB];
-  int64_t qrow[kNB];
   bf16x8_t qf[kNB][KSTEPS];
 #pragma unroll
   for (int nb = 0; nb < kNB; ++nb) {
-    const int col = w.col_start + wave * arckv::kWaveCols + nb * 32 + l32;
+    const int col = w.col_start + wave * kWC + nb * 32 + l32;
     const int tok = col / G, g = col % G;
     cval[nb] = col < ncols && (q0 + tok) < n_q;
     pos[nb] = cval[nb] ? P + tok : -1;
-    qrow[nb] = static_cast<int64_t>(q0 + tok) * hq + w.kvh * G + g;
+    const int64_t qrow = static_cast<int64_t>(q0 + tok) * hq + w.kvh * G + g;
 #pragma unroll
     for (int ks = 0; ks < KSTEPS; ++ks)
-      qf[nb][ks] = cval[nb] ? *reinterpret_cast<const bf16x8_t*>(q + qrow[nb] * D + ks * 16 + hg * 8)
+      qf[nb][ks] = cval[nb] ? *reinterpret_cast<const bf16x8_t*>(q + qrow * D + ks * 16 + hg * 8)
                             : bf16x8_t{};
   }
+
+  // vmcnt(0), as an instruction the compiler's wait insertion understands: the Q operands have
+  // arrived before any tile load (whose count the waits below track by hand) is issued
+  __builtin_amdgcn_s_waitcnt(0x0F70);
 
   const int last_col = min(w.col_start + kCols, ncols) - 1;
   const int wg_max_pos = P + last_col / G;
@@ -150,18 +184,30 @@ __global__ __launch_bounds__(64 * NW, 1) void prefill_attn_kernel(
   }
   const int64_t head_k = static_cast<int64_t>(w.kvh) * 16 * D;   // head offset inside a block
   const int64_t blk_stride = static_cast<int64_t>(hkv) * 16 * D;  // elements per physical block
-  auto phys_of = [&](int b) -> int64_t {
-    int32_t ph = b < nblk ? bt[b] : 0;
-    if (ph < 0 || ph >= num_blocks) ph = 0;  // never dereferenced unmasked (see masking)
-    return static_cast<int64_t>(ph) * blk_stride + head_k;
-  };
-  // tile t (keys kv_lo + 64 t ...) lives in LDS stage t % kStages
-  auto load_tile = [&](int tile) {
+  // Physical block numbers of the next tile to be issued: tiles are issued in order, and each
+  // issue reads the table entries of the one after it, so the scalar loads' latency is spent
+  // during a whole step rather than in front of the tile's loads.
+  int32_t next_ph[NLD];
+  auto fetch_ph = [&](int tile) {
     const int b0 = (kv_lo + tile * kBK) >> 4;
-    char* st = smem + (tile % kStages) * 2 * TILE;
 #pragma unroll
     for (int i = 0; i < NLD; ++i) {
-      const int64_t base = phys_of(b0 + blk_of[i]);
+      const int b = b0 + blk_of[i];
+      next_ph[i] = b < nblk ? bt[b] : 0;
+    }
+  };
+  fetch_ph(0);
+  // tile t (keys kv_lo + 64 t ...) lives in LDS stage t % kStages
+  auto load_tile = [&](int tile) {
+    char* st = smem + (tile % kStages) * 2 * TILE;
+    int32_t ph[NLD];
+#pragma unroll
+    for (int i = 0; i < NLD; ++i) ph[i] = next_ph[i];
+    fetch_ph(tile + 1);
+#pragma unroll
+    for (int i = 0; i < NLD; ++i) {
+      const int32_t pb = (ph[i] < 0 || ph[i] >= num_blocks) ? 0 : ph[i];  // never used unmasked
+      const int64_t base = static_cast<int64_t>(pb) * blk_stride + head_k;
       load_lds16(k_pool + base + k_off[i], (lds_void*)(st + i * LDB + wave * 1024));
       load_lds16(v_pool + base + v_off[i], (lds_void*)(st + TILE + i * LDB + wave * 1024));
     }
@@ -225,7 +271,7 @@ __global__ __launch_bounds__(64 * NW, 1) void prefill_attn_kernel(
       for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) m = fmaxf(m, s[mb][nb][r]);
-      m = fmaxf(m, __shfl_xor(m, 32));
+      m = max_halves(m);
       mx[nb] = m * scale_log2;
       grow = grow || (mx[nb] > m_run[nb] + kLazy);
     }
@@ -250,10 +296,13 @@ __global__ __launch_bounds__(64 * NW, 1) void prefill_attn_kernel(
   // p = 2^(s * scale * log2 e - m) rounded to bf16: the P^T operands of the P.V product, kept
   // as 32-bit bf16 pairs.  (The row sum reads these scalars; extracting words from the 8-element
   // vector instead was compiled into four reads of one register.)
+  // The row sums l accumulate the fp32 p (before the bf16 rounding the P.V operand gets); plain
+  // adds co-issue with the MFMAs where a bf16 dot product of the rounded pairs does not.
   auto exp_phase = [&](f32x16_t (&s)[2][kNB], uint32_t (&pw)[kNB][4][4]) {
 #pragma unroll
     for (int nb = 0; nb < kNB; ++nb) {
       const float mu = m_run[nb] == -INFINITY ? 0.f : m_run[nb];
+      float lsum = 0.f;
 #pragma unroll
       for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
@@ -262,21 +311,10 @@ __global__ __launch_bounds__(64 * NW, 1) void prefill_attn_kernel(
           for (int j = 0; j < 4; ++j) {
             const f32x2_t two = {fast_exp2(fmaf(s[mb][nb][8 * half + 2 * j], scale_log2, -mu)),
                                  fast_exp2(fmaf(s[mb][nb][8 * half + 2 * j + 1], scale_log2, -mu))};
+            lsum += two[0];
+            lsum += two[1];
             pw[nb][2 * mb + half][j] = __builtin_bit_cast(uint32_t, __builtin_convertvector(two, bf16x2_t));
           }
-    }
-  };
-  // row sums of the bf16-rounded p (exactly what the P.V product weighs V with)
-  auto row_sum = [&](const uint32_t (&pw)[kNB][4][4]) {
-#pragma unroll
-    for (int nb = 0; nb < kNB; ++nb) {
-      float lsum = 0.f;
-#pragma unroll
-      for (int k = 0; k < 4; ++k)
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-          lsum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, pw[nb][k][j]),
-                                                 __builtin_bit_cast(bf16x2_t, 0x3F803F80u), lsum, false);
       l_run[nb] += lsum;
     }
   };
@@ -320,12 +358,12 @@ __global__ __launch_bounds__(64 * NW, 1) void prefill_attn_kernel(
   // next tile needs masking (diagonal tiles, prompt end) run in a second, peeled loop, so the
   // main loop carries no mask code.
   static_assert(kStages >= 4, "the wait below assumes one tile in flight beyond i+2");
+  f32x16_t sa[2][kNB], sb[2][kNB];
+  uint32_t pb[kNB][4][4];
   auto tile_masked = [&](int t) {
     const int t0 = kv_lo + t * kBK;
     return (t0 + kBK - 1 > wg_min_pos) || (t0 + kBK > L);
   };
-  f32x16_t sa[2][kNB], sb[2][kNB];
-  uint32_t pb[kNB][4][4];
   if (ntiles > 0) {
     for (int t = 0; t < kStages - 1; ++t)
       if (t < ntiles) load_tile(t);
@@ -350,7 +388,6 @@ __global__ __launch_bounds__(64 * NW, 1) void prefill_attn_kernel(
     exp_phase(sc, pb);
     // phase B
     mma_pv(pb, i);
-    row_sum(pb);
     if constexpr (MASK_NEXT) {
       if (i + 1 < ntiles) {  // past the key range S(i+1) is stale LDS: never feed it to the max
         apply_mask(sn, t0 + kBK);
@@ -359,10 +396,15 @@ __global__ __launch_bounds__(64 * NW, 1) void prefill_attn_kernel(
     } else {
       update_max(sn);  // main-loop steps always have a next tile
     }
-    // the next step reads tile i+2 (K) and i+1 (V): only the loads just issued may be pending
-    if (issue) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * NLD * (kStages - 3)) : "memory");
-    else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    __syncthreads();
+    // The next step reads tile i+2 (K) and i+1 (V): only the loads just issued may be pending.
+    // The wait and the barrier are written out: a fenced __syncthreads() would also wait for
+    // those newest loads (their LDS writes count as outstanding memory operations), which
+    // would leave the ring only one tile deep.  lgkmcnt(0): this wave's LDS reads of the
+    // stage the next step overwrites have returned.
+    if (issue)
+      asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(2 * NLD * (kStages - 3)) : "memory");
+    else
+      asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
   };
   // first step whose next tile is masked (tile_masked is monotone in the tile index)
   int n_main = ntiles > 0 ? ntiles - 1 : 0;
@@ -398,12 +440,13 @@ __global__ __launch_bounds__(64 * NW, 1) void prefill_attn_kernel(
   // ---- epilogue: O^T register r of block md holds dim 32 md + 8 (r / 4) + 4 hg + r % 4 ------
 #pragma unroll
   for (int nb = 0; nb < kNB; ++nb) {
-    const float lt = l_run[nb] + __shfl_xor(l_run[nb], 32);
+    const float lt = sum_halves(l_run[nb]);
     const float inv = lt > 0.f ? 1.f / lt : 0.f;
-    const int local = wave * arckv::kWaveCols + nb * 32 + l32;
+    const int local = wave * kWC + nb * 32 + l32;
     if (w.slot < 0) {
       if (!cval[nb]) continue;
-      uint16_t* dst = out + qrow[nb] * D;
+      const int col = w.col_start + local;  // recomputed: not kept live through the loop
+      uint16_t* dst = out + (static_cast<int64_t>(q0 + col / G) * hq + w.kvh * G + col % G) * D;
 #pragma unroll
       for (int md = 0; md < DM; ++md)
 #pragma unroll
@@ -475,13 +518,20 @@ __global__ __launch_bounds__(kCombineThreads) void attn_combine_kernel(
   }
 }
 
-template <int D, int G, int NW>
+#ifndef ARCKV_WIDE_NB
+#define ARCKV_WIDE_NB 1
+#endif
+constexpr int kWideNB = ARCKV_WIDE_NB;
+constexpr int kWideWaves = arckv::kWideCols / (32 * kWideNB);
+static_assert(kWideWaves * 32 * kWideNB == arckv::kWideCols, "wide tile width");
+
+template <int D, int G, int NW, int NB>
 void launch_attn(dim3 grid, hipStream_t st, const uint16_t* kp, const uint16_t* vp,
                  const uint16_t* q, uint16_t* out, const int32_t* bt, int bt_stride,
                  const int32_t* cu_q, const int32_t* seq_lens, int n_reqs, const Work* work,
                  int64_t n_q, int64_t num_blocks, int hq, int hkv, float scale_log2, float* ws_o,
                  float* ws_lse, int64_t ws_slots) {
-  hipLaunchKernelGGL((prefill_attn_kernel<D, G, NW>), grid, dim3(64 * NW), 0, st, kp, vp, q, out,
+  hipLaunchKernelGGL((prefill_attn_kernel<D, G, NW, NB>), grid, dim3(64 * NW), 0, st, kp, vp, q, out,
                      bt, bt_stride, cu_q, seq_lens, n_reqs, work, n_q, num_blocks, hq, hkv,
                      scale_log2, ws_o, ws_lse, ws_slots);
 }
@@ -533,11 +583,11 @@ extern "C" int32_t arckv_prefill_attention(const void* k_pool, const void* v_poo
 #define ARCKV_LAUNCH(DD, GG)                                                                   \
   do {                                                                                         \
     if (tile_cols == arckv::kWideCols)                                                         \
-      launch_attn<DD, GG, 8>(grid, st, kp, vp, qp, op, block_tables, bt_stride, cu_q, seq_lens, \
+      launch_attn<DD, GG, kWideWaves, kWideNB>(grid, st, kp, vp, qp, op, block_tables, bt_stride, cu_q, seq_lens, \
                              n_reqs, wk, n_q, num_blocks, num_q_heads, num_kv_heads,           \
                              scale_log2, ws_o, ws_lse, ws_slots);                              \
     else                                                                                       \
-      launch_attn<DD, GG, 4>(grid, st, kp, vp, qp, op, block_tables, bt_stride, cu_q, seq_lens, \
+      launch_attn<DD, GG, 4, 1>(grid, st, kp, vp, qp, op, block_tables, bt_stride, cu_q, seq_lens, \
                              n_reqs, wk, n_q, num_blocks, num_q_heads, num_kv_heads,           \
                              scale_log2, ws_o, ws_lse, ws_slots);                              \
   } while (0)
