@@ -64,6 +64,23 @@ def scatter_bytes(S, hkv, d):
     return float(np.sum(8.0 * np.asarray(S, dtype=np.float64) * hkv * d))
 
 
+def measured_traffic(workload: str):
+    """HBM bytes per prefill_attn launch (FETCH_SIZE + WRITE_SIZE, calibrated against a plain
+    copy kernel) from the committed profile of this workload, or None when there is none or it
+    was taken on a different version of the kernel source."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "prefill_attn_traffic.json")
+    src = os.path.join(ROOT, "paper_2606_21238_amd", "csrc", "kernels", "prefill_attn.hip")
+    try:
+        data = json.load(open(path))
+        if data.get("kernel_source_sha256") != hashlib.sha256(open(src, "rb").read()).hexdigest():
+            return None
+        e = data["workloads"][workload]
+        return round(e["fetch_bytes_per_launch"] + e["write_bytes_per_launch"], 1)
+    except (OSError, KeyError, ValueError):
+        return None
+
+
 def cpu_baseline(cfg, sample, budget_s: float):
     """Times the fp64 oracle on query rows of staged batches (bounded by budget_s seconds)."""
     from oracle import attention as oatt
@@ -247,11 +264,7 @@ def main():
         if ev is not None:
             ev[0].record()
         eng.scatter(db, kn, vn)
-        if ev is not None:
-            ev[1].record()
-        eng.attention(db, q, out)
-        if ev is not None:
-            ev[2].record()
+        eng.attention(db, q, out, events=None if ev is None else ev[1:])
         h3 = time.perf_counter()
         eng.release()
         h4 = time.perf_counter()
@@ -267,7 +280,11 @@ def main():
         staged[i] = None
     torch.cuda.synchronize()
 
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(steps)]
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(steps)]
+    for evs in events:          # a first record creates each event's HIP handle
+        for e in evs:
+            e.record()
+    torch.cuda.synchronize()
     plans, n_work = [], []
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -286,7 +303,8 @@ def main():
     F = [attn_flops(S, L, hq, d) for S, L in zip(S_list, L_list)]
     B = [attn_bytes(S, L, hq, hkv, d) for S, L in zip(S_list, L_list)]
     t_scatter = [e[0].elapsed_time(e[1]) * 1e-3 for e in events]
-    t_attn = [e[1].elapsed_time(e[2]) * 1e-3 for e in events]
+    t_attn = [e[1].elapsed_time(e[2]) * 1e-3 for e in events]        # prefill_attn kernel
+    t_comb = [e[2].elapsed_time(e[3]) * 1e-3 for e in events]        # split-KV combine (if any)
     total_f = float(np.sum(F))
     suffix_tokens = int(sum(int(s.sum()) for s in S_list))
     roof_t = [max(f / (PEAK_BF16_TFLOPS * 1e12), b / (PEAK_HBM_GBS * 1e9)) for f, b in zip(F, B)]
@@ -300,6 +318,7 @@ def main():
         per_launch = float(np.mean(B))
     hit = lambda a, b: (a["prefix_hit_tokens"] - b["prefix_hit_tokens"]) / max(
         1, a["prompt_tokens"] - b["prompt_tokens"])
+    traffic = measured_traffic(args.workload)
 
     result = {
         "metric": "prefix-cached prefill attn TFLOP/s & % MI355X roofline; suffix tokens/s",
@@ -323,14 +342,16 @@ def main():
         "suffix_tokens_per_s": round(suffix_tokens / wall, 1),
         "roofline": {
             "bound": bound,
-            "kernel": "prefill_attn (+ split-KV combine when planned)",
+            "kernel": "prefill_attn_kernel",
             "achieved": round(achieved, 2),
             "peak": peak,
             "unit": unit,
             "frac": round(achieved / peak, 4),
-            "traffic": None,
+            "traffic": traffic,
             "algorithmic_per_launch": per_launch,
             "mean_launch_us": round(float(np.mean(t_attn)) * 1e6, 1),
+            "combine_mean_us": round(float(np.mean(t_comb)) * 1e6, 1),
+            "frac_with_combine": round(achieved / peak * float(np.sum(t_attn)) / float(np.sum(t_attn) + np.sum(t_comb)), 4),
             "mixed_roofline_frac": round(float(np.sum(roof_t) / np.sum(t_attn)), 4),
             "tflops_attention": round(total_f / np.sum(t_attn) / 1e12, 2),
             "hbm_gbs_attention": round(float(np.sum(B)) / np.sum(t_attn) / 1e9, 1),
@@ -338,6 +359,7 @@ def main():
         "breakdown_ms_per_step": {
             "scatter": round(float(np.mean(t_scatter)) * 1e3, 4),
             "attention": round(float(np.mean(t_attn)) * 1e3, 4),
+            "combine": round(float(np.mean(t_comb)) * 1e3, 4),
             "step_wall": round(wall / steps * 1e3, 4),
             "scatter_gbs": round(scatter_bytes(np.concatenate(S_list), hkv, d)
                                  / max(float(np.sum(t_scatter)), 1e-12) / 1e9, 1),

@@ -262,6 +262,19 @@ int32_t arckv_prefill_attention(const void* k_pool, const void* v_pool, const vo
                                 int32_t num_kv_heads, int32_t head_dim, float scale,
                                 void* workspace, int64_t ws_bytes, void* stream);
 
+/* Same as arckv_prefill_attention, for callers that time its two kernels: hipEvent_t handles
+ * (each may be NULL) recorded on stream right before the attention kernel (ev_begin), between
+ * it and the split-KV combine (ev_mid) and after the combine (ev_end).  The events must have
+ * been created by the caller, which keeps ownership. */
+int32_t arckv_prefill_attention_timed(const void* k_pool, const void* v_pool, const void* q,
+                                      void* out, const int32_t* block_tables, int32_t bt_stride,
+                                      const int32_t* cu_q, const int32_t* seq_lens, int32_t n_reqs,
+                                      int64_t n_q, int64_t num_blocks, const int32_t* work,
+                                      int64_t n_work, int64_t n_combine, int32_t tile_cols,
+                                      int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                                      float scale, void* workspace, int64_t ws_bytes, void* stream,
+                                      void* ev_begin, void* ev_mid, void* ev_end);
+
 #ifdef __cplusplus
 }
 #endif

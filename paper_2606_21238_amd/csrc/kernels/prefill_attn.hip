@@ -538,15 +538,15 @@ void launch_attn(dim3 grid, hipStream_t st, const uint16_t* kp, const uint16_t* 
 
 }  // namespace
 
-extern "C" int32_t arckv_prefill_attention(const void* k_pool, const void* v_pool, const void* q,
-                                           void* out, const int32_t* block_tables,
-                                           int32_t bt_stride, const int32_t* cu_q,
-                                           const int32_t* seq_lens, int32_t n_reqs, int64_t n_q,
-                                           int64_t num_blocks, const int32_t* work,
-                                           int64_t n_work, int64_t n_combine, int32_t tile_cols,
-                                           int32_t num_q_heads, int32_t num_kv_heads,
-                                           int32_t head_dim, float scale, void* workspace,
-                                           int64_t ws_bytes, void* stream) {
+namespace {
+
+int32_t prefill_attention(const void* k_pool, const void* v_pool, const void* q, void* out,
+                          const int32_t* block_tables, int32_t bt_stride, const int32_t* cu_q,
+                          const int32_t* seq_lens, int32_t n_reqs, int64_t n_q, int64_t num_blocks,
+                          const int32_t* work, int64_t n_work, int64_t n_combine, int32_t tile_cols,
+                          int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim, float scale,
+                          void* workspace, int64_t ws_bytes, void* stream, hipEvent_t ev_begin,
+                          hipEvent_t ev_mid, hipEvent_t ev_end) {
   if (num_q_heads < 1 || num_kv_heads < 1 || num_q_heads % num_kv_heads != 0 || n_reqs < 0 ||
       n_q < 0 || num_blocks < 0 || n_work < 0 || n_combine < 0 || ws_bytes < 0 || bt_stride < 0 ||
       !std::isfinite(scale) || scale <= 0.f)
@@ -558,7 +558,12 @@ extern "C" int32_t arckv_prefill_attention(const void* k_pool, const void* v_poo
     return arckv::fail(ARCKV_EUNSUPPORTED, "prefill_attention: group size %d not in {1,2,4,8}", G);
   if (tile_cols != arckv::kWideCols && tile_cols != arckv::kNarrowCols)
     return arckv::fail(ARCKV_EINVAL, "prefill_attention: tile_cols %d is not a planned width", tile_cols);
-  if (n_work == 0 && n_combine == 0) return ARCKV_OK;
+  if (n_work == 0 && n_combine == 0) {  // nothing to run; the events still mark the stream
+    for (hipEvent_t ev : {ev_begin, ev_mid, ev_end})
+      if (ev != nullptr && hipEventRecord(ev, static_cast<hipStream_t>(stream)) != hipSuccess)
+        return arckv::fail(ARCKV_EDEVICE, "prefill_attention: event record failed");
+    return ARCKV_OK;
+  }
   if (k_pool == nullptr || v_pool == nullptr || q == nullptr || out == nullptr ||
       block_tables == nullptr || cu_q == nullptr || seq_lens == nullptr || work == nullptr)
     return arckv::fail(ARCKV_EINVAL, "prefill_attention: NULL pointer");
@@ -578,6 +583,10 @@ extern "C" int32_t arckv_prefill_attention(const void* k_pool, const void* v_poo
   auto* wk = reinterpret_cast<const Work*>(work);
   const float scale_log2 = scale * 1.4426950408889634f;
 
+  auto record = [&](hipEvent_t ev) -> bool {
+    return ev == nullptr || hipEventRecord(ev, st) == hipSuccess;
+  };
+  if (!record(ev_begin)) return arckv::fail(ARCKV_EDEVICE, "prefill_attention: event record failed");
   if (n_work > 0) {
     const dim3 grid(static_cast<unsigned>(n_work));
 #define ARCKV_LAUNCH(DD, GG)                                                                   \
@@ -611,6 +620,7 @@ extern "C" int32_t arckv_prefill_attention(const void* k_pool, const void* v_poo
     if (e != hipSuccess)
       return arckv::fail(ARCKV_EDEVICE, "prefill_attention: %s", hipGetErrorString(e));
   }
+  if (!record(ev_mid)) return arckv::fail(ARCKV_EDEVICE, "prefill_attention: event record failed");
   if (n_combine > 0) {
     const dim3 grid(static_cast<unsigned>(n_combine), kCombineSplit);
     const Work* items = wk + n_work;
@@ -624,5 +634,36 @@ extern "C" int32_t arckv_prefill_attention(const void* k_pool, const void* v_poo
     if (e != hipSuccess)
       return arckv::fail(ARCKV_EDEVICE, "attn_combine: %s", hipGetErrorString(e));
   }
+  if (!record(ev_end)) return arckv::fail(ARCKV_EDEVICE, "prefill_attention: event record failed");
   return ARCKV_OK;
+}
+
+}  // namespace
+
+extern "C" int32_t arckv_prefill_attention(const void* k_pool, const void* v_pool, const void* q,
+                                           void* out, const int32_t* block_tables,
+                                           int32_t bt_stride, const int32_t* cu_q,
+                                           const int32_t* seq_lens, int32_t n_reqs, int64_t n_q,
+                                           int64_t num_blocks, const int32_t* work,
+                                           int64_t n_work, int64_t n_combine, int32_t tile_cols,
+                                           int32_t num_q_heads, int32_t num_kv_heads,
+                                           int32_t head_dim, float scale, void* workspace,
+                                           int64_t ws_bytes, void* stream) {
+  return prefill_attention(k_pool, v_pool, q, out, block_tables, bt_stride, cu_q, seq_lens, n_reqs,
+                           n_q, num_blocks, work, n_work, n_combine, tile_cols, num_q_heads,
+                           num_kv_heads, head_dim, scale, workspace, ws_bytes, stream, nullptr,
+                           nullptr, nullptr);
+}
+
+extern "C" int32_t arckv_prefill_attention_timed(
+    const void* k_pool, const void* v_pool, const void* q, void* out, const int32_t* block_tables,
+    int32_t bt_stride, const int32_t* cu_q, const int32_t* seq_lens, int32_t n_reqs, int64_t n_q,
+    int64_t num_blocks, const int32_t* work, int64_t n_work, int64_t n_combine, int32_t tile_cols,
+    int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim, float scale, void* workspace,
+    int64_t ws_bytes, void* stream, void* ev_begin, void* ev_mid, void* ev_end) {
+  return prefill_attention(k_pool, v_pool, q, out, block_tables, bt_stride, cu_q, seq_lens, n_reqs,
+                           n_q, num_blocks, work, n_work, n_combine, tile_cols, num_q_heads,
+                           num_kv_heads, head_dim, scale, workspace, ws_bytes, stream,
+                           static_cast<hipEvent_t>(ev_begin), static_cast<hipEvent_t>(ev_mid),
+                           static_cast<hipEvent_t>(ev_end));
 }

@@ -12,7 +12,8 @@ from dataclasses import dataclass
 
 import numpy as np
 
-from . import (BlockCache, BatchPlan, attention_plan, hash_blocks_batch, kv_scatter, prefill_attention)
+from . import (BlockCache, BatchPlan, attention_plan, hash_blocks_batch, lib)
+from . import _lib
 
 
 @dataclass
@@ -27,6 +28,8 @@ class DeviceBatch:
     n_combine: int
     ws_bytes: int
     tile_cols: int
+    n_tokens: int = 0          # computed (suffix) tokens of the batch: rows of q / k_new / v_new
+    work_ptr: int = 0          # device address of the work array
 
 
 class PrefillEngine:
@@ -96,16 +99,47 @@ class PrefillEngine:
         wk = dev[o:o + ap.work.size].view(-1, 8)
         if ap.ws_bytes > self._ws.numel():
             self._ws = torch.empty(ap.ws_bytes, dtype=torch.uint8, device=self.device)
-        return DeviceBatch(plan, bt, cu, sl, sm, wk, ap.n_work, ap.n_combine, ap.ws_bytes, ap.tile_cols)
+        return DeviceBatch(plan, bt, cu, sl, sm, wk, ap.n_work, ap.n_combine, ap.ws_bytes, ap.tile_cols,
+                           int(plan.cu_q[-1]), wk.data_ptr())
 
     # ---- device steps --------------------------------------------------------------------
-    def scatter(self, db: DeviceBatch, k_new, v_new, stream=None):
-        kv_scatter(self.k_pool, self.v_pool, k_new, v_new, db.slot_mapping, stream)
+    # The engine built every device buffer itself, so these calls skip the binding's per-call
+    # tensor checks and pass raw addresses straight to the C ABI (the library still validates
+    # sizes); they only check the shapes of the caller's q / k / v / out.
+    def _stream(self, stream):
+        if stream is not None:
+            return int(stream)
+        import torch
+        return torch.cuda.current_stream(self.device).cuda_stream
 
-    def attention(self, db: DeviceBatch, q, out, stream=None):
-        prefill_attention(self.k_pool, self.v_pool, q, out, db.block_tables, db.cu_q, db.seq_lens,
-                          db.work, db.n_work, db.n_combine, db.tile_cols, self.scale,
-                          self._ws if db.ws_bytes else None, db.ws_bytes, stream)
+    def scatter(self, db: DeviceBatch, k_new, v_new, stream=None):
+        shape = (db.n_tokens, self.hkv, self.d)
+        if tuple(k_new.shape) != shape or tuple(v_new.shape) != shape or not (
+                k_new.is_contiguous() and v_new.is_contiguous()) or k_new.element_size() != 2:
+            raise ValueError(f"k_new / v_new must be contiguous 16-bit {shape}")
+        _lib.check(lib().arckv_kv_scatter(self.k_pool.data_ptr(), self.v_pool.data_ptr(), k_new.data_ptr(),
+                                          v_new.data_ptr(), db.slot_mapping.data_ptr(), db.n_tokens,
+                                          self.num_phys, self.hkv, self.d, self._stream(stream)),
+                   "arckv_kv_scatter")
+
+    def attention(self, db: DeviceBatch, q, out, stream=None, events=None):
+        """Prefill attention of the batch.  `events`: optional (begin, mid, end) torch.cuda.Event
+        triple (already recorded once, so that each has its HIP handle), recorded by the library
+        right before the attention kernel, between it and the split-KV combine, and after it."""
+        shape = (db.n_tokens, self.hq, self.d)
+        if tuple(q.shape) != shape or tuple(out.shape) != shape or not (
+                q.is_contiguous() and out.is_contiguous()) or q.element_size() != 2:
+            raise ValueError(f"q / out must be contiguous 16-bit {shape}")
+        args = (self.k_pool.data_ptr(), self.v_pool.data_ptr(), q.data_ptr(), out.data_ptr(),
+                db.block_tables.data_ptr(), int(db.block_tables.shape[1]), db.cu_q.data_ptr(),
+                db.seq_lens.data_ptr(), db.plan.n_reqs, db.n_tokens, self.num_phys, db.work_ptr,
+                db.n_work, db.n_combine, db.tile_cols, self.hq, self.hkv, self.d, self.scale,
+                self._ws.data_ptr() if db.ws_bytes else None, db.ws_bytes, self._stream(stream))
+        if events is None:
+            _lib.check(lib().arckv_prefill_attention(*args), "arckv_prefill_attention")
+        else:
+            _lib.check(lib().arckv_prefill_attention_timed(*args, *(e.cuda_event for e in events)),
+                       "arckv_prefill_attention_timed")
 
     def step(self, token_lists, qkv_for_plan, stream=None):
         """One batch: plan, upload, scatter, attend, release.  qkv_for_plan(plan) returns the

@@ -1,6 +1,8 @@
 """Summarise rocprofv3 CSV output (kernel stats and --pmc counter collections) as short text.
 
     python -m paper_2606_21238_amd.profsum <rocprofv3 -d directory> [--match REGEX]
+    python -m paper_2606_21238_amd.profsum <dir> --match REGEX --last K     # timed dispatches
+    python -m paper_2606_21238_amd.profsum --traffic-json OUT ...           # see the end of file
 
 Kernel stats: calls, total and average duration per kernel.  Counter collections: per
 kernel and counter, the number of dispatches and the mean value per dispatch.
@@ -65,11 +67,95 @@ def summarize(directory: str, match: str | None = None) -> str:
     return "\n".join(out) + "\n"
 
 
+def _dispatches(directory: str, kind: str):
+    """Rows of the kernel-trace or counter-collection CSVs, in dispatch order."""
+    rows = []
+    for path in glob.glob(os.path.join(directory, "**", f"*{kind}.csv"), recursive=True):
+        with open(path) as f:
+            rows += list(csv.DictReader(f))
+    key = "Start_Timestamp" if kind == "kernel_trace" else "Dispatch_Id"
+    rows.sort(key=lambda r: int(float(_col(r, key))))
+    return rows
+
+
+def last_durations(directory: str, match: str, last: int) -> str:
+    """Mean duration of each matching kernel over its last `last` dispatches (the timed steps of
+    a bench run come last)."""
+    per = defaultdict(list)
+    for r in _dispatches(directory, "kernel_trace"):
+        name = _col(r, "Kernel_Name", "KernelName")
+        if re.search(match, name):
+            per[_short(name)].append((int(_col(r, "End_Timestamp")) - int(_col(r, "Start_Timestamp"))) / 1e3)
+    out = [f"# mean over the last {last} dispatches (kernel_trace.csv)",
+           f"{'kernel':<90} {'dispatches':>10} {'avg_us':>10}"]
+    for k, v in sorted(per.items()):
+        tail = v[-last:]
+        out.append(f"{k:<90} {len(tail):>10} {sum(tail) / len(tail):>10.2f}")
+    return "\n".join(out) + "\n"
+
+
+def last_counter(directory: str, match: str, counter: str, last: int) -> float:
+    """Mean value of `counter` per dispatch of the kernels matching `match`, over the last
+    `last` such dispatches (values of one dispatch summed over its rows)."""
+    per = defaultdict(float)
+    order = []
+    for r in _dispatches(directory, "counter_collection"):
+        name = _col(r, "Kernel_Name", "KernelName")
+        if not re.search(match, name) or _col(r, "Counter_Name", "CounterName") != counter:
+            continue
+        d = int(float(_col(r, "Dispatch_Id")))
+        if d not in per:
+            order.append(d)
+        per[d] += float(_col(r, "Counter_Value", "CounterValue"))
+    tail = order[-last:]
+    return sum(per[d] for d in tail) / max(1, len(tail))
+
+
+def traffic_entry(fetch_dir: str, write_dir: str, kernel: str, calib: str, calib_mib: int, last: int):
+    """HBM bytes per launch of `kernel` from FETCH_SIZE / WRITE_SIZE (KiB per dispatch), each
+    scaled by what the counter reads for the calibration kernel that reads and writes exactly
+    `calib_mib` MiB."""
+    f_cal = last_counter(fetch_dir, calib, "FETCH_SIZE", 1)
+    w_cal = last_counter(write_dir, calib, "WRITE_SIZE", 1)
+    f_factor = calib_mib * 1024.0 / f_cal
+    w_factor = calib_mib * 1024.0 / w_cal
+    fetch = last_counter(fetch_dir, kernel, "FETCH_SIZE", last) * 1024.0 * f_factor
+    write = last_counter(write_dir, kernel, "WRITE_SIZE", last) * 1024.0 * w_factor
+    return {"fetch_bytes_per_launch": fetch, "write_bytes_per_launch": write,
+            "fetch_factor": f_factor, "write_factor": w_factor, "dispatches": last}
+
+
 if __name__ == "__main__":
     args = sys.argv[1:]
-    m = None
-    if "--match" in args:
-        i = args.index("--match")
-        m = args[i + 1]
-        del args[i:i + 2]
-    sys.stdout.write(summarize(args[0], m))
+
+    def opt(name, default=None):
+        if name in args:
+            i = args.index(name)
+            v = args[i + 1]
+            del args[i:i + 2]
+            return v
+        return default
+
+    m = opt("--match")
+    last = opt("--last")
+    traffic = opt("--traffic-json")
+    if traffic:
+        # --traffic-json OUT --workload W --kernel-source SRC --fetch-dir D1 --write-dir D2
+        #   --calib-match REGEX --calib-mib N --last K --match KERNEL_REGEX
+        import hashlib
+        import json
+        w = opt("--workload")
+        src = opt("--kernel-source")
+        entry = traffic_entry(opt("--fetch-dir"), opt("--write-dir"), m, opt("--calib-match"),
+                              int(opt("--calib-mib")), int(last))
+        sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
+        data = json.load(open(traffic)) if os.path.exists(traffic) else {}
+        if data.get("kernel_source_sha256") != sha:
+            data = {"kernel_source_sha256": sha, "workloads": {}}
+        data["workloads"][w] = entry
+        json.dump(data, open(traffic, "w"), indent=1, sort_keys=True)
+        print(json.dumps({w: entry}))
+    elif last:
+        sys.stdout.write(last_durations(args[0], m or ".", int(last)))
+    else:
+        sys.stdout.write(summarize(args[0], m))

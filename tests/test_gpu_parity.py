@@ -284,3 +284,27 @@ def test_empty_work_is_a_noop():
                          torch.zeros((1, 8), dtype=torch.int32, device=DEV), 0, 0, 256, 0.125)
     torch.cuda.synchronize()
     assert int(out.abs().sum()) == 0
+
+
+def test_timed_entry_point_matches_and_records_events():
+    """arckv_prefill_attention_timed computes the same bytes and records its three events."""
+    cfg = get_config("docqa")
+    print_case("timed entry point vs plain entry point (docqa hit batch)")
+    ls = Lockstep(cfg)
+    warm, hot = stream_docqa_hit(cfg)
+    ls.batch(warm, rows_fn=lambda r, p: [0], check_pool=False)
+    toks = [r.tokens for r in hot]
+    plan = ls.eng.plan(toks)
+    db = ls.eng.upload(plan)
+    q, _, _ = ls.bank.batch_suffix(hot, plan.prefix_lens)
+    out1, out2 = torch.empty_like(q), torch.empty_like(q)
+    ls.eng.attention(db, q, out1)
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    for e in evs:
+        e.record()
+    torch.cuda.synchronize()
+    ls.eng.attention(db, q, out2, events=evs)
+    torch.cuda.synchronize()
+    ls.eng.release()
+    assert torch.equal(out1.view(torch.int16), out2.view(torch.int16))
+    assert evs[0].elapsed_time(evs[1]) > 0 and evs[1].elapsed_time(evs[2]) >= 0
