@@ -16,6 +16,7 @@
 // its own L2): all tiles of one (request, KV head) group land on the same XCD, so the K/V
 // they all stream is fetched into that XCD's L2 once.
 #include <algorithm>
+#include <cmath>
 #include <unordered_map>
 #include <vector>
 
@@ -125,8 +126,22 @@ extern "C" int32_t arckv_attention_plan(const int32_t* cu_q, const int32_t* seq_
   } else {  // fewer groups than XCDs: spread tiles over all XCDs instead
     for (size_t i = 0; i < items.size(); ++i) per_xcd[i % kXcds].push_back(items[i]);
   }
+  // Within an XCD: longest first (the tail of the launch is what load balance costs), but
+  // items whose key ranges are within ~10 % of each other count as equally long and are kept
+  // together by group, so that the work-groups running at the same time on the XCD are few
+  // groups' query tiles streaming the same keys and values, which the XCD's L2 serves once.
+  std::unordered_map<int64_t, int64_t> rank_of;
+  for (size_t g = 0; g < groups.size(); ++g) rank_of[groups[g].first] = static_cast<int64_t>(g);
+  auto bucket = [](int64_t cost) {  // log_{1.1} of the key-range length
+    return cost > 0 ? static_cast<int64_t>(std::log(static_cast<double>(cost)) / std::log(1.1)) : -1;
+  };
   for (auto& v : per_xcd)
-    std::stable_sort(v.begin(), v.end(), [](const Item& a, const Item& b) { return a.cost > b.cost; });
+    std::stable_sort(v.begin(), v.end(), [&](const Item& a, const Item& b) {
+      const int64_t ba = bucket(a.cost), bb = bucket(b.cost);
+      if (ba != bb) return ba > bb;
+      const int64_t ra = rank_of[a.group], rb = rank_of[b.group];
+      return ra != rb ? ra < rb : a.cost > b.cost;
+    });
   size_t longest = 0;
   for (auto& v : per_xcd) longest = std::max(longest, v.size());
   std::vector<Item> ordered;
