@@ -38,6 +38,11 @@ Readings fixed by this project where the paper is silent:
 * Physical placement: a page created by a miss takes the physical block of
   the page evicted by the same reference, else the head of a FIFO free list.
 
+DBL (Sec. 4, the evaluated variant with a fixed 1:1 split between the recency and the
+frequency queue) is the same policy with the adaptation switched off: p stays at c/2 and
+ghost hits (Cases II and III) only move x and call REPLACE.  This is the fixed-target form
+FRC_p of the ARC paper with p = c/2.
+
 Every reference is appended to a decision log (``Event``) so that another
 implementation can be compared decision by decision.
 """
@@ -68,13 +73,14 @@ class Event:
 
 
 class ARC:
-    """ARC(c) with pins and physical block placement."""
+    """ARC(c) with pins and physical block placement (adaptive=False: DBL, p fixed at c/2)."""
 
-    def __init__(self, capacity: int, free_blocks):
+    def __init__(self, capacity: int, free_blocks, adaptive: bool = True):
         if capacity < 1:
             raise ValueError("capacity must be >= 1")
         self.c = int(capacity)
-        self.p = 0.0
+        self.adaptive = adaptive
+        self.p = 0.0 if adaptive else self.c / 2.0
         # OrderedDicts in LRU -> MRU order; resident lists map key -> physical block.
         self.T1: OrderedDict[int, int] = OrderedDict()
         self.T2: OrderedDict[int, int] = OrderedDict()
@@ -133,15 +139,17 @@ class ARC:
             self.T2[x] = phys
             case = CASE_I
         elif x in self.B1:                                     # Case II
-            d1 = 1.0 if len(self.B1) >= len(self.B2) else len(self.B2) / len(self.B1)
-            self.p = min(self.p + d1, float(c))
+            if self.adaptive:
+                d1 = 1.0 if len(self.B1) >= len(self.B2) else len(self.B2) / len(self.B1)
+                self.p = min(self.p + d1, float(c))
             evicted, evicted_from, phys = self._replace(False)
             del self.B1[x]
             self.T2[x] = phys
             case = CASE_II
         elif x in self.B2:                                     # Case III
-            d2 = 1.0 if len(self.B2) >= len(self.B1) else len(self.B1) / len(self.B2)
-            self.p = max(self.p - d2, 0.0)
+            if self.adaptive:
+                d2 = 1.0 if len(self.B2) >= len(self.B1) else len(self.B1) / len(self.B2)
+                self.p = max(self.p - d2, 0.0)
             evicted, evicted_from, phys = self._replace(True)
             del self.B2[x]
             self.T2[x] = phys

@@ -110,6 +110,8 @@ class Planner:
         self.scratch = deque(order[n_pages:])
         if policy == "arc":
             self.cache = ARC(capacity, pages)
+        elif policy == "dbl":
+            self.cache = ARC(capacity, pages, adaptive=False)
         elif policy == "lru":
             self.cache = LRU(capacity, pages)
         else:

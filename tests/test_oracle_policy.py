@@ -39,6 +39,36 @@ def run_arc(refs, c):
     return a, hits
 
 
+DBL_TRACES = json.load(open(GOLDEN))["dbl_traces"]
+
+
+@pytest.mark.parametrize("tr", DBL_TRACES, ids=lambda t: f"dbl_c{t['c']}_{t['refs']}")
+def test_dbl_hand_derived_trace(tr):
+    a = ARC(tr["c"], range(1000, 1000 + tr["c"]), adaptive=False)
+    hits = 0
+    for ch in tr["refs"]:
+        ev = a.reference(key(ch))
+        hits += ev.case == CASE_I
+        a.check_invariants()
+    assert [CASE_NAMES[e.case] for e in a.log] == tr["cases"]
+    assert [chr(e.evicted) if e.evicted_from != FROM_NONE else "" for e in a.log] == tr["evicted"]
+    assert [e.p_after for e in a.log] == [float(x) for x in tr["p"]]
+    assert hits == tr["hits"]
+    T1, T2, B1, B2, p = a.snapshot()
+    assert (names(T1), names(T2), names(B1), names(B2), p) == (tr["T1"], tr["T2"], tr["B1"], tr["B2"], tr["p_final"])
+
+
+def test_dbl_keeps_p_at_half_capacity_and_the_invariants():
+    rng = random.Random(4)
+    for c in (1, 2, 5, 16):
+        a = ARC(c, range(100000), adaptive=False)
+        for _ in range(3000):
+            a.reference(rng.randrange(3 * c))
+            a.check_invariants()
+            assert a.p == c / 2
+        assert any(e.case in (CASE_II, CASE_III) for e in a.log)    # ghost hits happened
+
+
 @pytest.mark.parametrize("tr", TRACES, ids=lambda t: f"c{t['c']}_{t['refs']}")
 def test_arc_hand_derived_trace(tr):
     a, hits = run_arc(tr["refs"], tr["c"])
