@@ -176,7 +176,7 @@ def main():
     ap.add_argument("--workload", default="docqa", choices=sorted(DEFAULT_STEPS))
     ap.add_argument("--steps", type=int, default=None)
     ap.add_argument("--warmup", type=int, default=None)
-    ap.add_argument("--policy", default="arc", choices=["arc", "lru"])
+    ap.add_argument("--policy", default="arc", choices=["arc", "lru", "dbl"])
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle CPU time")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
@@ -206,8 +206,8 @@ def main():
 
     # ---- staging (untimed): plans on a shadow cache, then the timed batches' Q/K/V in HBM ----
     shadow = ak.BlockCache(args.policy, cfg.capacity, cfg.num_phys, cfg.scratch, order)
-    other = ak.BlockCache("lru" if args.policy == "arc" else "arc", cfg.capacity, cfg.num_phys,
-                          cfg.scratch, order)
+    other_policy = "arc" if args.policy == "lru" else "lru"
+    other = ak.BlockCache(other_policy, cfg.capacity, cfg.num_phys, cfg.scratch, order)
     prefix = []
     zero = {"prefix_hit_tokens": 0, "prompt_tokens": 0}
     s_w = l_w = s_e = l_e = s_sw = l_sw = zero
@@ -378,7 +378,7 @@ def main():
         # the whole stream after its warm-up requests, replayed on the host for both policies
         result["cache"]["hit_rate_stream_after_warmup"] = {
             args.policy: round(hit(s_end, s_sw), 4),
-            ("lru" if args.policy == "arc" else "arc"): round(hit(l_end, l_sw), 4),
+            other_policy: round(hit(l_end, l_sw), 4),
             "requests": int(s_end["requests"] - s_sw["requests"]),
         }
 

@@ -55,6 +55,7 @@ extern "C" {
 /* policies and reference order */
 #define ARCKV_POLICY_ARC 0
 #define ARCKV_POLICY_LRU 1
+#define ARCKV_POLICY_DBL 2 /* ARC with p fixed at c/2 (Sec. 4's static two-queue variant) */
 #define ARCKV_REF_TAIL_FIRST 0
 #define ARCKV_REF_HEAD_FIRST 1
 
@@ -105,11 +106,13 @@ int32_t arckv_hash_blocks_batch(const int32_t* const* tokens, const int64_t* n_t
  * is the LRU-most unpinned page of the list the rule selects, else of the other list (it
  * then goes to the ghost list of the list it left).  A new page takes the physical block
  * of the page its reference evicted, else the head of a FIFO free list.
+ * DBL (Sec. 4: a fixed 1:1 split between the recency and the frequency queue) runs the same
+ * rules with p held at c/2: ghost hits move the page and call REPLACE but do not steer p.
  * ------------------------------------------------------------------------------------- */
 typedef struct arckv_cache arckv_cache;
 
 typedef struct {
-  int32_t policy;                    /* ARCKV_POLICY_ARC or ARCKV_POLICY_LRU             */
+  int32_t policy;                    /* ARCKV_POLICY_ARC, _LRU or _DBL                   */
   int32_t ref_order;                 /* ARCKV_REF_TAIL_FIRST (default) or HEAD_FIRST     */
   int64_t capacity_blocks;           /* c >= 1: cacheable pages                          */
   int64_t num_phys_blocks;           /* pool size; >= capacity_blocks + scratch_blocks   */
@@ -169,7 +172,7 @@ int32_t arckv_release_batch(arckv_cache* cache);
 
 typedef struct {
   int64_t t1, t2, b1, b2;   /* list sizes (LRU policy: t1 = resident pages)          */
-  double p;                 /* ARC adaptive target (0 for LRU)                       */
+  double p;                 /* ARC target for |T1| (c/2 for DBL, 0 for LRU)          */
   int64_t capacity;
   int64_t references;       /* policy references issued                              */
   int64_t requests, prompt_tokens, prefix_hit_tokens, computed_tokens;

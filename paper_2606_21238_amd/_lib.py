@@ -10,7 +10,7 @@ LIB_PATH = os.path.join(_PKG, "lib", "libarckv.so")
 
 OK, EINVAL, ENOSPC, EDEVICE, ESTATE, EUNSUPPORTED = 0, -1, -2, -3, -4, -5
 STATUS_NAMES = {0: "OK", -1: "EINVAL", -2: "ENOSPC", -3: "EDEVICE", -4: "ESTATE", -5: "EUNSUPPORTED"}
-POLICY = {"arc": 0, "lru": 1}
+POLICY = {"arc": 0, "lru": 1, "dbl": 2}
 REF_ORDER = {"tail_first": 0, "head_first": 1}
 WORK_INTS = 8
 

@@ -13,6 +13,10 @@
 //   REPLACE: T1 non-empty and (|T1| > p or (x in B2 and |T1| == p)) ? T1 LRU -> B1 : T2 LRU -> B2
 // p is an IEEE binary64 value; sizes are compared with it exactly.
 //
+// DBL (Sec. 4: the two queues at a fixed 1:1 split) is the same machine with the adaptation
+// off: p starts at c/2 and Cases II/III leave it there (the fixed-target FRC_p of the ARC
+// paper).
+//
 // Serving additions (the paper is silent on them): pages used by the batch in flight are
 // pinned and skipped by victim selection (falling back to the other resident list, whose
 // ghost list then receives the page); a new page takes the evicted page's physical block or
@@ -221,7 +225,9 @@ struct arckv_cache {
       const double b1 = static_cast<double>(lists[ARCKV_LIST_B1].size);
       const double b2 = static_cast<double>(lists[ARCKV_LIST_B2].size);
       const bool in_b2 = where == ARCKV_LIST_B2;
-      if (!in_b2) {
+      if (policy != ARCKV_POLICY_ARC) {
+        // DBL: the target stays at c/2
+      } else if (!in_b2) {
         const double d1 = b1 >= b2 ? 1.0 : b2 / b1;
         p = std::min(p + d1, static_cast<double>(c_));
       } else {
@@ -309,9 +315,9 @@ struct arckv_cache {
     arckv_event ev{};
     ev.key = x;
     const int32_t st =
-        policy == ARCKV_POLICY_ARC ? reference_arc(x, ev) : reference_lru(x, ev);
+        policy == ARCKV_POLICY_LRU ? reference_lru(x, ev) : reference_arc(x, ev);
     if (st != ARCKV_OK) return st;
-    ev.p_after = policy == ARCKV_POLICY_ARC ? p : 0.0;
+    ev.p_after = policy == ARCKV_POLICY_LRU ? 0.0 : p;
     phys_out = ev.phys_block;
     case_counts[ev.kase] += 1;
     references += 1;
@@ -328,7 +334,8 @@ struct arckv_cache {
 extern "C" int32_t arckv_cache_create(const arckv_cache_cfg* cfg, arckv_cache** out) {
   if (cfg == nullptr || out == nullptr) return arckv::fail(ARCKV_EINVAL, "cache_create: NULL");
   *out = nullptr;
-  if (cfg->policy != ARCKV_POLICY_ARC && cfg->policy != ARCKV_POLICY_LRU)
+  if (cfg->policy != ARCKV_POLICY_ARC && cfg->policy != ARCKV_POLICY_LRU &&
+      cfg->policy != ARCKV_POLICY_DBL)
     return arckv::fail(ARCKV_EINVAL, "cache_create: unknown policy %d", cfg->policy);
   if (cfg->ref_order != ARCKV_REF_TAIL_FIRST && cfg->ref_order != ARCKV_REF_HEAD_FIRST)
     return arckv::fail(ARCKV_EINVAL, "cache_create: unknown reference order");
@@ -354,6 +361,7 @@ extern "C" int32_t arckv_cache_create(const arckv_cache_cfg* cfg, arckv_cache** 
   auto* c = new (std::nothrow) arckv_cache();
   if (c == nullptr) return arckv::fail(ARCKV_ENOSPC, "cache_create: out of host memory");
   c->policy = cfg->policy;
+  c->p = cfg->policy == ARCKV_POLICY_DBL ? static_cast<double>(cfg->capacity_blocks) / 2.0 : 0.0;
   c->ref_order = cfg->ref_order;
   c->c = cfg->capacity_blocks;
   c->num_phys = np;

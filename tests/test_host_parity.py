@@ -78,7 +78,7 @@ class Pair:
         assert st["case_counts"] == t.case_counts
 
 
-@pytest.mark.parametrize("policy", ["arc", "lru"])
+@pytest.mark.parametrize("policy", ["arc", "lru", "dbl"])
 @pytest.mark.parametrize("ref_order", ["tail_first", "head_first"])
 @pytest.mark.parametrize("seed", [0, 1, 2])
 def test_random_streams_bit_exact(policy, ref_order, seed):

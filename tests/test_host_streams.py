@@ -5,8 +5,8 @@ into batches (library batch formation vs oracle's), planned and released by the 
 and by the oracle planner with the same policy and seeded free list.  Compared per batch: block
 tables, cu_q, sequence lengths, hit blocks, slot mappings; over the whole stream: every policy
 decision (case, evicted / dropped identity and list, physical block, p after the reference),
-the final T1 / T2 / B1 / B2 contents, p, and the token totals.  ARC and LRU both run, so the
-reported hit rates of the two policies are each the oracle's.
+the final T1 / T2 / B1 / B2 contents, p, and the token totals.  ARC, DBL and LRU all run, so
+the reported hit rates of the policies are each the oracle's.
 """
 
 import numpy as np
@@ -90,7 +90,7 @@ def multiturn():
     return sized(base, cap), reqs, oracle_hashes(reqs)
 
 
-@pytest.mark.parametrize("policy", ["arc", "lru"])
+@pytest.mark.parametrize("policy", ["arc", "lru", "dbl"])
 def test_multiturn_stream_bit_exact(multiturn, policy):
     cfg, reqs, hashes = multiturn
     assert len(reqs) == 1024
@@ -112,7 +112,7 @@ def trace_head():
     return trace_case(2000)
 
 
-@pytest.mark.parametrize("policy", ["arc", "lru"])
+@pytest.mark.parametrize("policy", ["arc", "lru", "dbl"])
 def test_trace_first_2000_bit_exact(trace_head, policy):
     cfg, reqs, hashes = trace_head
     lib, orc = replay(cfg, reqs, policy, hashes)
@@ -123,7 +123,8 @@ def test_trace_first_2000_bit_exact(trace_head, policy):
 
 @pytest.mark.slow
 def test_trace_full_replay_bit_exact():
-    """All 10,000 requests, both policies (about two minutes of oracle time)."""
+    """All 10,000 requests, the two policies bench reports (about two minutes of oracle time;
+    DBL runs on the first 2,000 above)."""
     cfg, reqs, hashes = trace_case(None)
     assert len(reqs) == 10000
     for policy in ("arc", "lru"):
