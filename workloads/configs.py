@@ -68,6 +68,20 @@ CONFIGS = {
                     extra=dict(n_docs=500, doc_min=4096, doc_max=16384, zipf_s=1.1, oneoff_frac=0.3,
                                question_tokens=128, n_requests=10000, warmup_requests=2000,
                                cache_frac=0.2)),
+    # 6: document QA with windowed Zipf sampling (Sec. 4, document QA): 3,072 requests in
+    #    windows of 512; inside a window the QA items are drawn Zipf(1.0) by rank, and the
+    #    rank -> item map is reshuffled for every window.  An item is a document plus one of
+    #    its questions; items of one document share the document as prefix.  Two stand-ins:
+    #    long articles with many questions each, and short passages with few.
+    #    (capacity 0 = set by the sweep; host-only workloads)
+    "wzqa_long": Config("wzqa_long", 1006, 32, 8, 128, capacity=0, scratch=16, num_phys=0, max_batch=1,
+                        extra=dict(n_docs=128, doc_min=2048, doc_max=8192, questions_per_doc=8,
+                                   question_min=24, question_max=96, n_requests=3072, window=512,
+                                   zipf_s=1.0, sizes_tokens=[10000, 20000, 40000, 80000, 160000])),
+    "wzqa_short": Config("wzqa_short", 1007, 32, 8, 128, capacity=0, scratch=16, num_phys=0, max_batch=1,
+                         extra=dict(n_docs=1024, doc_min=256, doc_max=1536, questions_per_doc=2,
+                                    question_min=12, question_max=48, n_requests=3072, window=512,
+                                    zipf_s=1.0, sizes_tokens=[5000, 10000, 20000, 40000, 80000])),
 }
 
 

@@ -352,6 +352,54 @@ def stream_trace(cfg: Config, n_requests: int | None = None):
     return out, capacity
 
 
+# ---------------------------------------------------------------------------------------------
+# configuration 6: document QA with windowed Zipf sampling
+# ---------------------------------------------------------------------------------------------
+
+def wzqa_items(cfg: Config):
+    """The QA items: (document index, question index, document length, question length).
+    Document lengths U{doc_min..doc_max}, question lengths U{question_min..question_max},
+    questions_per_doc items per document (seeded)."""
+    e = cfg.extra
+    rng = np.random.default_rng(derive_seed(cfg.seed, KIND_STREAM, 6, 1))
+    doc_len = rng.integers(e["doc_min"], e["doc_max"] + 1, size=e["n_docs"])
+    nq = e["questions_per_doc"]
+    q_len = rng.integers(e["question_min"], e["question_max"] + 1, size=e["n_docs"] * nq)
+    return [(d, d * nq + k, int(doc_len[d]), int(q_len[d * nq + k]))
+            for d in range(e["n_docs"]) for k in range(nq)]
+
+
+def wzqa_ranks(cfg: Config, n_requests: int | None = None):
+    """Per request: (window, rank drawn, item index).  Window w = request // window; the
+    ranks are i.i.d. Zipf(zipf_s) over all items; each window draws its own seeded
+    permutation rank -> item, so popularity shifts at window boundaries."""
+    e = cfg.extra
+    n_requests = e["n_requests"] if n_requests is None else n_requests
+    n_items = e["n_docs"] * e["questions_per_doc"]
+    rng = np.random.default_rng(derive_seed(cfg.seed, KIND_STREAM, 6, 2))
+    p = zipf_probs(n_items, e["zipf_s"])
+    out = []
+    n_windows = -(-n_requests // e["window"])
+    for w in range(n_windows):                  # whole windows, so a shorter stream is a prefix
+        rank_to_item = rng.permutation(n_items)
+        for rk in rng.choice(n_items, size=e["window"], p=p):
+            out.append((w, int(rk), int(rank_to_item[rk])))
+    return out[:n_requests]
+
+
+def stream_wzqa(cfg: Config, n_requests: int | None = None):
+    """Document QA requests with windowed Zipf popularity: each request is its item's
+    document followed by the item's question (token streams seeded per document and per
+    question, so a repeated item repeats its whole prompt)."""
+    items = wzqa_items(cfg)
+    out = []
+    for _, _, it in wzqa_ranks(cfg, n_requests):
+        d, qi, dl, ql = items[it]
+        out.append(make_request(cfg, [(Source(KIND_DOC, d, dl), 0, dl),
+                                      (Source(KIND_QUESTION, qi, ql), 0, ql)]))
+    return out
+
+
 def sized(cfg: Config, capacity: int) -> Config:
     """The configuration with a stream-derived cache capacity and a pool of capacity + scratch."""
     import dataclasses
