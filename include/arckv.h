@@ -232,8 +232,9 @@ int32_t arckv_kv_scatter(void* k_pool, void* v_pool, const void* k_new, const vo
 
 /* Work decomposition (host): one work item is a query tile of *tile_cols (column = token x
  * query head of one KV group, token-major) of one (request, KV head) over a key range.
- * Long key ranges are split when the batch has too few tiles to fill num_cus compute units;
- * split tiles are merged by a log-sum-exp combine pass.
+ * Long key ranges are split when the batch has too few tiles to fill num_cus compute units
+ * (into one round of at most num_cus items); split tiles are merged by a log-sum-exp combine
+ * pass.
  * cu_q, seq_lens: HOST copies of the plan's arrays.  work: host int32 buffer of
  * ARCKV_WORK_INTS * work_cap entries or NULL to query sizes.
  * Outputs: *n_work attention items, *n_combine combine items (both stored in work, the
@@ -253,7 +254,7 @@ int32_t arckv_attention_plan(const int32_t* cu_q, const int32_t* seq_lens, int32
  * block_tables: device int32 [n_reqs][bt_stride]; cu_q: device [n_reqs + 1]; seq_lens:
  * device [n_reqs] (the same values given to arckv_attention_plan).  work: device copy of
  * the plan's items, tile_cols: the plan's tile width.  workspace: device, >= the planned
- * ws_bytes (may be NULL if 0).
+ * ws_bytes (may be NULL if 0).  Calls that overlap in time must not share a workspace.
  * Block-table entries outside [0, num_blocks) are read as zero keys/values.
  * head_dim in {64, 128}; num_q_heads / num_kv_heads in {1, 2, 4, 8}. */
 int32_t arckv_prefill_attention(const void* k_pool, const void* v_pool, const void* q, void* out,

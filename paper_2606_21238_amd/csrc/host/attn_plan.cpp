@@ -7,9 +7,11 @@
 // tokens sees keys 0..P+i).  Tiles are 256 columns wide, or 128 when no request of the batch
 // has more than 128 columns (short suffixes), so that no work-group computes on empty
 // columns.  When a batch has fewer tiles than compute units (short suffixes over long cached
-// prefixes), tiles are split along the key range into about one item per compute unit, at
-// least 512 keys each; split tiles write fp32 partials plus a base-2 log-sum-exp, merged
-// afterwards by one combine item per tile.
+// prefixes), tiles are split along the key range so that the whole batch runs as one round of
+// at most one item per compute unit: the smallest cap on key tiles per item (at least 8, i.e.
+// 512 keys) for which the pieces fit, each tile cut into equal pieces under the cap.  Split
+// items write fp32 partials plus a base-2 log-sum-exp, merged afterwards by one combine item
+// per tile.
 //
 // Items are ordered longest key range first so the longest ones start first, and the order
 // is interleaved over the 8 XCDs (work-groups are dispatched round-robin over XCDs, each with
@@ -62,7 +64,6 @@ extern "C" int32_t arckv_attention_plan(const int32_t* cu_q, const int32_t* seq_
 
   struct Tile { int32_t req, kvh, col_start, kv_end; };
   std::vector<Tile> tiles;
-  int64_t total_keys = 0;
   for (int32_t r = 0; r < n_reqs; ++r) {
     const int64_t S = static_cast<int64_t>(cu_q[r + 1]) - cu_q[r];
     const int64_t L = seq_lens[r];
@@ -74,30 +75,42 @@ extern "C" int32_t arckv_attention_plan(const int32_t* cu_q, const int32_t* seq_
       const int32_t kv_end = static_cast<int32_t>(P + last / G + 1);
       for (int32_t h = 0; h < num_kv_heads; ++h) {
         tiles.push_back({r, h, static_cast<int32_t>(cs), kv_end});
-        total_keys += kv_end;
       }
     }
   }
   const int64_t base = static_cast<int64_t>(tiles.size());
   const int64_t target = static_cast<int64_t>(num_cus);  // one work-group per CU at a time
-  int64_t chunk = INT32_MAX;
+  auto key_tiles = [](const Tile& t) { return (static_cast<int64_t>(t.kv_end) + kKeyTile - 1) / kKeyTile; };
+  int64_t cap = INT32_MAX;  // key tiles per item
   if (base > 0 && base < target) {
-    const int64_t want = (total_keys + target - 1) / target;
-    chunk = std::max<int64_t>(512, (want + kKeyTile - 1) / kKeyTile * kKeyTile);
+    int64_t total_t = 0, max_t = 0;
+    for (const Tile& t : tiles) {
+      total_t += key_tiles(t);
+      max_t = std::max(max_t, key_tiles(t));
+    }
+    int64_t lo = std::max<int64_t>(8, (total_t + target - 1) / target), hi = std::max(lo, max_t);
+    while (lo < hi) {  // smallest cap whose pieces fit in one round
+      const int64_t mid = (lo + hi) / 2;
+      int64_t cnt = 0;
+      for (const Tile& t : tiles) cnt += (key_tiles(t) + mid - 1) / mid;
+      if (cnt <= target) hi = mid; else lo = mid + 1;
+    }
+    cap = lo;
   }
 
   std::vector<Item> items, combines;
   int64_t slot = 0;
   for (const Tile& t : tiles) {
-    const int64_t ns = (t.kv_end + chunk - 1) / chunk;
+    const int64_t nt = key_tiles(t);
+    const int64_t ns = (nt + cap - 1) / cap;
     const int64_t group = static_cast<int64_t>(t.req) * num_kv_heads + t.kvh;
     if (ns <= 1) {
       items.push_back({{t.req, t.kvh, t.col_start, 0, t.kv_end, -1, 0, 0}, t.kv_end, group});
       continue;
     }
-    for (int64_t s = 0; s < ns; ++s) {
-      const int32_t a = static_cast<int32_t>(s * chunk);
-      const int32_t b = static_cast<int32_t>(std::min<int64_t>((s + 1) * chunk, t.kv_end));
+    for (int64_t s = 0; s < ns; ++s) {  // equal pieces of whole key tiles
+      const int32_t a = static_cast<int32_t>(s * nt / ns * kKeyTile);
+      const int32_t b = static_cast<int32_t>(std::min<int64_t>((s + 1) * nt / ns * kKeyTile, t.kv_end));
       items.push_back({{t.req, t.kvh, t.col_start, a, b, static_cast<int32_t>(slot + s), 0, 0}, b - a, group});
     }
     combines.push_back({{t.req, t.kvh, t.col_start, static_cast<int32_t>(slot), static_cast<int32_t>(ns), 0, 0, 0}, 0, group});

@@ -8,10 +8,12 @@
 // Sec. 4; layout V1: K [blk][kvh][16][D], V [blk][kvh][D][16]).
 //
 // Design (MI355X-first):
-//  * One work-group = 8 (or, for short suffixes, 4) wave64s = one query tile of one (request,
-//    KV head); a
+//  * One work-group = 8 wave64s (two per SIMD) = one query tile of one (request, KV head); a
 //    column is (token, head-of-group), token-major, so every K/V tile a work-group loads
-//    serves all G query heads of its KV head (GQA packed into the MFMA N dimension).
+//    serves all G query heads of its KV head (GQA packed into the MFMA N dimension).  Wide
+//    tiles: 8 waves x 32 columns.  Narrow tiles (short suffixes): 4 x 32 columns, the two
+//    groups of 4 waves taking the two 32-key halves of every K/V tile with separate online
+//    softmax states that merge through LDS at the end.
 //  * Transposed formulation: S^T = K . Q^T and O^T = V^T . P^T with v_mfma_f32_32x32x16_bf16.
 //    Query columns sit on lanes, keys / head dims on the M (register) dimension, so a lane
 //    owns whole columns: row max and row sum are in-lane plus one exchange with lane +- 32.
@@ -23,12 +25,14 @@
 //    the B-operand layout of the P.V step, so P^T goes from registers to the next MFMA with
 //    no shuffle, and V^T (dim-major blocks) is read as one 16-byte operand per lane.
 //  * K/V tiles of 64 keys (4 blocks) are gathered from the scattered physical blocks with
-//    16-byte loads into registers, then into double-buffered, XOR-swizzled LDS; the next
-//    tile's loads are in flight while the current tile is multiplied.
+//    16-byte direct global-to-LDS loads into a 4-stage ring of XOR-swizzled LDS tiles; two
+//    tiles are in flight while the current one is multiplied.  The first tiles' loads go out
+//    behind the query loads, so one wait covers both.
 //  * fp32 online softmax in base 2 (scale * log2 e folded into one FMA per score), causal
 //    masking only on tiles that cross the diagonal, bf16 P with fp32 accumulation.
-//  * Long key ranges with too few query tiles are split by the host plan; split items write
-//    fp32 partials plus a base-2 log-sum-exp that attn_combine merges.
+//  * Long key ranges with too few query tiles are split by the host plan into one round of
+//    work-groups; split items write fp32 partials plus a base-2 log-sum-exp that
+//    attn_combine merges.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -105,9 +109,12 @@ __device__ __forceinline__ void load_lds16(const void* g, lds_void* l) {
                : "memory", "m0");
 }
 
-// NW waves (32 query columns each) per work-group: 8 (wide tiles, two waves per SIMD) or 4
-// (narrow tiles for short suffixes); one work-group per CU either way (the K/V ring fills LDS).
-template <int D, int G, int NW, int NB>
+// NW waves per work-group (two per SIMD), one work-group per CU (the K/V ring fills LDS).
+// KH = 1 (wide tiles): each wave owns 32 NB query columns and every key.  KH = 2 (narrow
+// tiles, short suffixes): the waves form two halves over the same 4 x 32 columns, half h
+// taking keys [32 h, 32 h + 32) of every 64-key tile, each with its own online softmax; the
+// halves merge through LDS at the end.  Both keep two waves per SIMD for any tile width.
+template <int D, int G, int NW, int NB, int KH>
 __global__ __launch_bounds__(64 * NW, 1) void prefill_attn_kernel(
     const uint16_t* __restrict__ k_pool, const uint16_t* __restrict__ v_pool,
     const uint16_t* __restrict__ q, uint16_t* __restrict__ out,
@@ -118,7 +125,10 @@ __global__ __launch_bounds__(64 * NW, 1) void prefill_attn_kernel(
   constexpr int kThreads = 64 * NW;
   constexpr int kNB = NB;                        // 32-column MFMA blocks per wave
   constexpr int kWC = 32 * NB;                   // query columns per wave
-  constexpr int kCols = NW * kWC;                // query columns of the work-group
+  constexpr int kCW = NW / KH;                   // waves per key half
+  constexpr int kCols = kCW * kWC;               // query columns of the work-group
+  constexpr int kMB = 2 / KH;                    // 32-key blocks of a tile per wave
+  static_assert((KH == 1 || KH == 2) && (KH == 1 || NB == 1) && kCW * KH == NW, "key halves");
   constexpr int KSTEPS = D / 16;                 // k-steps of Q.K^T
   constexpr int DM = D / 32;                     // 32-row blocks of O^T
   constexpr int TILE = kBK * D * 2;              // bytes of one K (or V) tile
@@ -132,6 +142,7 @@ __global__ __launch_bounds__(64 * NW, 1) void prefill_attn_kernel(
   if (w.req < 0 || w.req >= n_reqs || w.kvh < 0 || w.kvh >= hkv || w.col_start < 0) return;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int cw = wave % kCW, kh = wave / kCW;    // column wave, key half
   const int l32 = lane & 31, hg = lane >> 5;
   const int q0 = cu_q[w.req];
   const int S = cu_q[w.req + 1] - q0;
@@ -147,7 +158,7 @@ __global__ __launch_bounds__(64 * NW, 1) void prefill_attn_kernel(
   bf16x8_t qf[kNB][KSTEPS];
 #pragma unroll
   for (int nb = 0; nb < kNB; ++nb) {
-    const int col = w.col_start + wave * kWC + nb * 32 + l32;
+    const int col = w.col_start + cw * kWC + nb * 32 + l32;
     const int tok = col / G, g = col % G;
     cval[nb] = col < ncols && (q0 + tok) < n_q;
     pos[nb] = cval[nb] ? P + tok : -1;
@@ -157,10 +168,6 @@ __global__ __launch_bounds__(64 * NW, 1) void prefill_attn_kernel(
       qf[nb][ks] = cval[nb] ? *reinterpret_cast<const bf16x8_t*>(q + qrow * D + ks * 16 + hg * 8)
                             : bf16x8_t{};
   }
-
-  // vmcnt(0), as an instruction the compiler's wait insertion understands: the Q operands have
-  // arrived before any tile load (whose count the waits below track by hand) is issued
-  __builtin_amdgcn_s_waitcnt(0x0F70);
 
   const int last_col = min(w.col_start + kCols, ncols) - 1;
   const int wg_max_pos = P + last_col / G;
@@ -214,18 +221,18 @@ __global__ __launch_bounds__(64 * NW, 1) void prefill_attn_kernel(
   };
 
   // ---- MFMA pieces ------------------------------------------------------------------------
-  // S^T (64 keys x this wave's 64 columns) = K . Q^T
-  auto mma_s = [&](f32x16_t (&s)[2][kNB], int tile) {
+  // S^T (this wave's 32 kMB keys of the tile x its columns) = K . Q^T
+  auto mma_s = [&](f32x16_t (&s)[kMB][kNB], int tile) {
     const char* kb = smem + (tile % kStages) * 2 * TILE;
 #pragma unroll
-    for (int mb = 0; mb < 2; ++mb)
+    for (int mb = 0; mb < kMB; ++mb)
 #pragma unroll
       for (int nb = 0; nb < kNB; ++nb) s[mb][nb] = f32x16_t{};
 #pragma unroll
     for (int ks = 0; ks < KSTEPS; ++ks)
 #pragma unroll
-      for (int mb = 0; mb < 2; ++mb) {
-        const int r = mb * 32 + pi_row(l32);
+      for (int mb = 0; mb < kMB; ++mb) {
+        const int r = (kh * kMB + mb) * 32 + pi_row(l32);
         const int c = 2 * ks + hg;
         const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(kb + r * 2 * D + ((c ^ fk<D>(r)) * 16));
 #pragma unroll
@@ -243,16 +250,16 @@ __global__ __launch_bounds__(64 * NW, 1) void prefill_attn_kernel(
 #pragma unroll
   for (int nb = 0; nb < kNB; ++nb) { m_run[nb] = -INFINITY; l_run[nb] = 0.f; }
 
-  // causal / prompt-end mask: accumulator register r of S^T block mb holds key
-  // t0 + 32 mb + 16 (r / 8) + 8 hg + r % 8 of this lane's column
-  auto apply_mask = [&](f32x16_t (&s)[2][kNB], int t0) {
+  // causal / prompt-end mask: accumulator register r of this wave's S^T block mb holds key
+  // t0 + 32 (kh kMB + mb) + 16 (r / 8) + 8 hg + r % 8 of this lane's column
+  auto apply_mask = [&](f32x16_t (&s)[kMB][kNB], int t0) {
 #pragma unroll
     for (int nb = 0; nb < kNB; ++nb)
 #pragma unroll
-      for (int mb = 0; mb < 2; ++mb)
+      for (int mb = 0; mb < kMB; ++mb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const int key = t0 + mb * 32 + 16 * (r >> 3) + 8 * hg + (r & 7);
+          const int key = t0 + (kh * kMB + mb) * 32 + 16 * (r >> 3) + 8 * hg + (r & 7);
           s[mb][nb][r] = key > pos[nb] ? -INFINITY : s[mb][nb][r];
         }
   };
@@ -261,14 +268,14 @@ __global__ __launch_bounds__(64 * NW, 1) void prefill_attn_kernel(
   // then O and l must be scaled by alpha before the next P.V product (apply_rescale).
   float alpha[kNB];
   bool pending = false;  // wave-uniform
-  auto update_max = [&](f32x16_t (&s)[2][kNB]) {
+  auto update_max = [&](f32x16_t (&s)[kMB][kNB]) {
     float mx[kNB];
     bool grow = false;
 #pragma unroll
     for (int nb = 0; nb < kNB; ++nb) {
       float m = -INFINITY;
 #pragma unroll
-      for (int mb = 0; mb < 2; ++mb)
+      for (int mb = 0; mb < kMB; ++mb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) m = fmaxf(m, s[mb][nb][r]);
       m = max_halves(m);
@@ -298,13 +305,13 @@ __global__ __launch_bounds__(64 * NW, 1) void prefill_attn_kernel(
   // vector instead was compiled into four reads of one register.)
   // The row sums l accumulate the fp32 p (before the bf16 rounding the P.V operand gets); plain
   // adds co-issue with the MFMAs where a bf16 dot product of the rounded pairs does not.
-  auto exp_phase = [&](f32x16_t (&s)[2][kNB], uint32_t (&pw)[kNB][4][4]) {
+  auto exp_phase = [&](f32x16_t (&s)[kMB][kNB], uint32_t (&pw)[kNB][2 * kMB][4]) {
 #pragma unroll
     for (int nb = 0; nb < kNB; ++nb) {
       const float mu = m_run[nb] == -INFINITY ? 0.f : m_run[nb];
       float lsum = 0.f;
 #pragma unroll
-      for (int mb = 0; mb < 2; ++mb)
+      for (int mb = 0; mb < kMB; ++mb)
 #pragma unroll
         for (int half = 0; half < 2; ++half)
 #pragma unroll
@@ -318,15 +325,16 @@ __global__ __launch_bounds__(64 * NW, 1) void prefill_attn_kernel(
       l_run[nb] += lsum;
     }
   };
-  // O^T (D x this wave's 64 columns) += V^T . P^T
-  auto mma_pv = [&](const uint32_t (&pw)[kNB][4][4], int tile) {
+  // O^T (D x this wave's columns) += V^T . P^T over this wave's 16-key blocks of the tile
+  auto mma_pv = [&](const uint32_t (&pw)[kNB][2 * kMB][4], int tile) {
     const char* vb = smem + (tile % kStages) * 2 * TILE + TILE;
 #pragma unroll
-    for (int sp = 0; sp < 4; ++sp)
+    for (int sp = 0; sp < 2 * kMB; ++sp)
 #pragma unroll
       for (int md = 0; md < DM; ++md) {
         const int d = md * 32 + l32;
-        const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(vb + sp * BLK_BYTES + d * 32 + ((hg ^ sv(d)) * 16));
+        const int blk = kh * 2 * kMB + sp;
+        const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(vb + blk * BLK_BYTES + d * 32 + ((hg ^ sv(d)) * 16));
 #pragma unroll
         for (int nb = 0; nb < kNB; ++nb) {
           const u32x4_t w4 = {pw[nb][sp][0], pw[nb][sp][1], pw[nb][sp][2], pw[nb][sp][3]};
@@ -358,22 +366,27 @@ __global__ __launch_bounds__(64 * NW, 1) void prefill_attn_kernel(
   // next tile needs masking (diagonal tiles, prompt end) run in a second, peeled loop, so the
   // main loop carries no mask code.
   static_assert(kStages >= 4, "the wait below assumes one tile in flight beyond i+2");
-  f32x16_t sa[2][kNB], sb[2][kNB];
-  uint32_t pb[kNB][4][4];
+  f32x16_t sa[kMB][kNB], sb[kMB][kNB];
+  uint32_t pb[kNB][2 * kMB][4];
   auto tile_masked = [&](int t) {
     const int t0 = kv_lo + t * kBK;
     return (t0 + kBK - 1 > wg_min_pos) || (t0 + kBK > L);
   };
+  // The Q operand loads above are still in flight: the first tiles' loads go out behind them
+  // and one vmcnt(0) covers both (an instruction the compiler's wait insertion understands,
+  // so it adds no wait of its own before the Q operands are used).
   if (ntiles > 0) {
     for (int t = 0; t < kStages - 1; ++t)
       if (t < ntiles) load_tile(t);
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  }
+  __builtin_amdgcn_s_waitcnt(0x0F70);
+  if (ntiles > 0) {
     __syncthreads();
     mma_s(sa, 0);
     if (tile_masked(0)) apply_mask(sa, kv_lo);
     update_max(sa);
   }
-  auto step = [&](auto mask_next, f32x16_t (&sc)[2][kNB], f32x16_t (&sn)[2][kNB], int i) {
+  auto step = [&](auto mask_next, f32x16_t (&sc)[kMB][kNB], f32x16_t (&sn)[kMB][kNB], int i) {
     constexpr bool MASK_NEXT = decltype(mask_next)::value;
     const int t0 = kv_lo + i * kBK;
     const bool issue = i + kStages - 1 < ntiles;
@@ -424,7 +437,7 @@ __global__ __launch_bounds__(64 * NW, 1) void prefill_attn_kernel(
   if (i < n_main) {
     step(std::false_type{}, sa, sb, i);
 #pragma unroll
-    for (int mb = 0; mb < 2; ++mb)
+    for (int mb = 0; mb < kMB; ++mb)
 #pragma unroll
       for (int nb = 0; nb < kNB; ++nb) sa[mb][nb] = sb[mb][nb];
     ++i;
@@ -432,57 +445,119 @@ __global__ __launch_bounds__(64 * NW, 1) void prefill_attn_kernel(
   for (; i < ntiles; ++i) {
     step(std::true_type{}, sa, sb, i);
 #pragma unroll
-    for (int mb = 0; mb < 2; ++mb)
+    for (int mb = 0; mb < kMB; ++mb)
 #pragma unroll
       for (int nb = 0; nb < kNB; ++nb) sa[mb][nb] = sb[mb][nb];
   }
 
+  // ---- key halves: half 1 hands (m, l, O) to half 0 through LDS ---------------------------
+  // Every wave has passed the barrier ending its last step (or ran no step and read no LDS),
+  // so the ring is free.  Layout: O as [column wave][md][r / 4][lane] float4, then m and l as
+  // [column wave][lane]; a lane of half 0 reads exactly what the same lane of half 1 wrote.
+  if constexpr (KH == 2) {
+    f32x4_t* xo = reinterpret_cast<f32x4_t*>(smem) + cw * (DM * 4 * 64);
+    float* xm = reinterpret_cast<float*>(smem + kCW * DM * 4 * 64 * 16) + cw * 128;
+    __syncthreads();
+    if (kh == 1) {
+#pragma unroll
+      for (int md = 0; md < DM; ++md)
+#pragma unroll
+        for (int r4 = 0; r4 < 4; ++r4) {
+          f32x4_t v;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) v[j] = o[md][0][4 * r4 + j];
+          xo[(md * 4 + r4) * 64 + lane] = v;
+        }
+      xm[lane] = m_run[0];
+      xm[64 + lane] = l_run[0];
+    }
+    __syncthreads();
+  }
+  const bool active = kh == 0;  // waves that hold the (merged) result
+  if (KH == 2 && active) {
+    const f32x4_t* xo = reinterpret_cast<const f32x4_t*>(smem) + cw * (DM * 4 * 64);
+    const float* xm = reinterpret_cast<const float*>(smem + kCW * DM * 4 * 64 * 16) + cw * 128;
+    const float mb_ = xm[lane], lb = xm[64 + lane];
+    const float m = fmaxf(m_run[0], mb_);
+    const float a = m_run[0] == -INFINITY ? 0.f : fast_exp2(m_run[0] - m);
+    const float b = mb_ == -INFINITY ? 0.f : fast_exp2(mb_ - m);
+#pragma unroll
+    for (int md = 0; md < DM; ++md)
+#pragma unroll
+      for (int r4 = 0; r4 < 4; ++r4) {
+        const f32x4_t v = xo[(md * 4 + r4) * 64 + lane];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) o[md][0][4 * r4 + j] = a * o[md][0][4 * r4 + j] + b * v[j];
+      }
+    l_run[0] = a * l_run[0] + b * lb;
+    m_run[0] = m;
+  }
+
   // ---- epilogue: O^T register r of block md holds dim 32 md + 8 (r / 4) + 4 hg + r % 4 ------
+  // O is normalised in registers; lse (base 2) is what a split item reports with it.
+  float lse[kNB];
 #pragma unroll
   for (int nb = 0; nb < kNB; ++nb) {
     const float lt = sum_halves(l_run[nb]);
     const float inv = lt > 0.f ? 1.f / lt : 0.f;
-    const int local = wave * kWC + nb * 32 + l32;
-    if (w.slot < 0) {
-      if (!cval[nb]) continue;
-      const int col = w.col_start + local;  // recomputed: not kept live through the loop
-      uint16_t* dst = out + (static_cast<int64_t>(q0 + col / G) * hq + w.kvh * G + col % G) * D;
+    lse[nb] = lt > 0.f ? m_run[nb] + __log2f(lt) : -INFINITY;
 #pragma unroll
-      for (int md = 0; md < DM; ++md)
+    for (int md = 0; md < DM; ++md) o[md][nb] *= inv;
+  }
+  auto store_out = [&](int nb) __attribute__((always_inline)) {
+    const int col = w.col_start + cw * kWC + nb * 32 + l32;  // recomputed: not kept live through the loop
+    uint16_t* dst = out + (static_cast<int64_t>(q0 + col / G) * hq + w.kvh * G + col % G) * D;
 #pragma unroll
-        for (int r4 = 0; r4 < 4; ++r4) {
-          f32x4_t v;
+    for (int md = 0; md < DM; ++md)
 #pragma unroll
-          for (int j = 0; j < 4; ++j) v[j] = o[md][nb][4 * r4 + j] * inv;
-          *reinterpret_cast<bf16x4_t*>(dst + md * 32 + 8 * r4 + 4 * hg) = __builtin_convertvector(v, bf16x4_t);
-        }
-    } else if (w.slot < ws_slots && cval[nb]) {
-      float* po = ws_o + (static_cast<int64_t>(w.slot) * kCols + local) * D;
+      for (int r4 = 0; r4 < 4; ++r4) {
+        f32x4_t v;
 #pragma unroll
-      for (int md = 0; md < DM; ++md)
+        for (int j = 0; j < 4; ++j) v[j] = o[md][nb][4 * r4 + j];
+        *reinterpret_cast<bf16x4_t*>(dst + md * 32 + 8 * r4 + 4 * hg) = __builtin_convertvector(v, bf16x4_t);
+      }
+  };
+  if (w.slot < 0) {
+    if (active)
 #pragma unroll
-        for (int r4 = 0; r4 < 4; ++r4) {
-          f32x4_t v;
+      for (int nb = 0; nb < kNB; ++nb)
+        if (cval[nb]) store_out(nb);
+    return;
+  }
+  if (w.slot >= ws_slots || !active) return;
 #pragma unroll
-          for (int j = 0; j < 4; ++j) v[j] = o[md][nb][4 * r4 + j] * inv;
-          *reinterpret_cast<f32x4_t*>(po + md * 32 + 8 * r4 + 4 * hg) = v;
-        }
-      if (hg == 0)
-        ws_lse[static_cast<int64_t>(w.slot) * kCols + local] =
-            lt > 0.f ? m_run[nb] + __log2f(lt) : -INFINITY;
-    }
+  for (int nb = 0; nb < kNB; ++nb) {
+    if (!cval[nb]) continue;
+    const int local = cw * kWC + nb * 32 + l32;
+    float* po = ws_o + (static_cast<int64_t>(w.slot) * kCols + local) * D;
+#pragma unroll
+    for (int md = 0; md < DM; ++md)
+#pragma unroll
+      for (int r4 = 0; r4 < 4; ++r4) {
+        f32x4_t v;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) v[j] = o[md][nb][4 * r4 + j];
+        *reinterpret_cast<f32x4_t*>(po + md * 32 + 8 * r4 + 4 * hg) = v;
+      }
+    if (hg == 0) ws_lse[static_cast<int64_t>(w.slot) * kCols + local] = lse[nb];
   }
 }
 
-// Merges the key-range splits of one query tile: o = sum_s 2^lse_s O_s / sum_s 2^lse_s.
-// Grid: (combine items, kCombineSplit); block y handles every kCombineSplit-th column.
+// Merges the key-range splits of one query tile: o = sum_s 2^(lse_s - M) O_s / sum_s 2^(lse_s - M)
+// with M = max_s lse_s, per column.  Grid: (combine items, tile_cols / kCombineCols); a block
+// takes kCombineCols columns: it first turns the pieces' lse into per-column weights in LDS
+// (one round of loads), then each thread sums its columns' float4 slices over the pieces with
+// all of a group of pieces' loads in flight at once (a second round).
 constexpr int kCombineThreads = 256;
-constexpr int kCombineSplit = 8;
+constexpr int kCombineCols = 32;
+constexpr int kCombineMaxSplits = 64;  // pieces weighted in LDS at a time
 template <int D>
 __global__ __launch_bounds__(kCombineThreads) void attn_combine_kernel(
     uint16_t* __restrict__ out, const Work* __restrict__ items, const int32_t* __restrict__ cu_q,
     int n_reqs, int64_t n_q, int hq, int G, int tile_cols, const float* __restrict__ ws_o,
     const float* __restrict__ ws_lse, int64_t ws_slots) {
+  __shared__ float wt[kCombineMaxSplits][kCombineCols];
+  __shared__ float mx[kCombineCols], inv[kCombineCols];
   const Work w = items[blockIdx.x];  // {req, kvh, col_start, slot0, n_splits}
   const int slot0 = w.kv_start, ns = w.kv_end;
   if (w.req < 0 || w.req >= n_reqs || w.kvh < 0 || (w.kvh + 1) * G > hq || w.col_start < 0 ||
@@ -490,30 +565,59 @@ __global__ __launch_bounds__(kCombineThreads) void attn_combine_kernel(
     return;
   const int q0 = cu_q[w.req];
   const int ncols = (cu_q[w.req + 1] - q0) * G;
+  const int c0 = blockIdx.y * kCombineCols;  // first local column of this block
   constexpr int D4 = D / 4;
-  const int my_cols = (tile_cols + kCombineSplit - 1) / kCombineSplit;
-  for (int e = threadIdx.x; e < my_cols * D4; e += kCombineThreads) {
-    const int local = (e / D4) * kCombineSplit + blockIdx.y, d4 = e % D4;
+  const int tid = threadIdx.x;
+  // per-column maximum of the pieces' lse
+  if (tid < kCombineCols) {
+    float m = -INFINITY;
+    for (int s = 0; s < ns; ++s)
+      m = fmaxf(m, ws_lse[static_cast<int64_t>(slot0 + s) * tile_cols + c0 + tid]);
+    mx[tid] = m;
+  }
+  __syncthreads();
+  f32x4_t acc[kCombineCols * D4 / kCombineThreads];
+  constexpr int PER = kCombineCols * D4 / kCombineThreads;  // float4 slices per thread
+  static_assert(PER * kCombineThreads == kCombineCols * D4, "combine split");
+#pragma unroll
+  for (int k = 0; k < PER; ++k) acc[k] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  float wsum_part = 0.f;
+  for (int sb = 0; sb < ns; sb += kCombineMaxSplits) {
+    const int nb = min(kCombineMaxSplits, ns - sb);
+    // weights of pieces [sb, sb + nb) for the block's columns
+    for (int e = tid; e < nb * kCombineCols; e += kCombineThreads) {
+      const int s = e / kCombineCols, c = e % kCombineCols;
+      const float l = ws_lse[static_cast<int64_t>(slot0 + sb + s) * tile_cols + c0 + c];
+      wt[s][c] = l == -INFINITY ? 0.f : fast_exp2(l - mx[c]);
+    }
+    __syncthreads();
+    if (tid < kCombineCols)
+      for (int s = 0; s < nb; ++s) wsum_part += wt[s][tid];
+#pragma unroll 4
+    for (int s = 0; s < nb; ++s) {
+      const float* po = ws_o + (static_cast<int64_t>(slot0 + sb + s) * tile_cols + c0) * D;
+      f32x4_t v[PER];
+#pragma unroll
+      for (int k = 0; k < PER; ++k) {
+        const int e = tid + k * kCombineThreads;  // column e / D4, slice e % D4
+        v[k] = *reinterpret_cast<const f32x4_t*>(po + static_cast<int64_t>(e / D4) * D + 4 * (e % D4));
+      }
+#pragma unroll
+      for (int k = 0; k < PER; ++k) acc[k] += wt[s][(tid + k * kCombineThreads) / D4] * v[k];
+    }
+    __syncthreads();
+  }
+  if (tid < kCombineCols) inv[tid] = wsum_part > 0.f ? 1.f / wsum_part : 0.f;
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const int e = tid + k * kCombineThreads;
+    const int local = c0 + e / D4, d4 = e % D4;
     const int col = w.col_start + local;
     if (local >= tile_cols || col >= ncols) continue;
     const int tok = col / G, g = col % G;
     if (q0 + tok >= n_q) continue;
-    float m = -INFINITY;
-    for (int s = 0; s < ns; ++s) m = fmaxf(m, ws_lse[static_cast<int64_t>(slot0 + s) * tile_cols + local]);
-    f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
-    float wsum = 0.f;
-    for (int s = 0; s < ns; ++s) {
-      const float lse = ws_lse[static_cast<int64_t>(slot0 + s) * tile_cols + local];
-      const float wt = lse == -INFINITY ? 0.f : fast_exp2(lse - m);
-      wsum += wt;
-      if (wt > 0.f) {
-        const f32x4_t v = *reinterpret_cast<const f32x4_t*>(
-            ws_o + (static_cast<int64_t>(slot0 + s) * tile_cols + local) * D + 4 * d4);
-        acc += wt * v;
-      }
-    }
-    const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
-    const bf16x4_t b = __builtin_convertvector(acc * inv, bf16x4_t);
+    const bf16x4_t b = __builtin_convertvector(acc[k] * inv[e / D4], bf16x4_t);
     *reinterpret_cast<bf16x4_t*>(out + (static_cast<int64_t>(q0 + tok) * hq + w.kvh * G + g) * D + 4 * d4) = b;
   }
 }
@@ -525,13 +629,13 @@ constexpr int kWideNB = ARCKV_WIDE_NB;
 constexpr int kWideWaves = arckv::kWideCols / (32 * kWideNB);
 static_assert(kWideWaves * 32 * kWideNB == arckv::kWideCols, "wide tile width");
 
-template <int D, int G, int NW, int NB>
+template <int D, int G, int NW, int NB, int KH>
 void launch_attn(dim3 grid, hipStream_t st, const uint16_t* kp, const uint16_t* vp,
                  const uint16_t* q, uint16_t* out, const int32_t* bt, int bt_stride,
                  const int32_t* cu_q, const int32_t* seq_lens, int n_reqs, const Work* work,
                  int64_t n_q, int64_t num_blocks, int hq, int hkv, float scale_log2, float* ws_o,
                  float* ws_lse, int64_t ws_slots) {
-  hipLaunchKernelGGL((prefill_attn_kernel<D, G, NW, NB>), grid, dim3(64 * NW), 0, st, kp, vp, q, out,
+  hipLaunchKernelGGL((prefill_attn_kernel<D, G, NW, NB, KH>), grid, dim3(64 * NW), 0, st, kp, vp, q, out,
                      bt, bt_stride, cu_q, seq_lens, n_reqs, work, n_q, num_blocks, hq, hkv,
                      scale_log2, ws_o, ws_lse, ws_slots);
 }
@@ -592,11 +696,11 @@ int32_t prefill_attention(const void* k_pool, const void* v_pool, const void* q,
 #define ARCKV_LAUNCH(DD, GG)                                                                   \
   do {                                                                                         \
     if (tile_cols == arckv::kWideCols)                                                         \
-      launch_attn<DD, GG, kWideWaves, kWideNB>(grid, st, kp, vp, qp, op, block_tables, bt_stride, cu_q, seq_lens, \
+      launch_attn<DD, GG, kWideWaves, kWideNB, 1>(grid, st, kp, vp, qp, op, block_tables, bt_stride, cu_q, seq_lens, \
                              n_reqs, wk, n_q, num_blocks, num_q_heads, num_kv_heads,           \
                              scale_log2, ws_o, ws_lse, ws_slots);                              \
     else                                                                                       \
-      launch_attn<DD, GG, 4, 1>(grid, st, kp, vp, qp, op, block_tables, bt_stride, cu_q, seq_lens, \
+      launch_attn<DD, GG, 8, 1, 2>(grid, st, kp, vp, qp, op, block_tables, bt_stride, cu_q, seq_lens, \
                              n_reqs, wk, n_q, num_blocks, num_q_heads, num_kv_heads,           \
                              scale_log2, ws_o, ws_lse, ws_slots);                              \
   } while (0)
@@ -622,7 +726,7 @@ int32_t prefill_attention(const void* k_pool, const void* v_pool, const void* q,
   }
   if (!record(ev_mid)) return arckv::fail(ARCKV_EDEVICE, "prefill_attention: event record failed");
   if (n_combine > 0) {
-    const dim3 grid(static_cast<unsigned>(n_combine), kCombineSplit);
+    const dim3 grid(static_cast<unsigned>(n_combine), static_cast<unsigned>(tile_cols / kCombineCols));
     const Work* items = wk + n_work;
     if (head_dim == 64)
       hipLaunchKernelGGL(attn_combine_kernel<64>, grid, dim3(kCombineThreads), 0, st, op, items,

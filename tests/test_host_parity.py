@@ -192,11 +192,13 @@ def attention_plan_coverage(cu_q, seq_lens, hq, hkv, d, num_cus):
     assert tc == (128 if max_cols <= 128 else 256)
     items = ap.work[: ap.n_work]
     comb = ap.work[ap.n_work: ap.n_work + ap.n_combine]
-    cover = {}
+    cover, n_live, n_slots = {}, 0, 0
     for it in items:
         req, kvh, cs, a, b, slot = (int(x) for x in it[:6])
         if req < 0:
             continue
+        n_live += 1
+        n_slots += slot >= 0
         assert a % 64 == 0 and b > a
         cover.setdefault((req, kvh, cs), []).append((a, b, slot))
     for r in range(len(seq_lens)):
@@ -214,15 +216,26 @@ def attention_plan_coverage(cu_q, seq_lens, hq, hkv, d, num_cus):
                 else:
                     slots = [x[2] for x in ranges]
                     assert slots == list(range(slots[0], slots[0] + len(slots)))
+                    # pieces of whole key tiles, as equal as whole tiles allow
+                    sizes = [(x[1] - x[0] + 63) // 64 for x in ranges]
+                    assert max(sizes) - min(sizes) <= 1
                     assert any(list(c[:5]) == [r, h, cs, slots[0], len(slots)] for c in comb)
     assert not cover
+    if n_slots:  # a split batch runs as one round: at most one item per compute unit
+        assert n_live <= num_cus
+        slot_bytes = tc * (d + 1) * 4
+        assert ap.ws_bytes == n_slots * slot_bytes
+    else:
+        assert ap.ws_bytes == 0
     return ap
 
 
 def test_attention_plan_covers_every_tile_once():
     attention_plan_coverage([0, 64], [320], 4, 2, 64, 256)
     ap = attention_plan_coverage(np.cumsum([0] + [128] * 8).tolist(), [8320] * 8, 32, 8, 128, 256)
-    assert ap.n_combine > 0 and ap.ws_bytes > 0            # short suffixes: split key ranges
+    assert ap.n_combine == 128 and ap.ws_bytes > 0         # short suffixes: split key ranges
+    ap = attention_plan_coverage([0, 16], [32784], 32, 8, 128, 256)
+    assert ap.n_combine == 8 and ap.n_work <= 256           # one round of pieces
     ap = attention_plan_coverage([0, 2048, 4096, 6144, 8192], [34816] * 4, 64, 8, 128, 256)
     assert ap.n_combine == 0                                # plenty of tiles: no split
     rng = np.random.default_rng(3)
