@@ -11,7 +11,8 @@ continues across warm-up and timed steps).
 Other workloads (`--workload`): `docqa_hit` (8 cached 8192-token documents + fresh 128-token
 questions), `longctx` (70B-shaped layer, 64/8 heads: 4 cached 32768-token documents + fresh
 2048-token suffixes), `short32|short48|short64` (16 sessions per batch adding S new tokens to
-fully cached lognormal histories; KV-read bound), `multiturn` (64 conversation sessions,
+fully cached lognormal histories; KV-read bound), `decode` (64 sessions per batch adding one
+token each to fully cached lognormal histories, rotating over 256 sessions), `multiturn` (64 conversation sessions,
 lognormal histories, new turns of 32..512 tokens, cache 40 % of the histories; the first 256
 requests warm up) and `trace` (10,000-request replay over 500 Zipf(1.1) documents with 30 %
 one-off documents, cache 20 % of the recurring documents; the first 2,000 requests warm up, the
@@ -43,7 +44,8 @@ PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA (published)
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E (published)
 
 DEFAULT_STEPS = {"docqa": (48, 16), "docqa_hit": (20, 3), "longctx": (8, 2), "short32": (40, 4),
-                 "short48": (40, 4), "short64": (40, 4), "multiturn": (None, None), "trace": (40, None)}
+                 "short48": (40, 4), "short64": (40, 4), "decode": (40, 4), "multiturn": (None, None),
+                 "trace": (40, None)}
 
 
 def attn_flops(S, L, hq, d):
@@ -159,6 +161,13 @@ def make_workload(name: str, steps, warmup):
         desc = ("longctx: 70B-shaped layer, 64 q / 8 kv heads, head_dim 128, block 16; 4 cached "
                 "32768-token documents scattered over a 16384-block pool + fresh 2048-token suffixes")
         return cfg, warm + st_b[:warmup], st_b[warmup:], desc, "mfma", [], None
+    if name == "decode":
+        cfg = get_config("decode")
+        warm, st_b = st.steps_short(cfg, warmup + steps, 1, batch=cfg.max_batch, n_sessions=cfg.extra["n_sessions"])
+        desc = ("decode: 64 sessions/batch rotating over 256, each adding 1 new token to a fully cached "
+                "lognormal(7.5, 0.8) history (block-aligned, clipped to [256, 16384]); 32 q / 8 kv heads, "
+                "head_dim 128, block 16")
+        return cfg, warm + st_b[:warmup], st_b[warmup:], desc, "hbm", [], None
     if name.startswith("short"):
         S = int(name[5:])
         cfg = get_config("short")

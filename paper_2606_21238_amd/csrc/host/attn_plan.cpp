@@ -4,14 +4,18 @@
 // c = token * G + g (G query heads share a KV head, token-major), so the K/V tiles a work
 // item streams serve all G heads of its group at once.  The key range of a tile ends at the
 // last visible key of its last column (causal: suffix token i of a request with P cached
-// tokens sees keys 0..P+i).  Tiles are 256 columns wide, or 128 when no request of the batch
-// has more than 128 columns (short suffixes), so that no work-group computes on empty
-// columns.  When a batch has fewer tiles than compute units (short suffixes over long cached
+// tokens sees keys 0..P+i).  Tiles are 256 columns wide, 128 when no request of the batch has
+// more than 128 columns (short suffixes) and 32 when none has more than 32 (decode-like
+// batches), so that work-groups compute on few empty columns.  When a batch has fewer tiles than compute units (short suffixes over long cached
 // prefixes), tiles are split along the key range so that the whole batch runs as one round of
 // at most one item per compute unit: the smallest cap on key tiles per item (at least 8, i.e.
 // 512 keys) for which the pieces fit, each tile cut into equal pieces under the cap.  Split
 // items write fp32 partials plus a base-2 log-sum-exp, merged afterwards by one combine item
 // per tile.
+//
+// With at least as many tiles as compute units, a tile longer than one compute unit's share
+// of all key tiles (e.g. one long history in a decode batch) is cut to that share, so that it
+// does not set the length of the launch.
 //
 // Items are ordered longest key range first so the longest ones start first, and the order
 // is interleaved over the 8 XCDs (work-groups are dispatched round-robin over XCDs, each with
@@ -59,7 +63,9 @@ extern "C" int32_t arckv_attention_plan(const int32_t* cu_q, const int32_t* seq_
   int64_t max_cols = 0;
   for (int32_t r = 0; r < n_reqs; ++r)
     max_cols = std::max<int64_t>(max_cols, (static_cast<int64_t>(cu_q[r + 1]) - cu_q[r]) * G);
-  const int kCols = max_cols <= arckv::kNarrowCols ? arckv::kNarrowCols : arckv::kWideCols;
+  const int kCols = max_cols <= arckv::kTinyCols     ? arckv::kTinyCols
+                    : max_cols <= arckv::kNarrowCols ? arckv::kNarrowCols
+                                                     : arckv::kWideCols;
   *tile_cols = kCols;
 
   struct Tile { int32_t req, kvh, col_start, kv_end; };
@@ -82,20 +88,25 @@ extern "C" int32_t arckv_attention_plan(const int32_t* cu_q, const int32_t* seq_
   const int64_t target = static_cast<int64_t>(num_cus);  // one work-group per CU at a time
   auto key_tiles = [](const Tile& t) { return (static_cast<int64_t>(t.kv_end) + kKeyTile - 1) / kKeyTile; };
   int64_t cap = INT32_MAX;  // key tiles per item
-  if (base > 0 && base < target) {
+  if (base > 0) {
     int64_t total_t = 0, max_t = 0;
     for (const Tile& t : tiles) {
       total_t += key_tiles(t);
       max_t = std::max(max_t, key_tiles(t));
     }
-    int64_t lo = std::max<int64_t>(8, (total_t + target - 1) / target), hi = std::max(lo, max_t);
-    while (lo < hi) {  // smallest cap whose pieces fit in one round
-      const int64_t mid = (lo + hi) / 2;
-      int64_t cnt = 0;
-      for (const Tile& t : tiles) cnt += (key_tiles(t) + mid - 1) / mid;
-      if (cnt <= target) hi = mid; else lo = mid + 1;
+    const int64_t share = std::max<int64_t>(8, (total_t + target - 1) / target);
+    if (base < target) {
+      int64_t lo = share, hi = std::max(lo, max_t);
+      while (lo < hi) {  // smallest cap whose pieces fit in one round
+        const int64_t mid = (lo + hi) / 2;
+        int64_t cnt = 0;
+        for (const Tile& t : tiles) cnt += (key_tiles(t) + mid - 1) / mid;
+        if (cnt <= target) hi = mid; else lo = mid + 1;
+      }
+      cap = lo;
+    } else {
+      cap = share;  // several rounds: no item longer than one compute unit's share
     }
-    cap = lo;
   }
 
   std::vector<Item> items, combines;

@@ -9,12 +9,14 @@
 
 namespace arckv {
 
-// Query columns (token x query head of one KV group) per attention work-group: each wave64
-// owns kWaveCols columns; a work-group has 8 waves (wide tiles) or 4 waves (narrow tiles, for
-// batches whose suffixes are short).  Shared by the host work plan and the kernel.
+// Query columns (token x query head of one KV group) per attention work-group, shared by the
+// host work plan and the kernel: wide tiles (8 waves x 32 columns), narrow tiles for short
+// suffixes (4 x 32 columns, the 8 waves split over the keys of each K/V tile) and tiny tiles
+// for decode-like batches (32 columns, 2 waves split over the keys).
 constexpr int kWaveCols = 32;
 constexpr int kWideCols = 8 * kWaveCols;
 constexpr int kNarrowCols = 4 * kWaveCols;
+constexpr int kTinyCols = kWaveCols;
 
 // Records a thread-local message for arckv_last_error() and returns `code`.
 int32_t fail(int32_t code, const char* fmt, ...) __attribute__((format(printf, 2, 3)));

@@ -8,12 +8,13 @@
 // Sec. 4; layout V1: K [blk][kvh][16][D], V [blk][kvh][D][16]).
 //
 // Design (MI355X-first):
-//  * One work-group = 8 wave64s (two per SIMD) = one query tile of one (request, KV head); a
+//  * One work-group = one query tile of one (request, KV head); a
 //    column is (token, head-of-group), token-major, so every K/V tile a work-group loads
 //    serves all G query heads of its KV head (GQA packed into the MFMA N dimension).  Wide
 //    tiles: 8 waves x 32 columns.  Narrow tiles (short suffixes): 4 x 32 columns, the two
 //    groups of 4 waves taking the two 32-key halves of every K/V tile with separate online
-//    softmax states that merge through LDS at the end.
+//    softmax states that merge through LDS at the end.  Tiny tiles (decode-like batches):
+//    32 columns, two waves taking the two key halves.
 //  * Transposed formulation: S^T = K . Q^T and O^T = V^T . P^T with v_mfma_f32_32x32x16_bf16.
 //    Query columns sit on lanes, keys / head dims on the M (register) dimension, so a lane
 //    owns whole columns: row max and row sum are in-lane plus one exchange with lane +- 32.
@@ -660,7 +661,7 @@ int32_t prefill_attention(const void* k_pool, const void* v_pool, const void* q,
     return arckv::fail(ARCKV_EUNSUPPORTED, "prefill_attention: head_dim %d not in {64,128}", head_dim);
   if (G != 1 && G != 2 && G != 4 && G != 8)
     return arckv::fail(ARCKV_EUNSUPPORTED, "prefill_attention: group size %d not in {1,2,4,8}", G);
-  if (tile_cols != arckv::kWideCols && tile_cols != arckv::kNarrowCols)
+  if (tile_cols != arckv::kWideCols && tile_cols != arckv::kNarrowCols && tile_cols != arckv::kTinyCols)
     return arckv::fail(ARCKV_EINVAL, "prefill_attention: tile_cols %d is not a planned width", tile_cols);
   if (n_work == 0 && n_combine == 0) {  // nothing to run; the events still mark the stream
     for (hipEvent_t ev : {ev_begin, ev_mid, ev_end})
@@ -697,6 +698,10 @@ int32_t prefill_attention(const void* k_pool, const void* v_pool, const void* q,
   do {                                                                                         \
     if (tile_cols == arckv::kWideCols)                                                         \
       launch_attn<DD, GG, kWideWaves, kWideNB, 1>(grid, st, kp, vp, qp, op, block_tables, bt_stride, cu_q, seq_lens, \
+                             n_reqs, wk, n_q, num_blocks, num_q_heads, num_kv_heads,           \
+                             scale_log2, ws_o, ws_lse, ws_slots);                              \
+    else if (tile_cols == arckv::kTinyCols)                                                    \
+      launch_attn<DD, GG, 2, 1, 2>(grid, st, kp, vp, qp, op, block_tables, bt_stride, cu_q, seq_lens, \
                              n_reqs, wk, n_q, num_blocks, num_q_heads, num_kv_heads,           \
                              scale_log2, ws_o, ws_lse, ws_slots);                              \
     else                                                                                       \

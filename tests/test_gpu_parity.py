@@ -132,6 +132,9 @@ SWEEP = [
     ([(2000, 1536)], 16, 2, 64),
     ([(700, 0), (33, 32), (1, 0)], 8, 8, 128),
     ([(5000, 4990)], 8, 2, 128),                 # many pieces per tile
+    # decode-like batches (one new token per request: 32-column tiles)
+    ([(L, L - 1) for L in (1, 2, 17, 64, 65, 300, 1024, 2049, 4097, 777, 33, 16)], 32, 8, 128),
+    ([(L, L - 2) for L in (2, 3, 40, 129, 1500, 3001)], 16, 2, 64),
 ]
 
 

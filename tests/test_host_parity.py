@@ -189,10 +189,10 @@ def attention_plan_coverage(cu_q, seq_lens, hq, hkv, d, num_cus):
     g = hq // hkv
     tc = ap.tile_cols
     max_cols = max(int(cu_q[r + 1] - cu_q[r]) * g for r in range(len(seq_lens)))
-    assert tc == (128 if max_cols <= 128 else 256)
+    assert tc == (32 if max_cols <= 32 else 128 if max_cols <= 128 else 256)
     items = ap.work[: ap.n_work]
     comb = ap.work[ap.n_work: ap.n_work + ap.n_combine]
-    cover, n_live, n_slots = {}, 0, 0
+    cover, n_live, n_slots, max_piece = {}, 0, 0, 0
     for it in items:
         req, kvh, cs, a, b, slot = (int(x) for x in it[:6])
         if req < 0:
@@ -200,13 +200,17 @@ def attention_plan_coverage(cu_q, seq_lens, hq, hkv, d, num_cus):
         n_live += 1
         n_slots += slot >= 0
         assert a % 64 == 0 and b > a
+        max_piece = max(max_piece, (b - a + 63) // 64)
         cover.setdefault((req, kvh, cs), []).append((a, b, slot))
+    n_tiles, total_tiles = 0, 0
     for r in range(len(seq_lens)):
         S = cu_q[r + 1] - cu_q[r]
         P = seq_lens[r] - S
         for cs in range(0, S * g, tc):
             last = min(cs + tc, S * g) - 1
             kv_end = P + last // g + 1
+            n_tiles += hkv
+            total_tiles += hkv * (-(-kv_end // 64))
             for h in range(hkv):
                 ranges = sorted(cover.pop((r, h, cs)))
                 assert ranges[0][0] == 0 and ranges[-1][1] == kv_end
@@ -221,8 +225,13 @@ def attention_plan_coverage(cu_q, seq_lens, hq, hkv, d, num_cus):
                     assert max(sizes) - min(sizes) <= 1
                     assert any(list(c[:5]) == [r, h, cs, slots[0], len(slots)] for c in comb)
     assert not cover
-    if n_slots:  # a split batch runs as one round: at most one item per compute unit
-        assert n_live <= num_cus
+    base = n_tiles
+    share = max(8, -(-total_tiles // num_cus))
+    if base < num_cus:
+        assert n_live <= num_cus          # split into one round: at most one item per CU
+    else:
+        assert max_piece <= max(share, 1)  # several rounds: no piece beyond one CU's share
+    if n_slots:
         slot_bytes = tc * (d + 1) * 4
         assert ap.ws_bytes == n_slots * slot_bytes
     else:

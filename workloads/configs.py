@@ -62,6 +62,12 @@ CONFIGS = {
     #    64 histories.
     "short": Config("short", 1003, 32, 8, 128, capacity=16384, scratch=16, num_phys=16400, max_batch=16,
                     extra=dict(hist_mu=7.5, hist_sigma=0.8, hist_min=256, hist_max=16384)),
+    # decode: one new token per request over a fully cached history (the KV-read-bound end of
+    #    short suffixes): 256 sessions with lognormal(7.5, 0.8) histories clipped to [256, 16384]
+    #    and rounded down to whole blocks, batches of 64 sessions rotating over all 256 (about
+    #    2.7 GB of K/V in the pool, so consecutive steps read different KV).
+    "decode": Config("decode", 1008, 32, 8, 128, capacity=65536, scratch=64, num_phys=65600, max_batch=64,
+                     extra=dict(hist_mu=7.5, hist_sigma=0.8, hist_min=256, hist_max=16384, n_sessions=256)),
     # 5: trace replay: 10,000 requests over 500 documents of U[4096, 16384] tokens,
     #    Zipf(1.1) popularity, 30 % one-off documents; capacity 20 % of the working set.
     "trace": Config("trace", 1005, 32, 8, 128, capacity=0, scratch=16, num_phys=0, max_batch=16,
