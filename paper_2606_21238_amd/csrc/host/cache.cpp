@@ -119,6 +119,8 @@ struct arckv_cache {
 
   uint64_t epoch = 1;
   bool in_flight = false;
+  int32_t scan_from[5] = {-1, -1, -1, -1, -1};  // per list: see lru_unpinned
+  uint64_t scan_epoch[5] = {0, 0, 0, 0, 0};
 
   arckv_event* log_buf = nullptr;
   int64_t log_cap = 0;
@@ -131,6 +133,9 @@ struct arckv_cache {
   // ---- list primitives ----------------------------------------------------------------
   void unlink(int32_t n) {
     Node& x = nodes[n];
+    if ((x.list == ARCKV_LIST_T1 || x.list == ARCKV_LIST_T2) && scan_epoch[x.list] == epoch &&
+        scan_from[x.list] == n)
+      scan_from[x.list] = x.next;  // every node before the successor is still pinned
     List& l = lists[x.list];
     if (x.prev >= 0) nodes[x.prev].next = x.next; else l.head = x.next;
     if (x.next >= 0) nodes[x.next].prev = x.prev; else l.tail = x.prev;
@@ -165,10 +170,21 @@ struct arckv_cache {
     free_nodes.push_back(n);
   }
   bool pinned(int32_t n) const { return in_flight && nodes[n].pin_epoch == epoch; }
-  int32_t lru_unpinned(int32_t list) const {
-    for (int32_t n = lists[list].head; n >= 0; n = nodes[n].next)
-      if (!pinned(n)) return n;
-    return -1;
+  // LRU-most unpinned page of T1 or T2.  Within a batch, pins are only added and every page
+  // that enters T1 / T2 is pinned right away, so the pinned run at the LRU end only grows:
+  // scan_from[list] (valid for the current epoch) is where the last scan stopped, and every
+  // page before it is pinned.  Each batch therefore walks a pinned page at most once instead
+  // of once per eviction.
+  int32_t lru_unpinned(int32_t list) {
+    const bool cached = in_flight && (list == ARCKV_LIST_T1 || list == ARCKV_LIST_T2) &&
+                        scan_epoch[list] == epoch;
+    int32_t n = cached ? scan_from[list] : lists[list].head;
+    while (n >= 0 && pinned(n)) n = nodes[n].next;
+    if (in_flight && (list == ARCKV_LIST_T1 || list == ARCKV_LIST_T2)) {
+      scan_from[list] = n;
+      scan_epoch[list] = epoch;
+    }
+    return n;
   }
   int32_t find(uint64_t key) const {
     return index.find(key);

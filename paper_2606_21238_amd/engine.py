@@ -52,11 +52,13 @@ class PrefillEngine:
             num_cus = torch.cuda.get_device_properties(self.device).multi_processor_count
         self.num_cus = int(num_cus)
         self._ws = torch.empty(0, dtype=torch.uint8, device=self.device)
-        # two reusable pinned staging buffers (one may still feed an in-flight copy) and the
-        # events that mark their copies done; allocating pinned memory per batch would stall
-        self._stage = [None, None]
-        self._stage_ev = [None, None]
-        self._dev_meta = [None, None]
+        # a ring of reusable pinned staging buffers and device metadata buffers, with the events
+        # that mark their copies done: the host may prepare up to four batches ahead of the GPU
+        # (a slow host step is then absorbed), and no pinned memory is allocated per batch
+        self._ring = 4
+        self._stage = [None] * self._ring
+        self._stage_ev = [None] * self._ring
+        self._dev_meta = [None] * self._ring
         self._turn = 0
 
     # ---- host steps ----------------------------------------------------------------------
@@ -73,7 +75,7 @@ class PrefillEngine:
         parts = [plan.block_tables.ravel(), plan.cu_q, plan.seq_lens, plan.slot_mapping, ap.work.ravel()]
         n_int = sum(p.size for p in parts)
         t = self._turn
-        self._turn ^= 1
+        self._turn = (t + 1) % self._ring
         if self._stage_ev[t] is not None:
             self._stage_ev[t].synchronize()          # the copy that last read this buffer is done
         if self._stage[t] is None or self._stage[t].numel() < n_int:
