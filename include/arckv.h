@@ -256,7 +256,9 @@ int32_t arckv_attention_plan(const int32_t* cu_q, const int32_t* seq_lens, int32
  * device [n_reqs] (the same values given to arckv_attention_plan).  work: device copy of
  * the plan's items, tile_cols: the plan's tile width.  workspace: device, >= the planned
  * ws_bytes (may be NULL if 0).  Calls that overlap in time must not share a workspace.
- * Block-table entries outside [0, num_blocks) are read as zero keys/values.
+ * A block-table entry outside [0, num_blocks) is never dereferenced: the kernel reads block 0
+ * in its place, so the keys it covers get unspecified (finite or not) values; entries past a
+ * request's last block (the -1 padding of a plan's rows) are not read at all.
  * head_dim in {64, 128}; num_q_heads / num_kv_heads in {1, 2, 4, 8}. */
 int32_t arckv_prefill_attention(const void* k_pool, const void* v_pool, const void* q, void* out,
                                 const int32_t* block_tables, int32_t bt_stride,

@@ -135,6 +135,13 @@ SWEEP = [
     # decode-like batches (one new token per request: 32-column tiles)
     ([(L, L - 1) for L in (1, 2, 17, 64, 65, 300, 1024, 2049, 4097, 777, 33, 16)], 32, 8, 128),
     ([(L, L - 2) for L in (2, 3, 40, 129, 1500, 3001)], 16, 2, 64),
+    # G = 4 at d = 64; column counts on and just past each tile width (32, 128, 256 columns)
+    ([(900, 892), (70, 62)], 8, 2, 64),                 # 32 columns: tiny tiles
+    ([(900, 891), (77, 68)], 8, 2, 64),                 # 36 columns: narrow tiles
+    ([(700, 668), (1000, 968)], 16, 4, 64),             # 128 columns: narrow tiles
+    ([(700, 667), (64, 31)], 16, 4, 64),                # 132 columns: wide tiles
+    ([(512, 448), (2048, 1984), (65, 1)], 32, 8, 128),  # 256 columns: wide tiles, one tile each
+    ([(513, 448), (130, 65)], 32, 8, 128),              # 260 columns: a second, 4-column tile
 ]
 
 
