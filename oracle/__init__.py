@@ -27,12 +27,15 @@ Contents, each module citing the passage of the paper it follows:
 * ``attention`` -- fp64 causal softmax attention of the uncached suffix over
   the gathered contiguous K/V (Sec. 2: prefill processes the prompt; with a
   cached prefix only the uncached tokens are computed).
+* ``qkv`` -- the producer of the computed tokens' Q/K/V: projection of their
+  hidden states and rotary position embedding (Sec. 4 serves Qwen3-14B; the
+  layer details are this project's reading of the public model configuration).
 
 Parity status: every function here is pinned by ``tests/test_oracle_*.py``
 against values fixed by the mathematics or by hand-derived traces; none is
 "parity unpinned".
 """
 
-from . import blockhash, arc, lru, planner, kvpool, attention  # noqa: F401
+from . import blockhash, arc, lru, planner, kvpool, attention, qkv  # noqa: F401
 
-__all__ = ["blockhash", "arc", "lru", "planner", "kvpool", "attention"]
+__all__ = ["blockhash", "arc", "lru", "planner", "kvpool", "attention", "qkv"]
