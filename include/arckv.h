@@ -282,6 +282,31 @@ int32_t arckv_prefill_attention_timed(const void* k_pool, const void* v_pool, co
                                       float scale, void* workspace, int64_t ws_bytes, void* stream,
                                       void* ev_begin, void* ev_mid, void* ev_end);
 
+/* ---------------------------------------------------------------------------------------
+ * Device: the producer of the computed tokens' Q/K/V (the attention inputs of a prefill;
+ * Sec. 4 serves Qwen3-14B, whose public configuration fixes the details): projection of the
+ * hidden states and rotary position embedding.
+ *   y = x W^T (rocBLAS, bf16 in and out, fp32 accumulate), then for every query and key head
+ *   at the token's absolute position p (request r's suffix token i: L_r - S_r + i) and
+ *   i < head_dim / 2, angle a = p * rope_theta^(-2 i / head_dim):
+ *   out[i] = u[i] cos a - u[i + D/2] sin a,  out[i + D/2] = u[i + D/2] cos a + u[i] sin a
+ *   (angles in fp64, reduced mod 2 pi, then fp32 sine / cosine and rotation); values pass
+ *   through.  Outputs bf16, round to nearest even.
+ * x: device bf16 [n_tokens][hidden], rows ordered by cu_q.  w_qkv: device bf16
+ * [(num_q_heads + 2 num_kv_heads) head_dim][hidden] (query heads, then key heads, then value
+ * heads).  cu_q [n_reqs + 1], seq_lens [n_reqs]: device, as for the attention call
+ * (n_tokens = cu_q[n_reqs]).  y_workspace: device, >= 2 n_tokens (num_q_heads + 2
+ * num_kv_heads) head_dim bytes, caller-owned.  q_out: device bf16 [n_tokens][num_q_heads]
+ * [head_dim]; k_out, v_out: device bf16 [n_tokens][num_kv_heads][head_dim] (the layout
+ * arckv_kv_scatter takes).  Stream-ordered on `stream`.  head_dim in {64, 128}: else
+ * EUNSUPPORTED; EINVAL on bad sizes, NULL pointers or rope_theta <= 1; ENOSPC if the workspace
+ * is too small; EDEVICE if rocBLAS or a launch fails.  n_tokens = 0 is a no-op. */
+int32_t arckv_qkv_rope(const void* x, const void* w_qkv, int64_t n_tokens, int32_t hidden,
+                       int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                       const int32_t* cu_q, const int32_t* seq_lens, int32_t n_reqs,
+                       double rope_theta, void* y_workspace, int64_t ws_bytes, void* q_out,
+                       void* k_out, void* v_out, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

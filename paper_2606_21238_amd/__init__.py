@@ -222,6 +222,29 @@ def kv_scatter(k_pool, v_pool, k_new, v_new, slot_mapping, stream=None):
                                       hkv, d, C.c_void_p(_stream(stream))), "arckv_kv_scatter")
 
 
+def qkv_rope(x, w_qkv, cu_q, seq_lens, num_q_heads: int, num_kv_heads: int, rope_theta: float,
+             q_out, k_out, v_out, workspace, stream=None):
+    """Projection + rotary embedding of the computed tokens (arckv_qkv_rope).  Device tensors:
+    x [T, H] bf16, w_qkv [(Hq + 2 Hkv) D, H] bf16, cu_q [n+1], seq_lens [n] int32, q_out
+    [T, Hq, D], k_out / v_out [T, Hkv, D] bf16, workspace >= 2 T (Hq + 2 Hkv) D bytes."""
+    t, h = int(x.shape[0]), int(x.shape[1])
+    d = int(q_out.shape[2])
+    n_out = (num_q_heads + 2 * num_kv_heads) * d
+    if tuple(w_qkv.shape) != (n_out, h):
+        raise ValueError(f"w_qkv must be [{n_out}, {h}]")
+    if tuple(q_out.shape) != (t, num_q_heads, d) or tuple(k_out.shape) != (t, num_kv_heads, d) \
+            or tuple(v_out.shape) != (t, num_kv_heads, d):
+        raise ValueError("q_out / k_out / v_out shapes do not match x and the head counts")
+    if cu_q.numel() != seq_lens.numel() + 1:
+        raise ValueError("cu_q must have len(seq_lens) + 1 entries")
+    _lib.check(lib().arckv_qkv_rope(
+        _dev(x, 16, "x"), _dev(w_qkv, 16, "w_qkv"), t, h, num_q_heads, num_kv_heads, d,
+        _dev(cu_q, 32, "cu_q"), _dev(seq_lens, 32, "seq_lens"), int(seq_lens.numel()), float(rope_theta),
+        _dev(workspace, None, "workspace"), int(workspace.numel() * workspace.element_size()),
+        _dev(q_out, 16, "q_out"), _dev(k_out, 16, "k_out"), _dev(v_out, 16, "v_out"),
+        C.c_void_p(_stream(stream))), "arckv_qkv_rope")
+
+
 @dataclass
 class AttnPlan:
     work: np.ndarray     # int32 [n_work + n_combine, 8]

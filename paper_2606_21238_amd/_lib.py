@@ -61,6 +61,7 @@ _SIGS = {
     "arckv_cache_snapshot": (i32, [vp, i32, P_u64, P_i32, i64, P_i64]),
     "arckv_pool_bytes": (i64, [i64, i32, i32]),
     "arckv_kv_scatter": (i32, [vp, vp, vp, vp, vp, i64, i64, i32, i32, vp]),
+    "arckv_qkv_rope": (i32, [vp, vp, i64, i32, i32, i32, i32, vp, vp, i32, f64, vp, i64, vp, vp, vp, vp]),
     "arckv_attention_plan": (i32, [P_i32, P_i32, i32, i32, i32, i32, i32, P_i32, i64, P_i64, P_i64,
                                    P_i64, P_i32]),
     "arckv_prefill_attention": (i32, [vp, vp, vp, vp, vp, i32, vp, vp, i32, i64, i64, vp, i64, i64,

@@ -23,7 +23,7 @@ LIB = os.path.join(LIBDIR, "libarckv.so")
 ARCH = "gfx950"
 
 HOST_SRC = ["host/blockhash.cpp", "host/cache.cpp", "host/attn_plan.cpp", "host/errors.cpp"]
-HIP_SRC = ["kernels/kv_scatter.hip", "kernels/prefill_attn.hip"]
+HIP_SRC = ["kernels/kv_scatter.hip", "kernels/prefill_attn.hip", "kernels/qkv_rope.hip"]
 
 
 def _hipcc() -> str:
@@ -67,7 +67,8 @@ def build(verbose: bool = False) -> str:
             if o.strip():
                 print(o)
     tmp = LIB + ".tmp"
-    _run([hipcc, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp])
+    # rocBLAS for the one plain GEMM (the Q/K/V projection)
+    _run([hipcc, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-lrocblas", "-o", tmp])
     os.replace(tmp, LIB)
     return LIB
 

@@ -54,3 +54,13 @@ def test_device_calls_validate_arguments_without_touching_a_device():
 def test_missing_library_fails_loudly(tmp_path):
     with pytest.raises(RuntimeError, match="not built"):
         _lib.load(str(tmp_path / "nope.so"))
+
+
+def test_qkv_rope_validates_arguments_without_touching_a_device():
+    L = ak.lib()
+    args = lambda d, theta, t=4: (None, None, t, 64, 4, 2, d, None, None, 1, theta, None, 0, None, None, None, None)
+    assert L.arckv_qkv_rope(*args(96, 1.0e6)) == _lib.EUNSUPPORTED
+    assert L.arckv_qkv_rope(*args(128, 1.0)) == _lib.EINVAL
+    assert L.arckv_qkv_rope(*args(128, 1.0e6)) == _lib.EINVAL          # NULL pointers
+    assert b"NULL" in L.arckv_last_error()
+    assert L.arckv_qkv_rope(*args(128, 1.0e6, t=0)) == _lib.OK         # nothing to do
