@@ -12,7 +12,9 @@ Other workloads (`--workload`): `docqa_hit` (8 cached 8192-token documents + fre
 questions), `longctx` (70B-shaped layer, 64/8 heads: 4 cached 32768-token documents + fresh
 2048-token suffixes), `short32|short48|short64` (16 sessions per batch adding S new tokens to
 fully cached lognormal histories; KV-read bound), `decode` (64 sessions per batch adding one
-token each to fully cached lognormal histories, rotating over 256 sessions), `multiturn` (64 conversation sessions,
+token each to fully cached lognormal histories, rotating over 256 sessions), `docqa14b`
+(the docqa stream on a Qwen3-14B-shaped layer, 40 / 8 heads, hidden 5120, with the Q/K/V
+projection and rotary embedding of the computed tokens in every step), `multiturn` (64 conversation sessions,
 lognormal histories, new turns of 32..512 tokens, cache 40 % of the histories; the first 256
 requests warm up) and `trace` (10,000-request replay over 500 Zipf(1.1) documents with 30 %
 one-off documents, cache 20 % of the recurring documents; the first 2,000 requests warm up, the
@@ -43,7 +45,7 @@ sys.path.insert(0, ROOT)
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA (published)
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E (published)
 
-DEFAULT_STEPS = {"docqa": (48, 16), "docqa_hit": (20, 3), "longctx": (8, 2), "short32": (40, 4),
+DEFAULT_STEPS = {"docqa": (48, 16), "docqa14b": (48, 16), "docqa_hit": (20, 3), "longctx": (8, 2), "short32": (40, 4),
                  "short48": (40, 4), "short64": (40, 4), "decode": (40, 4), "multiturn": (None, None),
                  "trace": (40, None)}
 
@@ -149,6 +151,15 @@ def make_workload(name: str, steps, warmup):
                 "question; 32 q / 8 kv heads, head_dim 128, block 16; KV pool 25% of document tokens "
                 "(8192 blocks)")
         return cfg, b[:warmup], b[warmup:], desc, "mfma", [], None
+    if name == "docqa14b":
+        cfg = get_config("docqa14b")
+        stream = st.stream_docqa(cfg, n_batches=warmup + steps)
+        b = [stream[i * cfg.max_batch:(i + 1) * cfg.max_batch] for i in range(warmup + steps)]
+        desc = ("docqa14b: the docqa stream (8 requests/batch, 8192-token documents drawn Zipf(1.1) from 64 + "
+                "128-token question, KV pool 25% of document tokens) on a Qwen3-14B-shaped layer: hidden 5120, "
+                "40 q / 8 kv heads, head_dim 128; each step projects the computed tokens' hidden states to "
+                "Q/K/V (rotary base 1e6), scatters K/V and runs attention")
+        return cfg, b[:warmup], b[warmup:], desc, "mfma", [], None
     if name == "docqa_hit":
         cfg = get_config("docqa")
         warm, st_b = st.steps_docqa_hit(cfg, warmup + steps)
@@ -241,10 +252,29 @@ def main():
 
     # stream workloads touch far more distinct sources than fit in HBM at once
     bank = TensorBank(cfg, "cuda", max_sources=64 if host_tail or warm_requests is not None else 1 << 30)
+    layer = "hidden" in cfg.extra            # the step starts from hidden states (Q/K/V projection)
+    if layer:
+        hidden, theta = cfg.extra["hidden"], cfg.extra["rope_theta"]
+        gen = torch.Generator(device="cuda")
+        gen.manual_seed(cfg.seed)
+        w_qkv = (torch.randn(((hq + 2 * hkv) * d, hidden), generator=gen, device="cuda")
+                 * hidden ** -0.5).to(torch.bfloat16)
+
+    def stage(i):
+        if not layer:
+            q, kn, vn = bank.batch_suffix(batches[i], prefix[i])
+            return (q, kn, vn, torch.empty_like(q), None)
+        n = sum(r.n_tokens - p for r, p in zip(batches[i], prefix[i]))
+        g = torch.Generator(device="cuda")
+        g.manual_seed(cfg.seed * 1000003 + i)
+        x = torch.randn((n, hidden), generator=g, device="cuda").to(torch.bfloat16)
+        q = torch.empty((n, hq, d), dtype=torch.bfloat16, device="cuda")
+        kn = torch.empty((n, hkv, d), dtype=torch.bfloat16, device="cuda")
+        return (q, kn, torch.empty_like(kn), torch.empty_like(q), x)
+
     staged = [None] * len(batches)
     for i in range(n_untimed, len(batches)):
-        q, kn, vn = bank.batch_suffix(batches[i], prefix[i])
-        staged[i] = (q, kn, vn, torch.empty_like(q))
+        staged[i] = stage(i)
     torch.cuda.synchronize()
 
     if args.copy_calibration_mib:
@@ -262,9 +292,8 @@ def main():
 
     def step(i, ev=None):
         if staged[i] is None:                       # untimed batches are staged just in time
-            q, kn, vn = bank.batch_suffix(batches[i], prefix[i])
-            staged[i] = (q, kn, vn, torch.empty_like(q))
-        q, kn, vn, out = staged[i]
+            staged[i] = stage(i)
+        q, kn, vn, out, x = staged[i]
         h0 = time.perf_counter()
         plan = eng.plan(tokens[i])
         h1 = time.perf_counter()
@@ -272,8 +301,12 @@ def main():
         h2 = time.perf_counter()
         if ev is not None:
             ev[0].record()
+        if layer:
+            eng.project(db, x, w_qkv, q, kn, vn, theta)
+        if ev is not None:
+            ev[1].record()
         eng.scatter(db, kn, vn)
-        eng.attention(db, q, out, events=None if ev is None else ev[1:])
+        eng.attention(db, q, out, events=None if ev is None else ev[2:])
         h3 = time.perf_counter()
         eng.release()
         h4 = time.perf_counter()
@@ -284,7 +317,7 @@ def main():
             host_t["release"] += h4 - h3
         return plan, db
 
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(steps)]
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(steps)]
     for evs in events:          # a first record creates each event's HIP handle
         for e in evs:
             e.record()
@@ -314,9 +347,11 @@ def main():
         L_list.append(plan.seq_lens.astype(np.int64))
     F = [attn_flops(S, L, hq, d) for S, L in zip(S_list, L_list)]
     B = [attn_bytes(S, L, hq, hkv, d) for S, L in zip(S_list, L_list)]
-    t_scatter = [e[0].elapsed_time(e[1]) * 1e-3 for e in events]
-    t_attn = [e[1].elapsed_time(e[2]) * 1e-3 for e in events]        # prefill_attn kernel
-    t_comb = [e[2].elapsed_time(e[3]) * 1e-3 for e in events]        # split-KV combine (if any)
+    t_proj = [e[0].elapsed_time(e[1]) * 1e-3 for e in events]        # Q/K/V projection (layer)
+    t_scatter = [e[1].elapsed_time(e[2]) * 1e-3 for e in events]
+    t_attn = [e[2].elapsed_time(e[3]) * 1e-3 for e in events]        # prefill_attn kernel
+    t_comb = [e[3].elapsed_time(e[4]) * 1e-3 for e in events]        # split-KV combine (if any)
+    proj_f = [2.0 * float(np.sum(S)) * cfg.extra["hidden"] * (hq + 2 * hkv) * d for S in S_list] if layer else []
     total_f = float(np.sum(F))
     suffix_tokens = int(sum(int(s.sum()) for s in S_list))
     roof_t = [max(f / (PEAK_BF16_TFLOPS * 1e12), b / (PEAK_HBM_GBS * 1e9)) for f, b in zip(F, B)]
@@ -334,7 +369,7 @@ def main():
 
     result = {
         "metric": "prefix-cached prefill attn TFLOP/s & % MI355X roofline; suffix tokens/s",
-        "value": round(total_f / wall / 1e12, 2),
+        "value": round((total_f + float(np.sum(proj_f))) / wall / 1e12, 2),
         "unit": "TFLOP/s",
         "n_gpus": 1,
         "steps": steps,
@@ -386,6 +421,19 @@ def main():
         "work_items_per_step": [int(np.mean([w for w, _ in n_work])), int(np.mean([c for _, c in n_work]))],
     }
 
+    if layer:
+        result["layer"] = {
+            "what": "per step: Q/K/V projection (rocBLAS GEMM + rotary/split kernel), KV scatter, "
+                    "attention, combine; value counts projection + attention flops",
+            "projection_tflops": round(float(np.sum(proj_f)) / float(np.sum(t_proj)) / 1e12, 2),
+            "projection_frac_of_bf16_peak": round(float(np.sum(proj_f)) / float(np.sum(t_proj)) / 1e12
+                                                  / PEAK_BF16_TFLOPS, 4),
+            "projection_ms": round(float(np.mean(t_proj)) * 1e3, 4),
+            "layer_gpu_ms": round(float(np.mean([a + b + c + e for a, b, c, e in
+                                                 zip(t_proj, t_scatter, t_attn, t_comb)])) * 1e3, 4),
+            "computed_tokens_per_step": int(np.mean([int(np.sum(S)) for S in S_list])),
+        }
+
     if warm_requests is not None:
         # the whole stream after its warm-up requests, replayed on the host for both policies
         result["cache"]["hit_rate_stream_after_warmup"] = {
@@ -394,11 +442,11 @@ def main():
             "requests": int(s_end["requests"] - s_sw["requests"]),
         }
 
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and not layer:   # (the layer workload's K/V come from its projection)
         # bounded oracle sample: the first timed batch's requests, 16 query rows at a time
         k = 0
         plan = plans[k]
-        q, _, _, _ = staged[n_untimed + k]
+        q = staged[n_untimed + k][0]
         qb = bits(q)
         sample = []
         for r, req in enumerate(timed[k]):

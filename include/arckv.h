@@ -259,7 +259,7 @@ int32_t arckv_attention_plan(const int32_t* cu_q, const int32_t* seq_lens, int32
  * A block-table entry outside [0, num_blocks) is never dereferenced: the kernel reads block 0
  * in its place, so the keys it covers get unspecified (finite or not) values; entries past a
  * request's last block (the -1 padding of a plan's rows) are not read at all.
- * head_dim in {64, 128}; num_q_heads / num_kv_heads in {1, 2, 4, 8}. */
+ * head_dim in {64, 128}; num_q_heads / num_kv_heads in {1, 2, 4, 5, 8}. */
 int32_t arckv_prefill_attention(const void* k_pool, const void* v_pool, const void* q, void* out,
                                 const int32_t* block_tables, int32_t bt_stride,
                                 const int32_t* cu_q, const int32_t* seq_lens, int32_t n_reqs,

@@ -54,8 +54,8 @@ extern "C" int32_t arckv_attention_plan(const int32_t* cu_q, const int32_t* seq_
   if (num_q_heads % num_kv_heads != 0)
     return arckv::fail(ARCKV_EINVAL, "attention_plan: num_q_heads %% num_kv_heads != 0");
   const int G = num_q_heads / num_kv_heads;
-  if (G != 1 && G != 2 && G != 4 && G != 8)
-    return arckv::fail(ARCKV_EUNSUPPORTED, "attention_plan: group size %d not in {1,2,4,8}", G);
+  if (G != 1 && G != 2 && G != 4 && G != 5 && G != 8)
+    return arckv::fail(ARCKV_EUNSUPPORTED, "attention_plan: group size %d not in {1,2,4,5,8}", G);
   if (head_dim != 64 && head_dim != 128)
     return arckv::fail(ARCKV_EUNSUPPORTED, "attention_plan: head_dim %d not in {64,128}", head_dim);
   if (n_reqs > 0 && cu_q[0] != 0) return arckv::fail(ARCKV_EINVAL, "attention_plan: cu_q[0] != 0");

@@ -659,8 +659,8 @@ int32_t prefill_attention(const void* k_pool, const void* v_pool, const void* q,
   const int G = num_q_heads / num_kv_heads;
   if (head_dim != 64 && head_dim != 128)
     return arckv::fail(ARCKV_EUNSUPPORTED, "prefill_attention: head_dim %d not in {64,128}", head_dim);
-  if (G != 1 && G != 2 && G != 4 && G != 8)
-    return arckv::fail(ARCKV_EUNSUPPORTED, "prefill_attention: group size %d not in {1,2,4,8}", G);
+  if (G != 1 && G != 2 && G != 4 && G != 5 && G != 8)
+    return arckv::fail(ARCKV_EUNSUPPORTED, "prefill_attention: group size %d not in {1,2,4,5,8}", G);
   if (tile_cols != arckv::kWideCols && tile_cols != arckv::kNarrowCols && tile_cols != arckv::kTinyCols)
     return arckv::fail(ARCKV_EINVAL, "prefill_attention: tile_cols %d is not a planned width", tile_cols);
   if (n_work == 0 && n_combine == 0) {  // nothing to run; the events still mark the stream
@@ -714,6 +714,7 @@ int32_t prefill_attention(const void* k_pool, const void* v_pool, const void* q,
         case 1: ARCKV_LAUNCH(64, 1); break;
         case 2: ARCKV_LAUNCH(64, 2); break;
         case 4: ARCKV_LAUNCH(64, 4); break;
+        case 5: ARCKV_LAUNCH(64, 5); break;
         default: ARCKV_LAUNCH(64, 8); break;
       }
     } else {
@@ -721,6 +722,7 @@ int32_t prefill_attention(const void* k_pool, const void* v_pool, const void* q,
         case 1: ARCKV_LAUNCH(128, 1); break;
         case 2: ARCKV_LAUNCH(128, 2); break;
         case 4: ARCKV_LAUNCH(128, 4); break;
+        case 5: ARCKV_LAUNCH(128, 5); break;
         default: ARCKV_LAUNCH(128, 8); break;
       }
     }

@@ -52,6 +52,7 @@ class PrefillEngine:
             num_cus = torch.cuda.get_device_properties(self.device).multi_processor_count
         self.num_cus = int(num_cus)
         self._ws = torch.empty(0, dtype=torch.uint8, device=self.device)
+        self._y = None          # projection output of the batch (arckv_qkv_rope workspace)
         # a ring of reusable pinned staging buffers and device metadata buffers, with the events
         # that mark their copies done: the host may prepare up to four batches ahead of the GPU
         # (a slow host step is then absorbed), and no pinned memory is allocated per batch
@@ -123,6 +124,28 @@ class PrefillEngine:
                                           v_new.data_ptr(), db.slot_mapping.data_ptr(), db.n_tokens,
                                           self.num_phys, self.hkv, self.d, self._stream(stream)),
                    "arckv_kv_scatter")
+
+    def project(self, db: DeviceBatch, x, w_qkv, q, k_new, v_new, rope_theta: float, stream=None):
+        """Q/K/V of the batch's computed tokens from their hidden states x [n_tokens, H]
+        (projection by w_qkv [(Hq + 2 Hkv) D, H] and rotary embedding, arckv_qkv_rope);
+        k_new / v_new then go to scatter()."""
+        import torch
+        t, h = db.n_tokens, int(x.shape[1])
+        n_out = (self.hq + 2 * self.hkv) * self.d
+        if tuple(x.shape) != (t, h) or tuple(w_qkv.shape) != (n_out, h) or x.element_size() != 2 or \
+                not (x.is_contiguous() and w_qkv.is_contiguous()):
+            raise ValueError(f"x must be contiguous 16-bit [{t}, H] and w_qkv [{n_out}, H]")
+        for a, c in ((q, self.hq), (k_new, self.hkv), (v_new, self.hkv)):
+            if tuple(a.shape) != (t, c, self.d) or not a.is_contiguous() or a.element_size() != 2:
+                raise ValueError("q / k_new / v_new must be contiguous 16-bit [n_tokens, heads, D]")
+        need = 2 * t * n_out
+        if self._y is None or self._y.numel() < need:
+            self._y = torch.empty(max(need, 1), dtype=torch.uint8, device=self.device)
+        _lib.check(lib().arckv_qkv_rope(x.data_ptr(), w_qkv.data_ptr(), t, h, self.hq, self.hkv, self.d,
+                                        db.cu_q.data_ptr(), db.seq_lens.data_ptr(), db.plan.n_reqs,
+                                        float(rope_theta), self._y.data_ptr(), self._y.numel(),
+                                        q.data_ptr(), k_new.data_ptr(), v_new.data_ptr(), self._stream(stream)),
+                   "arckv_qkv_rope")
 
     def attention(self, db: DeviceBatch, q, out, stream=None, events=None):
         """Prefill attention of the batch.  `events`: optional (begin, mid, end) torch.cuda.Event

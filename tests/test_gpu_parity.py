@@ -142,6 +142,11 @@ SWEEP = [
     ([(700, 667), (64, 31)], 16, 4, 64),                # 132 columns: wide tiles
     ([(512, 448), (2048, 1984), (65, 1)], 32, 8, 128),  # 256 columns: wide tiles, one tile each
     ([(513, 448), (130, 65)], 32, 8, 128),              # 260 columns: a second, 4-column tile
+    # G = 5 (Qwen3-14B's 40 / 8 heads): tile edges fall inside a token's group of heads
+    ([(1040, 1024), (300, 16), (77, 0)], 40, 8, 128),
+    ([(4000, 3949), (130, 78), (6, 0)], 40, 8, 128),    # 255, 260 and 30 columns
+    ([(700, 600), (33, 0), (1, 0)], 10, 2, 64),
+    ([(L, L - 1) for L in (1, 17, 300, 4097, 65, 2000)], 40, 8, 128),   # decode: tiny tiles
 ]
 
 

@@ -252,6 +252,9 @@ def test_attention_plan_covers_every_tile_once():
     L = S + 16 * rng.integers(0, 300, 10)
     attention_plan_coverage(np.concatenate([[0], np.cumsum(S)]).tolist(), L.tolist(), 32, 8, 128, 256)
     attention_plan_coverage([0, 1], [1], 8, 1, 128, 256)
+    # G = 5 (40 / 8 heads): tiles of 256 columns end inside a token's group of heads
+    attention_plan_coverage(np.concatenate([[0], np.cumsum(S)]).tolist(), L.tolist(), 40, 8, 128, 256)
+    attention_plan_coverage([0, 51, 103], [4000, 103], 40, 8, 128, 256)
 
 
 def test_attention_plan_places_a_group_on_one_xcd():

@@ -46,6 +46,12 @@ CONFIGS = {
     "docqa": Config("docqa", 1002, 32, 8, 128, capacity=8192, scratch=8, num_phys=8200, max_batch=8,
                     extra=dict(n_docs=64, doc_tokens=8192, question_tokens=128, zipf_s=1.1,
                                n_batches=64, warmup_batches=16)),
+    # 2 on a Qwen3-14B-shaped layer (public configuration: 40 q / 8 kv heads, head_dim 128,
+    #    hidden 5120, rotary base 1e6), with the Q/K/V projection in the step: the same stream,
+    #    documents and cache as docqa.
+    "docqa14b": Config("docqa14b", 1002, 40, 8, 128, capacity=8192, scratch=8, num_phys=8200, max_batch=8,
+                       extra=dict(n_docs=64, doc_tokens=8192, question_tokens=128, zipf_s=1.1,
+                                  n_batches=64, warmup_batches=16, hidden=5120, rope_theta=1.0e6)),
     # 3: multi-turn conversation, 8B shape: 64 sessions, lognormal histories,
     #    uniform new turns, Zipf(1.0) session activity, capacity 40 % of the working set.
     #    (capacity 0 = derived from the generated working set)
