@@ -298,9 +298,10 @@ int32_t arckv_prefill_attention_timed(const void* k_pool, const void* v_pool, co
  * (n_tokens = cu_q[n_reqs]).  y_workspace: device, >= 2 n_tokens (num_q_heads + 2
  * num_kv_heads) head_dim bytes, caller-owned.  q_out: device bf16 [n_tokens][num_q_heads]
  * [head_dim]; k_out, v_out: device bf16 [n_tokens][num_kv_heads][head_dim] (the layout
- * arckv_kv_scatter takes).  Stream-ordered on `stream`.  head_dim in {64, 128}: else
- * EUNSUPPORTED; EINVAL on bad sizes, NULL pointers or rope_theta <= 1; ENOSPC if the workspace
- * is too small; EDEVICE if rocBLAS or a launch fails.  n_tokens = 0 is a no-op. */
+ * arckv_kv_scatter takes).  y_workspace, q_out, k_out and v_out must be 16-byte aligned.
+ * Stream-ordered on `stream`.  head_dim in {64, 128}: else EUNSUPPORTED; EINVAL on bad sizes,
+ * NULL or misaligned pointers or rope_theta <= 1; ENOSPC if the workspace is too small;
+ * EDEVICE if rocBLAS or a launch fails.  n_tokens = 0 is a no-op. */
 int32_t arckv_qkv_rope(const void* x, const void* w_qkv, int64_t n_tokens, int32_t hidden,
                        int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
                        const int32_t* cu_q, const int32_t* seq_lens, int32_t n_reqs,

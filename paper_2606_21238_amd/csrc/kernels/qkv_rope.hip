@@ -5,13 +5,14 @@
 //   y = x W^T            x [T][H] bf16, W [(Hq + 2 Hkv) D][H] bf16, y bf16 (fp32 accumulate)
 //   q, k = rotary(y_q, y_k) at each token's absolute position; v = y_v
 //
-// The projection is a plain GEMM and goes to rocBLAS (bf16 in/out, fp32 compute).  One
-// work-group per token then reads the token's y row once: it finds the token's position from
-// cu_q / seq_lens (suffix token i of request r sits at L_r - S_r + i), computes the D/2 rotary
-// angles p * theta^(-2i/D) in fp64, reduced mod 2 pi before the fp32 sine and cosine, rotates
-// the (i, i + D/2) pairs of every query and key head in fp32 and writes bf16 (round to
-// nearest even) Q [T][Hq][D], K [T][Hkv][D] and V [T][Hkv][D]; K and V then go to the pool
-// through the KV scatter.
+// The projection is a plain GEMM and goes to rocBLAS (bf16 in/out, fp32 compute).  A
+// work-group of a few tokens then reads their y rows once, in 16-byte pieces: it finds each
+// token's position from cu_q / seq_lens (suffix token i of request r sits at L_r - S_r + i),
+// computes the D/2 rotary angles p * theta^(-2i/D) in fp64 (the frequencies once per
+// work-group), reduced mod 2 pi before the fp32 sine and cosine, rotates the (i, i + D/2)
+// pairs of every query and key head in fp32 and writes bf16 (round to nearest even)
+// Q [T][Hq][D], K [T][Hkv][D] and V [T][Hkv][D]; K and V then go to the pool through the KV
+// scatter.
 #include <hip/hip_runtime.h>
 #include <rocblas/rocblas.h>
 
@@ -23,6 +24,9 @@
 namespace {
 
 constexpr int kThreads = 256;
+constexpr int kTokens = 4;     // tokens per work-group (the rotary frequencies are shared)
+
+typedef uint16_t u16x8_t __attribute__((ext_vector_type(8)));
 
 __device__ __forceinline__ float bf16_to_f32(uint16_t b) {
   return __builtin_bit_cast(float, static_cast<uint32_t>(b) << 16);
@@ -32,45 +36,68 @@ __device__ __forceinline__ uint16_t f32_to_bf16(float f) {  // nearest even; inp
   return static_cast<uint16_t>((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
 }
 
+// Work-group = kTokens consecutive tokens.  A task is 8 consecutive rotary pairs (i .. i+7,
+// i+D/2 .. i+D/2+7) of one head of one token: two 16-byte loads and two 16-byte stores.
 template <int D>
 __global__ __launch_bounds__(kThreads) void qkv_rope_kernel(
-    const uint16_t* __restrict__ y, int hq, int hkv, const int32_t* __restrict__ cu_q,
-    const int32_t* __restrict__ seq_lens, int n_reqs, double theta, uint16_t* __restrict__ q_out,
-    uint16_t* __restrict__ k_out, uint16_t* __restrict__ v_out) {
+    const uint16_t* __restrict__ y, int64_t n_tokens, int hq, int hkv,
+    const int32_t* __restrict__ cu_q, const int32_t* __restrict__ seq_lens, int n_reqs,
+    double theta, uint16_t* __restrict__ q_out, uint16_t* __restrict__ k_out,
+    uint16_t* __restrict__ v_out) {
   constexpr int HALF = D / 2;
-  __shared__ float cs[HALF], sn[HALF];
-  __shared__ int pos_s;
-  const int64_t t = blockIdx.x;
+  constexpr int CH = HALF / 8;                       // 8-pair chunks per head
+  __shared__ double freq[HALF];
+  __shared__ float cs[kTokens][HALF], sn[kTokens][HALF];
+  __shared__ int pos_s[kTokens];
+  const int64_t t0 = static_cast<int64_t>(blockIdx.x) * kTokens;
+  const int nt = static_cast<int>(min<int64_t>(kTokens, n_tokens - t0));
   const int tid = threadIdx.x;
-  if (tid == 0) {  // request of token t: the last r with cu_q[r] <= t
+  if (tid < nt) {  // request of token t: the last r with cu_q[r] <= t
+    const int64_t t = t0 + tid;
     int lo = 0, hi = n_reqs - 1;
     while (lo < hi) {
       const int mid = (lo + hi + 1) / 2;
       if (cu_q[mid] <= t) lo = mid; else hi = mid - 1;
     }
-    pos_s = seq_lens[lo] - (cu_q[lo + 1] - cu_q[lo]) + static_cast<int>(t - cu_q[lo]);
+    pos_s[tid] = seq_lens[lo] - (cu_q[lo + 1] - cu_q[lo]) + static_cast<int>(t - cu_q[lo]);
   }
+  for (int i = tid; i < HALF; i += kThreads) freq[i] = std::pow(theta, -2.0 * i / D);
   __syncthreads();
-  const double p = static_cast<double>(pos_s);
-  for (int i = tid; i < HALF; i += kThreads) {
-    const double a = std::fmod(p * std::pow(theta, -2.0 * i / D), 6.283185307179586476925);
+  for (int e = tid; e < nt * HALF; e += kThreads) {
+    const int j = e / HALF, i = e % HALF;
+    const double a = std::fmod(static_cast<double>(pos_s[j]) * freq[i], 6.283185307179586476925);
     float s, c;
     sincosf(static_cast<float>(a), &s, &c);
-    cs[i] = c;
-    sn[i] = s;
+    cs[j][i] = c;
+    sn[j][i] = s;
   }
   __syncthreads();
-  const int nrot = hq + hkv;
-  const uint16_t* row = y + t * static_cast<int64_t>(hq + 2 * hkv) * D;
-  for (int e = tid; e < nrot * HALF; e += kThreads) {
-    const int h = e / HALF, i = e % HALF;
-    const float lo = bf16_to_f32(row[h * D + i]), hi = bf16_to_f32(row[h * D + i + HALF]);
-    uint16_t* dst = h < hq ? q_out + (t * hq + h) * D : k_out + (t * hkv + (h - hq)) * D;
-    dst[i] = f32_to_bf16(lo * cs[i] - hi * sn[i]);
-    dst[i + HALF] = f32_to_bf16(hi * cs[i] + lo * sn[i]);
+  const int nrot = hq + hkv, width = (hq + 2 * hkv) * D;
+  for (int e = tid; e < nt * nrot * CH; e += kThreads) {
+    const int j = e / (nrot * CH), r = e % (nrot * CH), h = r / CH, i = (r % CH) * 8;
+    const int64_t t = t0 + j;
+    const uint16_t* src = y + t * width + h * D + i;
+    const u16x8_t lo = *reinterpret_cast<const u16x8_t*>(src);
+    const u16x8_t hi = *reinterpret_cast<const u16x8_t*>(src + HALF);
+    u16x8_t olo, ohi;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const float a = bf16_to_f32(lo[k]), b = bf16_to_f32(hi[k]);
+      const float c = cs[j][i + k], s = sn[j][i + k];
+      olo[k] = f32_to_bf16(a * c - b * s);
+      ohi[k] = f32_to_bf16(b * c + a * s);
+    }
+    uint16_t* dst = h < hq ? q_out + (t * hq + h) * D + i : k_out + (t * hkv + (h - hq)) * D + i;
+    *reinterpret_cast<u16x8_t*>(dst) = olo;
+    *reinterpret_cast<u16x8_t*>(dst + HALF) = ohi;
   }
-  const uint16_t* vrow = row + static_cast<int64_t>(nrot) * D;
-  for (int e = tid; e < hkv * D; e += kThreads) v_out[t * hkv * D + e] = vrow[e];
+  // values: a plain copy of the token's Hkv * D trailing elements of y
+  for (int e = tid; e < nt * hkv * (D / 8); e += kThreads) {
+    const int j = e / (hkv * (D / 8)), r = e % (hkv * (D / 8));
+    const int64_t t = t0 + j;
+    *reinterpret_cast<u16x8_t*>(v_out + t * hkv * D + r * 8) =
+        *reinterpret_cast<const u16x8_t*>(y + t * width + nrot * D + r * 8);
+  }
 }
 
 // One rocBLAS handle per device, created on first use and kept for the process.
@@ -112,6 +139,10 @@ extern "C" int32_t arckv_qkv_rope(const void* x, const void* w_qkv, int64_t n_to
   if (x == nullptr || w_qkv == nullptr || cu_q == nullptr || seq_lens == nullptr ||
       y_workspace == nullptr || q_out == nullptr || k_out == nullptr || v_out == nullptr)
     return arckv::fail(ARCKV_EINVAL, "qkv_rope: NULL pointer");
+  for (const void* p : {static_cast<const void*>(y_workspace), static_cast<const void*>(q_out),
+                        static_cast<const void*>(k_out), static_cast<const void*>(v_out)})
+    if (reinterpret_cast<uintptr_t>(p) % 16 != 0)
+      return arckv::fail(ARCKV_EINVAL, "qkv_rope: workspace and outputs must be 16-byte aligned");
   if (ws_bytes < n_tokens * n_out * 2)
     return arckv::fail(ARCKV_ENOSPC, "qkv_rope: workspace %lld bytes < %lld", (long long)ws_bytes,
                        (long long)(n_tokens * n_out * 2));
@@ -131,16 +162,16 @@ extern "C" int32_t arckv_qkv_rope(const void* x, const void* w_qkv, int64_t n_to
       static_cast<rocblas_int>(n_out), rocblas_datatype_f32_r, rocblas_gemm_algo_standard, 0, 0);
   if (bs != rocblas_status_success)
     return arckv::fail(ARCKV_EDEVICE, "qkv_rope: rocblas_gemm_ex status %d", static_cast<int>(bs));
-  const dim3 grid(static_cast<unsigned>(n_tokens));
+  const dim3 grid(static_cast<unsigned>((n_tokens + kTokens - 1) / kTokens));
   auto* y = static_cast<const uint16_t*>(y_workspace);
   auto* q = static_cast<uint16_t*>(q_out);
   auto* k = static_cast<uint16_t*>(k_out);
   auto* v = static_cast<uint16_t*>(v_out);
   if (head_dim == 64)
-    hipLaunchKernelGGL(qkv_rope_kernel<64>, grid, dim3(kThreads), 0, s, y, num_q_heads, num_kv_heads,
+    hipLaunchKernelGGL(qkv_rope_kernel<64>, grid, dim3(kThreads), 0, s, y, n_tokens, num_q_heads, num_kv_heads,
                        cu_q, seq_lens, n_reqs, rope_theta, q, k, v);
   else
-    hipLaunchKernelGGL(qkv_rope_kernel<128>, grid, dim3(kThreads), 0, s, y, num_q_heads, num_kv_heads,
+    hipLaunchKernelGGL(qkv_rope_kernel<128>, grid, dim3(kThreads), 0, s, y, n_tokens, num_q_heads, num_kv_heads,
                        cu_q, seq_lens, n_reqs, rope_theta, q, k, v);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return arckv::fail(ARCKV_EDEVICE, "qkv_rope: %s", hipGetErrorString(e));

@@ -89,6 +89,7 @@ def check(r, hq, hkv, d):
     ([(300, 250), (17, 0), (40000, 39990)], 512, 8, 2, 128),           # positions up to 39999
     ([(129, 1), (64, 63)], 256, 16, 2, 64),
     ([(8320, 8192), (2100, 2048)], 5120, 40, 8, 128),                  # Qwen3-14B layer shape
+    ([(3, 0), (9, 6)], 128, 4, 4, 128),                                # 6 tokens: a ragged group
 ])
 def test_qkv_rope_matches_oracle(reqs, hidden, hq, hkv, d):
     print_case(f"qkv_rope {reqs} hidden={hidden} hq={hq} hkv={hkv} d={d}")
