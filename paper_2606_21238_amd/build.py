@@ -56,7 +56,7 @@ def build(verbose: bool = False) -> str:
     for src in HIP_SRC:
         obj = os.path.join(BUILD, os.path.basename(src) + ".o")
         jobs.append([hipcc, f"--offload-arch={ARCH}", *common,
-                     # no packed fp32 VALU ops are ever generated (see DESIGN: correctness)
+                     # no packed fp32 VALU ops are ever generated: some of their forms have given wrong results on gfx950
                      "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
                      "-c", os.path.join(CSRC, src), "-o", obj])
         objs.append(obj)

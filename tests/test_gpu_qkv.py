@@ -1,6 +1,6 @@
 """GPU parity of the Q/K/V producer (arckv_qkv_rope) against the oracle.
 
-Error bound of a bf16 output (derived from the arithmetic, see DESIGN): y's fp32 sum of H
+Error bound of a bf16 output (derived from the arithmetic): y's fp32 sum of H
 products can be off by H 2^-24 sum_h |x_h w_h| (the standard bound for a recursive sum), and
 its bf16 rounding and the oracle's differ by up to one bf16 ulp (<= 2^-7 relative); a
 rotation mixes the two members of a pair, so both errors are bounded by the pair's norm of
