@@ -108,6 +108,13 @@ int32_t arckv_hash_blocks_batch(const int32_t* const* tokens, const int64_t* n_t
  * of the page its reference evicted, else the head of a FIFO free list.
  * DBL (Sec. 4: a fixed 1:1 split between the recency and the frequency queue) runs the same
  * rules with p held at c/2: ghost hits move the page and call REPLACE but do not steer p.
+ * Length-aware victims (Sec. 6 proposes weighing prompt length beside recency and
+ * frequency): with victim_window W > 1, wherever a policy evicts from a resident list
+ * (REPLACE, ARC's IV-A T1 drop, LRU), it takes, among the W least recently used unpinned
+ * pages of that list, the one at the greatest depth (block index in its prompt; ties: the
+ * less recent one).  The list, the ghost bookkeeping and p are unchanged.  Losing a block at
+ * depth k costs the next request on its chain the recompute of blocks k onwards, so deeper
+ * blocks are the cheaper losses.
  * ------------------------------------------------------------------------------------- */
 typedef struct arckv_cache arckv_cache;
 
@@ -120,6 +127,8 @@ typedef struct {
   const int32_t* initial_free_order; /* permutation of [0, num_phys_blocks) or NULL for  */
                                      /* ascending; the first num_phys - scratch entries  */
                                      /* are the page free list, the rest the scratch FIFO */
+  int32_t victim_window;             /* W in [1, 4096] (0 = 1): length-aware victims, see */
+                                     /* below; 1 = the LRU-most unpinned page            */
 } arckv_cache_cfg;
 
 /* Creates a cache (host memory only).  EINVAL on a bad configuration. */

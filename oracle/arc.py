@@ -43,6 +43,15 @@ frequency queue) is the same policy with the adaptation switched off: p stays at
 ghost hits (Cases II and III) only move x and call REPLACE.  This is the fixed-target form
 FRC_p of the ARC paper with p = c/2.
 
+Length-aware victims (Sec. 6 names prompt length as a further eviction factor beside
+recency and frequency; the rule is this project's reading, not the paper's): with a victim
+window W > 1, every eviction from a resident list (REPLACE and the IV-A T1 drop) takes,
+among the W least recently used unpinned pages of that list, the page at the greatest
+depth (its block index in the prompt that referenced it), the less recent one on ties.
+Which list loses a page, the ghost lists and p follow the rules above unchanged; W = 1 is
+the plain policy.  Losing the block at depth k makes the next request on that chain
+recompute blocks k onwards, so among recently similar pages the deepest is the cheapest loss.
+
 Every reference is appended to a decision log (``Event``) so that another
 implementation can be compared decision by decision.
 """
@@ -57,6 +66,22 @@ CASE_I, CASE_II, CASE_III, CASE_IVA, CASE_IVA_T1DEL, CASE_IVB, LRU_HIT, LRU_MISS
 CASE_NAMES = ["I", "II", "III", "IVA", "IVA_T1DEL", "IVB", "LRU_HIT", "LRU_MISS"]
 FROM_NONE, FROM_T1, FROM_T2, FROM_B1, FROM_B2 = range(5)
 NO_HASH = 0
+
+
+def window_victim(lst, pinned, depth, window: int):
+    """The page an eviction takes from ``lst`` (keys in LRU -> MRU order): the deepest of the
+    ``window`` least recently used unpinned pages, the less recent on ties (window 1: the
+    LRU-most unpinned page); None if every page is pinned."""
+    best, seen = None, 0
+    for key in lst:
+        if key in pinned:
+            continue
+        if best is None or depth.get(key, 0) > depth.get(best, 0):
+            best = key
+        seen += 1
+        if seen == window:
+            break
+    return best
 
 
 @dataclass(frozen=True)
@@ -75,11 +100,13 @@ class Event:
 class ARC:
     """ARC(c) with pins and physical block placement (adaptive=False: DBL, p fixed at c/2)."""
 
-    def __init__(self, capacity: int, free_blocks, adaptive: bool = True):
-        if capacity < 1:
-            raise ValueError("capacity must be >= 1")
+    def __init__(self, capacity: int, free_blocks, adaptive: bool = True, window: int = 1):
+        if capacity < 1 or window < 1:
+            raise ValueError("capacity and window must be >= 1")
         self.c = int(capacity)
         self.adaptive = adaptive
+        self.window = int(window)
+        self.depth: dict[int, int] = {}       # block index of each key in its prompt
         self.p = 0.0 if adaptive else self.c / 2.0
         # OrderedDicts in LRU -> MRU order; resident lists map key -> physical block.
         self.T1: OrderedDict[int, int] = OrderedDict()
@@ -109,10 +136,7 @@ class ARC:
 
     # -- helpers -------------------------------------------------------------
     def _lru_unpinned(self, lst: OrderedDict):
-        for key in lst:           # iteration order is LRU -> MRU
-            if key not in self.pinned:
-                return key
-        return None
+        return window_victim(lst, self.pinned, self.depth, self.window)
 
     def _replace(self, x_in_b2: bool):
         """Evict one resident page to its ghost list; return (key, from, phys)."""
@@ -130,7 +154,7 @@ class ARC:
         raise RuntimeError("REPLACE found no unpinned resident page")
 
     # -- one reference ---------------------------------------------------------
-    def reference(self, x: int) -> Event:
+    def reference(self, x: int, depth: int = 0) -> Event:
         c = self.c
         evicted, evicted_from = NO_HASH, FROM_NONE
         dropped, dropped_from = NO_HASH, FROM_NONE
@@ -183,6 +207,7 @@ class ARC:
                     phys = self.free.popleft()
                 case = CASE_IVB
             self.T1[x] = phys
+        self.depth[x] = int(depth)
         ev = Event(x, case, evicted, evicted_from, dropped, dropped_from, phys, self.p)
         self.log.append(ev)
         return ev

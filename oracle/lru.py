@@ -10,14 +10,18 @@ from __future__ import annotations
 
 from collections import OrderedDict, deque
 
-from .arc import Event, LRU_HIT, LRU_MISS, FROM_NONE, FROM_T1, NO_HASH
+from .arc import Event, LRU_HIT, LRU_MISS, FROM_NONE, FROM_T1, NO_HASH, window_victim
 
 
 class LRU:
-    def __init__(self, capacity: int, free_blocks):
-        if capacity < 1:
-            raise ValueError("capacity must be >= 1")
+    """window > 1: length-aware victims, as for ``oracle.arc.ARC``."""
+
+    def __init__(self, capacity: int, free_blocks, window: int = 1):
+        if capacity < 1 or window < 1:
+            raise ValueError("capacity and window must be >= 1")
         self.c = int(capacity)
+        self.window = int(window)
+        self.depth: dict[int, int] = {}
         self.p = 0.0
         self.L: OrderedDict[int, int] = OrderedDict()    # LRU -> MRU, key -> phys
         self.free = deque(int(b) for b in free_blocks)
@@ -40,14 +44,14 @@ class LRU:
     def unpin_all(self) -> None:
         self.pinned.clear()
 
-    def reference(self, x: int) -> Event:
+    def reference(self, x: int, depth: int = 0) -> Event:
         if x in self.L:
             self.L.move_to_end(x)
             ev = Event(x, LRU_HIT, NO_HASH, FROM_NONE, NO_HASH, FROM_NONE, self.L[x], 0.0)
         else:
             evicted, evicted_from = NO_HASH, FROM_NONE
             if len(self.L) == self.c:
-                victim = next((k for k in self.L if k not in self.pinned), None)
+                victim = window_victim(self.L, self.pinned, self.depth, self.window)
                 if victim is None:
                     raise RuntimeError("LRU found no unpinned page")
                 phys = self.L.pop(victim)
@@ -58,6 +62,7 @@ class LRU:
                 phys = self.free.popleft()
             self.L[x] = phys
             ev = Event(x, LRU_MISS, evicted, evicted_from, NO_HASH, FROM_NONE, phys, 0.0)
+        self.depth[x] = int(depth)
         self.log.append(ev)
         return ev
 

@@ -26,6 +26,8 @@ Readings fixed by this project where the paper is silent:
   takes a block from a separate scratch FIFO and returns it on release.
 * Placement.  The pool's blocks, in the given initial order, are split into a
   page region (the first ``num_phys - scratch``) and the scratch FIFO (the rest).
+* Depth.  Each reference carries the block's index in its prompt, which a
+  length-aware victim window (``oracle.arc``) weighs.
 * Batch formation.  Consecutive requests, at most ``max_batch``, while the sum
   of their full blocks stays within the capacity c and their partial tails
   within the scratch blocks; this guarantees that a pin-aware victim exists.
@@ -99,7 +101,7 @@ def form_batches(n_tokens_list, max_batch: int, capacity: int, scratch_blocks: i
 
 class Planner:
     def __init__(self, policy: str, capacity: int, num_phys: int, scratch_blocks: int,
-                 initial_order=None, ref_order: str = "tail_first"):
+                 initial_order=None, ref_order: str = "tail_first", victim_window: int = 1):
         order = list(range(num_phys)) if initial_order is None else [int(b) for b in initial_order]
         if sorted(order) != list(range(num_phys)):
             raise PlanError("EINVAL", "initial order is not a permutation of the pool")
@@ -109,11 +111,11 @@ class Planner:
         pages = order[:n_pages]
         self.scratch = deque(order[n_pages:])
         if policy == "arc":
-            self.cache = ARC(capacity, pages)
+            self.cache = ARC(capacity, pages, window=victim_window)
         elif policy == "dbl":
-            self.cache = ARC(capacity, pages, adaptive=False)
+            self.cache = ARC(capacity, pages, adaptive=False, window=victim_window)
         elif policy == "lru":
-            self.cache = LRU(capacity, pages)
+            self.cache = LRU(capacity, pages, window=victim_window)
         else:
             raise PlanError("EINVAL", f"unknown policy {policy}")
         if ref_order not in ("tail_first", "head_first"):
@@ -153,7 +155,7 @@ class Planner:
             order = range(n_full - 1, -1, -1) if self.ref_order == "tail_first" else range(n_full)
             phys = [None] * n_full
             for i in order:
-                ev = cache.reference(hashes[i])
+                ev = cache.reference(hashes[i], depth=i)
                 phys[i] = ev.phys
                 cache.pin(hashes[i])
                 self.totals.case_counts[ev.case] += 1

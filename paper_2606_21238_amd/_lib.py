@@ -20,7 +20,8 @@ P_i32, P_i64, P_u64 = C.POINTER(i32), C.POINTER(i64), C.POINTER(u64)
 
 class CacheCfg(C.Structure):
     _fields_ = [("policy", i32), ("ref_order", i32), ("capacity_blocks", i64),
-                ("num_phys_blocks", i64), ("scratch_blocks", i64), ("initial_free_order", P_i32)]
+                ("num_phys_blocks", i64), ("scratch_blocks", i64), ("initial_free_order", P_i32),
+                ("victim_window", i32)]
 
 
 class Req(C.Structure):

@@ -40,6 +40,7 @@ struct Node {
   int32_t phys = -1;
   int32_t prev = -1, next = -1;
   int32_t list = ARCKV_LIST_NONE;
+  int32_t depth = 0;  // block index of the page in the prompt that last referenced it
 };
 
 struct List {
@@ -104,6 +105,7 @@ struct Victim {
 struct arckv_cache {
   int32_t policy = ARCKV_POLICY_ARC;
   int32_t ref_order = ARCKV_REF_TAIL_FIRST;
+  int32_t window = 1;  // victim window (length-aware eviction when > 1)
   int64_t c = 0;
   int64_t num_phys = 0;
   int64_t n_scratch = 0;
@@ -186,6 +188,20 @@ struct arckv_cache {
     }
     return n;
   }
+  // The page a policy evicts from a resident list: the LRU-most unpinned page, or, with a
+  // victim window W > 1, the deepest of the W least recently used unpinned pages (the first
+  // such page on ties).  Only the first one moves the scan cursor.
+  int32_t pick_victim(int32_t list) {
+    const int32_t first = lru_unpinned(list);
+    if (window <= 1 || first < 0) return first;
+    int32_t best = first, seen = 1;
+    for (int32_t m = nodes[first].next; m >= 0 && seen < window; m = nodes[m].next) {
+      if (pinned(m)) continue;
+      if (nodes[m].depth > nodes[best].depth) best = m;
+      ++seen;
+    }
+    return best;
+  }
   int32_t find(uint64_t key) const {
     return index.find(key);
   }
@@ -209,8 +225,8 @@ struct arckv_cache {
     int32_t first = prefer_t1 ? ARCKV_LIST_T1 : ARCKV_LIST_T2;
     int32_t second = prefer_t1 ? ARCKV_LIST_T2 : ARCKV_LIST_T1;
     int32_t src = first;
-    int32_t n = lru_unpinned(first);
-    if (n < 0) { src = second; n = lru_unpinned(second); }
+    int32_t n = pick_victim(first);
+    if (n < 0) { src = second; n = pick_victim(second); }
     if (n < 0) return false;
     v.key = nodes[n].key;
     v.from = src;
@@ -266,7 +282,7 @@ struct arckv_cache {
           phys = v.phys;
           ev.kase = ARCKV_CASE_IVA;
         } else {                                                      // IV-A, |T1| = c
-          const int32_t d = lru_unpinned(ARCKV_LIST_T1);
+          const int32_t d = pick_victim(ARCKV_LIST_T1);
           if (d < 0) return arckv::fail(ARCKV_ENOSPC, "IV-A: every T1 page pinned");
           phys = nodes[d].phys;
           ev.dropped = nodes[d].key;
@@ -307,7 +323,7 @@ struct arckv_cache {
     } else {
       int32_t phys = -1;
       if (lists[ARCKV_LIST_T1].size == c) {
-        const int32_t vtm = lru_unpinned(ARCKV_LIST_T1);
+        const int32_t vtm = pick_victim(ARCKV_LIST_T1);
         if (vtm < 0) return arckv::fail(ARCKV_ENOSPC, "LRU: every page pinned");
         phys = nodes[vtm].phys;
         ev.evicted = nodes[vtm].key;
@@ -327,12 +343,13 @@ struct arckv_cache {
     return ARCKV_OK;
   }
 
-  int32_t reference(uint64_t x, int32_t& phys_out) {
+  int32_t reference(uint64_t x, int32_t depth, int32_t& phys_out) {
     arckv_event ev{};
     ev.key = x;
     const int32_t st =
         policy == ARCKV_POLICY_LRU ? reference_lru(x, ev) : reference_arc(x, ev);
     if (st != ARCKV_OK) return st;
+    nodes[find(x)].depth = depth;
     ev.p_after = policy == ARCKV_POLICY_LRU ? 0.0 : p;
     phys_out = ev.phys_block;
     case_counts[ev.kase] += 1;
@@ -355,6 +372,8 @@ extern "C" int32_t arckv_cache_create(const arckv_cache_cfg* cfg, arckv_cache** 
     return arckv::fail(ARCKV_EINVAL, "cache_create: unknown policy %d", cfg->policy);
   if (cfg->ref_order != ARCKV_REF_TAIL_FIRST && cfg->ref_order != ARCKV_REF_HEAD_FIRST)
     return arckv::fail(ARCKV_EINVAL, "cache_create: unknown reference order");
+  if (cfg->victim_window < 0 || cfg->victim_window > 4096)
+    return arckv::fail(ARCKV_EINVAL, "cache_create: victim window %d not in [0, 4096]", cfg->victim_window);
   if (cfg->capacity_blocks < 1 || cfg->scratch_blocks < 0 || cfg->num_phys_blocks > INT32_MAX / 16 ||
       cfg->num_phys_blocks - cfg->scratch_blocks < cfg->capacity_blocks)
     return arckv::fail(ARCKV_EINVAL,
@@ -379,6 +398,7 @@ extern "C" int32_t arckv_cache_create(const arckv_cache_cfg* cfg, arckv_cache** 
   c->policy = cfg->policy;
   c->p = cfg->policy == ARCKV_POLICY_DBL ? static_cast<double>(cfg->capacity_blocks) / 2.0 : 0.0;
   c->ref_order = cfg->ref_order;
+  c->window = cfg->victim_window < 1 ? 1 : cfg->victim_window;
   c->c = cfg->capacity_blocks;
   c->num_phys = np;
   c->n_scratch = cfg->scratch_blocks;
@@ -464,7 +484,7 @@ extern "C" int32_t arckv_plan_batch(arckv_cache* c, const arckv_req* reqs, int32
     for (int64_t i = 0; i < nf; ++i) {
       const int64_t b = c->ref_order == ARCKV_REF_TAIL_FIRST ? nf - 1 - i : i;
       int32_t phys = -1;
-      const int32_t st = c->reference(q.hashes[b], phys);
+      const int32_t st = c->reference(q.hashes[b], static_cast<int32_t>(b), phys);
       if (st != ARCKV_OK) return st;  // unreachable with the capacity check above
       row[b] = phys;
     }

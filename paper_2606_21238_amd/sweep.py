@@ -11,6 +11,9 @@ native library -- once per (policy, cache size), and reports
 * the T1 ratio |T1| / (|T1| + |T2|) after every batch, for ARC and DBL, summarised as
   quantiles and a down-sampled series; and ARC's target p / c beside it.
 
+A policy may carry a victim window, ``arc@16``: length-aware eviction (Sec. 6 future work),
+the deepest of the 16 least recently used unpinned pages of the list a policy evicts from.
+
 Usage::
 
     python -m paper_2606_21238_amd.sweep --workload wzqa_long
@@ -54,13 +57,23 @@ class Replay:
         return np.where(tot > 0, self.t1 / np.maximum(tot, 1), 1.0)
 
 
+def parse_policy(name: str):
+    """'arc' -> ('arc', 1); 'lru@16' -> ('lru', 16) (victim window)."""
+    base, _, w = name.partition("@")
+    if base not in POLICIES:
+        raise ValueError(f"unknown policy {name!r}")
+    return base, int(w) if w else 1
+
+
 def replay(hashes, lens, policy: str, capacity: int, scratch: int, max_batch: int = 1,
            initial_order=None, ref_order: str = "tail_first") -> Replay:
     """Plans and releases every batch of the stream on a fresh cache of `capacity` pages and
-    `capacity + scratch` physical blocks; hashes[j] are request j's chained block identities."""
+    `capacity + scratch` physical blocks; hashes[j] are request j's chained block identities.
+    `policy` may carry a victim window (``arc@16``)."""
     lens = np.asarray(lens, dtype=np.int64)
     n = len(lens)
-    cache = BlockCache(policy, capacity, capacity + scratch, scratch, initial_order, ref_order)
+    base, window = parse_policy(policy)
+    cache = BlockCache(base, capacity, capacity + scratch, scratch, initial_order, ref_order, window)
     hit = np.zeros(n, dtype=np.int64)
     ends, t1, t2, p = [], [], [], []
     i = 0
@@ -134,7 +147,7 @@ def sweep(name: str, sizes_tokens=None, policies=POLICIES, max_batch: int = 1,
             t = time.perf_counter()
             r = replay(hashes, lens, pol, c, cfg.scratch, max_batch)
             entry = {"hit_rate": round(r.hit_rate(warmup), 6), "seconds": round(time.perf_counter() - t, 3)}
-            if pol != "lru":
+            if parse_policy(pol)[0] != "lru":
                 ratio = r.t1_ratio()
                 q = np.quantile(ratio[r.batch_end > warmup] if warmup else ratio, [0.1, 0.5, 0.9])
                 idx = np.unique(np.linspace(0, len(ratio) - 1, series_points).round().astype(int))

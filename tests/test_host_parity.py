@@ -34,10 +34,10 @@ def test_hash_matches_oracle():
 class Pair:
     """Library cache and oracle planner driven in lockstep."""
 
-    def __init__(self, policy, c, nphys, scratch, order=None, ref_order="tail_first"):
-        self.lib = ak.BlockCache(policy, c, nphys, scratch, order, ref_order)
+    def __init__(self, policy, c, nphys, scratch, order=None, ref_order="tail_first", window=1):
+        self.lib = ak.BlockCache(policy, c, nphys, scratch, order, ref_order, window)
         self.lib.set_log(1 << 20)
-        self.orc = Planner(policy, c, nphys, scratch, order, ref_order)
+        self.orc = Planner(policy, c, nphys, scratch, order, ref_order, window)
         self.n_events = 0
 
     def run(self, token_lists):
@@ -80,13 +80,14 @@ class Pair:
 
 @pytest.mark.parametrize("policy", ["arc", "lru", "dbl"])
 @pytest.mark.parametrize("ref_order", ["tail_first", "head_first"])
-@pytest.mark.parametrize("seed", [0, 1, 2])
-def test_random_streams_bit_exact(policy, ref_order, seed):
+@pytest.mark.parametrize("seed,window", [(0, 1), (1, 1), (2, 1), (3, 2), (4, 7)])
+def test_random_streams_bit_exact(policy, ref_order, seed, window):
+    """window > 1: length-aware victims, the same decisions on both sides."""
     cfg = get_config("tiny")
     rng = np.random.default_rng(100 + seed)
     c, scratch = int(rng.integers(8, 40)), 8
     nphys = c + scratch + int(rng.integers(0, 5))
-    pair = Pair(policy, c, nphys, scratch, rng.permutation(nphys), ref_order)
+    pair = Pair(policy, c, nphys, scratch, rng.permutation(nphys), ref_order, window)
     docs = [make_request(cfg, [(Source(KIND_DOC, d, 200), 0, 200)]).tokens for d in range(12)]
     pops = 1.0 / np.arange(1, 13) ** 1.1
     pops /= pops.sum()
@@ -182,6 +183,10 @@ def test_error_statuses_match_the_oracle():
         ak.BlockCache("arc", 10, 12, 4)              # pool too small for c + scratch
     with pytest.raises(ak.ArckvError):
         ak.BlockCache("arc", 4, 8, 2, initial_order=[0, 1, 2, 3, 4, 5, 6, 6])
+    for bad_window in (-1, 4097):
+        with pytest.raises(ak.ArckvError) as e2:
+            ak.BlockCache("lru", 4, 8, 2, victim_window=bad_window)
+        assert e2.value.code == "EINVAL"
 
 
 def attention_plan_coverage(cu_q, seq_lens, hq, hkv, d, num_cus):

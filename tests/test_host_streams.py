@@ -28,7 +28,7 @@ def oracle_hashes(reqs, chunk=512):
     return out
 
 
-def replay(cfg, reqs, policy, orc_hashes):
+def replay(cfg, reqs, policy, orc_hashes, window=1):
     """Drive library and oracle over the whole stream; returns (library cache, oracle planner)."""
     lens = [r.n_tokens for r in reqs]
     batches = form_batches(lens, cfg.max_batch, cfg.capacity, cfg.scratch)
@@ -39,9 +39,9 @@ def replay(cfg, reqs, policy, orc_hashes):
         i += n
     assert lib_batches == batches
     order = free_order(cfg.seed, cfg.num_phys)
-    lib = ak.BlockCache(policy, cfg.capacity, cfg.num_phys, cfg.scratch, order)
+    lib = ak.BlockCache(policy, cfg.capacity, cfg.num_phys, cfg.scratch, order, victim_window=window)
     lib.set_log(sum(len(h) for h in orc_hashes) + 1)
-    orc = Planner(policy, cfg.capacity, cfg.num_phys, cfg.scratch, order)
+    orc = Planner(policy, cfg.capacity, cfg.num_phys, cfg.scratch, order, victim_window=window)
     lib_hashes = ak.hash_blocks_batch([r.tokens for r in reqs])
     for a, b in batches:
         p = lib.plan_batch([(lib_hashes[j], lens[j]) for j in range(a, b)])
@@ -90,11 +90,11 @@ def multiturn():
     return sized(base, cap), reqs, oracle_hashes(reqs)
 
 
-@pytest.mark.parametrize("policy", ["arc", "lru", "dbl"])
-def test_multiturn_stream_bit_exact(multiturn, policy):
+@pytest.mark.parametrize("policy,window", [("arc", 1), ("lru", 1), ("dbl", 1), ("arc", 16), ("lru", 16)])
+def test_multiturn_stream_bit_exact(multiturn, policy, window):
     cfg, reqs, hashes = multiturn
     assert len(reqs) == 1024
-    lib, orc = replay(cfg, reqs, policy, hashes)
+    lib, orc = replay(cfg, reqs, policy, hashes, window)
     rate = check_decisions(lib, orc)
     print(f"multiturn {policy}: capacity {cfg.capacity} blocks, token hit rate {rate:.4f}")
     # sessions come back, so a large share of the prompt tokens is served from the cache
