@@ -45,8 +45,10 @@ extern "C" int32_t arckv_hash_blocks(const int32_t* tokens, int64_t n_tokens, ui
   return ARCKV_OK;
 }
 
-// Many sequences at once: up to kLanes independent chains advance in lock-step, so the serial
-// xor-multiply latency of one chain overlaps with the others.  Same definition, same result.
+// Many sequences at once: kLanes independent chains advance in lock-step, so the serial
+// xor-multiply latency of one chain overlaps with the others.  A lane whose sequence ends takes
+// the next unstarted sequence, so ragged lengths keep every lane busy.  Same definition, same
+// result.
 extern "C" int32_t arckv_hash_blocks_batch(const int32_t* const* tokens, const int64_t* n_tokens,
                                            int32_t n_seqs, uint64_t root, uint64_t* out,
                                            int64_t out_cap, int64_t* offsets) {
@@ -62,37 +64,54 @@ extern "C" int32_t arckv_hash_blocks_batch(const int32_t* const* tokens, const i
   if (offsets[n_seqs] > out_cap || (offsets[n_seqs] > 0 && out == nullptr))
     return arckv::fail(ARCKV_ENOSPC, "hash_blocks_batch: %lld blocks, capacity %lld",
                        (long long)offsets[n_seqs], (long long)out_cap);
-  for (int32_t g = 0; g < n_seqs; g += kLanes) {
-    const int lanes = n_seqs - g < kLanes ? n_seqs - g : kLanes;
-    uint64_t h[kLanes];
-    int64_t nf[kLanes];
-    int64_t most = 0;
+  // lane state: its sequence (-1: idle), the next block, the chain value, token and output cursors
+  int32_t seq[kLanes];
+  int64_t left[kLanes];
+  uint64_t h[kLanes];
+  const int32_t* tok[kLanes];
+  uint64_t* dst[kLanes];
+  int32_t next = 0;
+  auto refill = [&](int l) {
+    seq[l] = -1;
+    while (next < n_seqs && n_tokens[next] < ARCKV_BLOCK_TOKENS) ++next;  // no full block
+    if (next == n_seqs) return;
+    seq[l] = next;
+    left[l] = n_tokens[next] / ARCKV_BLOCK_TOKENS;
+    h[l] = root;
+    tok[l] = tokens[next];
+    dst[l] = out + offsets[next];
+    ++next;
+  };
+  int busy = 0;
+  for (int l = 0; l < kLanes; ++l) {
+    refill(l);
+    busy += seq[l] >= 0;
+  }
+  static const int32_t kZeros[ARCKV_BLOCK_TOKENS] = {};
+  while (busy > 0) {
+    uint64_t x[kLanes];
+    const int32_t* t16[kLanes];
     for (int l = 0; l < kLanes; ++l) {
-      h[l] = root;
-      nf[l] = 0;
+      x[l] = kFnvOffset;
+      t16[l] = seq[l] >= 0 ? tok[l] : kZeros;  // idle lanes hash zeros, never stored
     }
-    for (int l = 0; l < lanes; ++l) {
-      h[l] = root;
-      nf[l] = n_tokens[g + l] / ARCKV_BLOCK_TOKENS;
-      most = nf[l] > most ? nf[l] : most;
+    for (int byte = 0; byte < 8; ++byte)
+      for (int l = 0; l < kLanes; ++l) x[l] = mix_byte(x[l], static_cast<uint8_t>(h[l] >> (8 * byte)));
+    for (int t = 0; t < ARCKV_BLOCK_TOKENS; ++t) {
+      uint32_t v[kLanes];
+      for (int l = 0; l < kLanes; ++l) v[l] = static_cast<uint32_t>(t16[l][t]);
+      for (int byte = 0; byte < 4; ++byte)
+        for (int l = 0; l < kLanes; ++l) x[l] = mix_byte(x[l], static_cast<uint8_t>(v[l] >> (8 * byte)));
     }
-    for (int64_t i = 0; i < most; ++i) {
-      uint64_t x[kLanes];
-      for (int l = 0; l < kLanes; ++l) x[l] = kFnvOffset;
-      for (int byte = 0; byte < 8; ++byte)
-        for (int l = 0; l < kLanes; ++l) x[l] = mix_byte(x[l], static_cast<uint8_t>(h[l] >> (8 * byte)));
-      for (int t = 0; t < ARCKV_BLOCK_TOKENS; ++t) {
-        uint32_t v[kLanes];
-        for (int l = 0; l < kLanes; ++l)
-          v[l] = (l < lanes && i < nf[l]) ? static_cast<uint32_t>(tokens[g + l][i * ARCKV_BLOCK_TOKENS + t]) : 0u;
-        for (int byte = 0; byte < 4; ++byte)
-          for (int l = 0; l < kLanes; ++l) x[l] = mix_byte(x[l], static_cast<uint8_t>(v[l] >> (8 * byte)));
+    for (int l = 0; l < kLanes; ++l) {
+      if (seq[l] < 0) continue;
+      h[l] = x[l];
+      *dst[l]++ = x[l];
+      tok[l] += ARCKV_BLOCK_TOKENS;
+      if (--left[l] == 0) {
+        refill(l);
+        busy -= seq[l] < 0;
       }
-      for (int l = 0; l < lanes; ++l)
-        if (i < nf[l]) {
-          h[l] = x[l];
-          out[offsets[g + l] + i] = x[l];
-        }
     }
   }
   return ARCKV_OK;
