@@ -288,17 +288,16 @@ def main():
 
     eng = PrefillEngine(hq, hkv, d, cfg.capacity, cfg.num_phys, cfg.scratch, args.policy, order)
 
-    host_t = {"plan": 0.0, "upload": 0.0, "launch": 0.0, "release": 0.0}
+    host_t = {"prepare": 0.0, "launch": 0.0, "release": 0.0}
 
     def step(i, ev=None):
         if staged[i] is None:                       # untimed batches are staged just in time
             staged[i] = stage(i)
         q, kn, vn, out, x = staged[i]
         h0 = time.perf_counter()
-        plan = eng.plan(tokens[i])
-        h1 = time.perf_counter()
-        db = eng.upload(plan)
-        h2 = time.perf_counter()
+        db = eng.prepare(tokens[i])              # hash + plan + work plan + H2D, one native call
+        plan = db.plan
+        h1 = h2 = time.perf_counter()
         if ev is not None:
             ev[0].record()
         if layer:
@@ -311,8 +310,7 @@ def main():
         eng.release()
         h4 = time.perf_counter()
         if ev is not None:
-            host_t["plan"] += h1 - h0
-            host_t["upload"] += h2 - h1
+            host_t["prepare"] += h1 - h0
             host_t["launch"] += h3 - h2
             host_t["release"] += h4 - h3
         return plan, db

@@ -258,6 +258,34 @@ int32_t arckv_attention_plan(const int32_t* cu_q, const int32_t* seq_lens, int32
                              int64_t* n_work, int64_t* n_combine, int64_t* ws_bytes,
                              int32_t* tile_cols);
 
+/* ---------------------------------------------------------------------------------------
+ * Host: one batch's whole preparation in one call (Sec. 2 prefix caching and paged KV, Sec. 3
+ * block-level eviction): arckv_hash_blocks_batch of every prompt (root `root`),
+ * arckv_plan_batch on `cache`, then arckv_attention_plan, with the same results as those
+ * calls in sequence.  Everything the device steps read is written into `packed` (host
+ * int32; pinned memory lets one asynchronous copy move it), at the offsets reported:
+ *   block_tables [n_reqs][bt_stride] | cu_q [n_reqs + 1] | seq_lens [n_reqs] |
+ *   slot_mapping [n_slots] | work items [n_work + n_combine][ARCKV_WORK_INTS]
+ * prefix_lens and hit_blocks (host, [n_reqs]) receive P and k per request.  bt_stride is the
+ * smallest that fits (max ceil(n_tokens / 16)).  packed_cap must reach an upper bound that
+ * depends only on the prompt lengths, heads and num_cus: if it does not, ENOSPC with the
+ * bound in out->n_packed and the cache unchanged.  Other errors as for the three calls
+ * (a plan error leaves the cache unchanged; the batch is in flight on success). */
+typedef struct {
+  int32_t n_reqs, bt_stride;
+  int64_t off_block_tables, off_cu_q, off_seq_lens, off_slots, off_work; /* in int32 units  */
+  int64_t n_packed;        /* ints written (on ENOSPC: the capacity needed)                */
+  int64_t n_slots;         /* sum of S                                                     */
+  int64_t n_work, n_combine, ws_bytes;  /* as from arckv_attention_plan                    */
+  int32_t tile_cols, max_q_len, max_seq_len;
+} arckv_batch;
+
+int32_t arckv_prepare_batch(arckv_cache* cache, const int32_t* const* tokens,
+                            const int64_t* n_tokens, int32_t n_reqs, uint64_t root,
+                            int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                            int32_t num_cus, int32_t* packed, int64_t packed_cap,
+                            int32_t* prefix_lens, int32_t* hit_blocks, arckv_batch* out);
+
 /* Runs attention for one planned batch.
  * k_pool, v_pool: device, layout V1 (num_blocks blocks).  q: device bf16
  * [n_q][num_q_heads][head_dim], rows ordered by cu_q.  out: device bf16, same shape.

@@ -82,6 +82,16 @@ class BatchPlan:
         return len(self.seq_lens)
 
 
+@dataclass
+class PreparedBatch:
+    """What arckv_prepare_batch wrote: the plan and the attention work plan (copies), and the
+    packed int32 metadata (`packed[:n_packed]`, the caller's buffer) in the device layout."""
+    plan: BatchPlan
+    attn: "AttnPlan"
+    info: dict                 # bt_stride, off_* (int32 offsets into packed), n_packed, ...
+    packed: np.ndarray
+
+
 class BlockCache:
     """Host ARC (or LRU) cache with physical block placement; plans batches."""
 
@@ -129,6 +139,42 @@ class BlockCache:
                         _ptr(hb, _lib.i32), _ptr(slots, _lib.i32), cap, 0, 0, 0)
         _lib.check(lib().arckv_plan_batch(self._h, arr, n, C.byref(pc)), "arckv_plan_batch")
         return BatchPlan(bt, cu, sl, pl, hb, slots[: pc.n_slots].copy(), pc.max_q_len, pc.max_seq_len)
+
+    def prepare_native(self, token_lists, num_q_heads: int, num_kv_heads: int, head_dim: int,
+                       num_cus: int, packed: np.ndarray, root: int = 0):
+        """One call of arckv_prepare_batch into `packed` (contiguous writable int32).  Returns
+        (status, info dict, prefix_lens, hit_blocks) without raising; on ENOSPC info["n_packed"]
+        is the capacity needed (the cache is then unchanged)."""
+        toks = [t if (t.dtype == np.int32 and t.flags.c_contiguous) else np.ascontiguousarray(t, dtype=np.int32)
+                for t in token_lists]
+        n = len(toks)
+        addrs = np.fromiter((t.__array_interface__["data"][0] for t in toks), dtype=np.uint64, count=n)
+        lens = np.fromiter((t.shape[0] for t in toks), dtype=np.int64, count=n)
+        pl = np.empty(max(n, 1), dtype=np.int32)
+        hb = np.empty(max(n, 1), dtype=np.int32)
+        info = _lib.BatchC()
+        cap = 0 if packed is None else packed.size
+        st = lib().arckv_prepare_batch(self._h, addrs.__array_interface__["data"][0],
+                                       lens.__array_interface__["data"][0], n, root, num_q_heads,
+                                       num_kv_heads, head_dim, num_cus,
+                                       None if packed is None else packed.__array_interface__["data"][0],
+                                       cap, pl.__array_interface__["data"][0],
+                                       hb.__array_interface__["data"][0], C.byref(info))
+        d = {k: getattr(info, k) for k, _ in _lib.BatchC._fields_}
+        return st, d, pl[:n], hb[:n]
+
+    def prepare_batch(self, token_lists, num_q_heads: int, num_kv_heads: int, head_dim: int,
+                      num_cus: int = 256, packed: np.ndarray | None = None, root: int = 0) -> PreparedBatch:
+        """Hash, plan and work-plan one batch in one native call; `packed` grows if too small."""
+        while True:
+            st, d, pl, hb = self.prepare_native(token_lists, num_q_heads, num_kv_heads, head_dim,
+                                                num_cus, packed, root)
+            if st == _lib.ENOSPC and (packed is None or d["n_packed"] > packed.size):
+                packed = np.empty(d["n_packed"], dtype=np.int32)
+                continue
+            _lib.check(st, "arckv_prepare_batch")
+            break
+        return PreparedBatch(*unpack_prepared(packed, d, pl, hb), d, packed)
 
     def release_batch(self):
         _lib.check(lib().arckv_release_batch(self._h), "arckv_release_batch")
@@ -271,6 +317,23 @@ def attention_plan(cu_q, seq_lens, num_q_heads: int, num_kv_heads: int, head_dim
                                       C.byref(nw), C.byref(nc), C.byref(ws), C.byref(tc)),
                "arckv_attention_plan")
     return AttnPlan(work, int(nw.value), int(nc.value), int(ws.value), int(tc.value))
+
+
+def unpack_prepared(packed: np.ndarray, d: dict, prefix_lens, hit_blocks):
+    """(BatchPlan, AttnPlan) copies out of a packed buffer written by arckv_prepare_batch."""
+    n, stride = d["n_reqs"], d["bt_stride"]
+    o = d["off_block_tables"]
+    bt = packed[o:o + n * stride].reshape(n, stride).copy()
+    cu = packed[d["off_cu_q"]:d["off_cu_q"] + n + 1].copy()
+    sl = packed[d["off_seq_lens"]:d["off_seq_lens"] + n].copy()
+    slots = packed[d["off_slots"]:d["off_slots"] + d["n_slots"]].copy()
+    nw = d["n_work"] + d["n_combine"]
+    work = packed[d["off_work"]:d["off_work"] + nw * WORK_INTS].reshape(nw, WORK_INTS).copy()
+    if nw == 0:
+        work = np.zeros((1, WORK_INTS), dtype=np.int32)
+    plan = BatchPlan(bt, cu, sl, np.array(prefix_lens, dtype=np.int32), np.array(hit_blocks, dtype=np.int32),
+                     slots, d["max_q_len"], d["max_seq_len"])
+    return plan, AttnPlan(work, d["n_work"], d["n_combine"], d["ws_bytes"], d["tile_cols"])
 
 
 def prefill_attention(k_pool, v_pool, q, out, block_tables, cu_q, seq_lens, work, n_work: int,

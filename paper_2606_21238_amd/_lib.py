@@ -34,6 +34,13 @@ class PlanC(C.Structure):
                 ("slot_cap", i64), ("n_slots", i64), ("max_q_len", i32), ("max_seq_len", i32)]
 
 
+class BatchC(C.Structure):
+    _fields_ = [("n_reqs", i32), ("bt_stride", i32), ("off_block_tables", i64), ("off_cu_q", i64),
+                ("off_seq_lens", i64), ("off_slots", i64), ("off_work", i64), ("n_packed", i64),
+                ("n_slots", i64), ("n_work", i64), ("n_combine", i64), ("ws_bytes", i64),
+                ("tile_cols", i32), ("max_q_len", i32), ("max_seq_len", i32)]
+
+
 class Stats(C.Structure):
     _fields_ = [("t1", i64), ("t2", i64), ("b1", i64), ("b2", i64), ("p", f64), ("capacity", i64),
                 ("references", i64), ("requests", i64), ("prompt_tokens", i64),
@@ -65,6 +72,8 @@ _SIGS = {
     "arckv_qkv_rope": (i32, [vp, vp, i64, i32, i32, i32, i32, vp, vp, i32, f64, vp, i64, vp, vp, vp, vp]),
     "arckv_attention_plan": (i32, [P_i32, P_i32, i32, i32, i32, i32, i32, P_i32, i64, P_i64, P_i64,
                                    P_i64, P_i32]),
+    "arckv_prepare_batch": (i32, [vp, vp, vp, i32, u64, i32, i32, i32, i32, vp, i64, vp, vp,
+                                  C.POINTER(BatchC)]),
     "arckv_prefill_attention": (i32, [vp, vp, vp, vp, vp, i32, vp, vp, i32, i64, i64, vp, i64, i64,
                                       i32, i32, i32, i32, f32, vp, i64, vp]),
     "arckv_prefill_attention_timed": (i32, [vp, vp, vp, vp, vp, i32, vp, vp, i32, i64, i64, vp, i64,

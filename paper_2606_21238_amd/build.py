@@ -22,7 +22,7 @@ LIBDIR = os.path.join(PKG, "lib")
 LIB = os.path.join(LIBDIR, "libarckv.so")
 ARCH = "gfx950"
 
-HOST_SRC = ["host/blockhash.cpp", "host/cache.cpp", "host/attn_plan.cpp", "host/errors.cpp"]
+HOST_SRC = ["host/blockhash.cpp", "host/cache.cpp", "host/attn_plan.cpp", "host/prepare.cpp", "host/errors.cpp"]
 HIP_SRC = ["kernels/kv_scatter.hip", "kernels/prefill_attn.hip", "kernels/qkv_rope.hip"]
 
 

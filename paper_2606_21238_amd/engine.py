@@ -12,7 +12,7 @@ from dataclasses import dataclass
 
 import numpy as np
 
-from . import (BlockCache, BatchPlan, attention_plan, hash_blocks_batch, lib)
+from . import (BlockCache, BatchPlan, attention_plan, hash_blocks_batch, lib, unpack_prepared)
 from . import _lib
 
 
@@ -69,6 +69,43 @@ class PrefillEngine:
 
     def release(self):
         self.cache.release_batch()
+
+    def prepare(self, token_lists, stream=None) -> DeviceBatch:
+        """plan() + upload() in one native call (arckv_prepare_batch): hashes, the cache plan
+        and the attention work plan are written straight into the next pinned staging buffer of
+        the ring, then one asynchronous copy moves them to the device."""
+        import torch
+        t = self._turn
+        self._turn = (t + 1) % self._ring
+        if self._stage_ev[t] is not None:
+            self._stage_ev[t].synchronize()          # the copy that last read this buffer is done
+        while True:
+            host = None if self._stage[t] is None else self._stage[t].numpy()
+            st, d, pl, hb = self.cache.prepare_native(token_lists, self.hq, self.hkv, self.d, self.num_cus, host)
+            if st == _lib.ENOSPC and (host is None or d["n_packed"] > host.size):
+                cap = max(d["n_packed"], 1 << 16) * 2
+                self._stage[t] = torch.empty(cap, dtype=torch.int32, pin_memory=True)
+                self._dev_meta[t] = torch.empty(cap, dtype=torch.int32, device=self.device)
+                continue
+            _lib.check(st, "arckv_prepare_batch")
+            break
+        n_int = d["n_packed"]
+        dev = self._dev_meta[t][:n_int]
+        dev.copy_(self._stage[t][:n_int], non_blocking=True)
+        ev = torch.cuda.Event()
+        ev.record()
+        self._stage_ev[t] = ev
+        plan, ap = unpack_prepared(host, d, pl, hb)
+        n, stride = d["n_reqs"], d["bt_stride"]
+        bt = dev[d["off_block_tables"]:d["off_block_tables"] + n * stride].view(n, stride)
+        cu = dev[d["off_cu_q"]:d["off_cu_q"] + n + 1]
+        sl = dev[d["off_seq_lens"]:d["off_seq_lens"] + n]
+        sm = dev[d["off_slots"]:d["off_slots"] + d["n_slots"]]
+        wk = dev[d["off_work"]:d["off_work"] + (d["n_work"] + d["n_combine"]) * 8].view(-1, 8)
+        if d["ws_bytes"] > self._ws.numel():
+            self._ws = torch.empty(d["ws_bytes"], dtype=torch.uint8, device=self.device)
+        return DeviceBatch(plan, bt, cu, sl, sm, wk, d["n_work"], d["n_combine"], d["ws_bytes"],
+                           d["tile_cols"], int(d["n_slots"]), wk.data_ptr())
 
     def upload(self, plan: BatchPlan, stream=None) -> DeviceBatch:
         import torch
@@ -170,9 +207,9 @@ class PrefillEngine:
         """One batch: plan, upload, scatter, attend, release.  qkv_for_plan(plan) returns the
         computed tokens' (q, k_new, v_new) device tensors.  Returns (plan, out)."""
         import torch
-        plan = self.plan(token_lists)
+        db = self.prepare(token_lists, stream)
+        plan = db.plan
         try:
-            db = self.upload(plan, stream)
             q, k_new, v_new = qkv_for_plan(plan)
             out = torch.empty_like(q)
             self.scatter(db, k_new, v_new, stream)

@@ -53,14 +53,14 @@ class StreamRun:
         cfg = self.cfg
         toks = [r.tokens for r in reqs]
         oplan = self.orc.plan_batch(list(zip(obh.hash_blocks_many(toks), map(len, toks))))
-        plan = self.eng.plan(toks)
+        db = self.eng.prepare(toks)          # hash + plan + work plan in one native call
+        plan = db.plan
         assert plan.prefix_lens.tolist() == oplan.prefix_lens
         assert plan.slot_mapping.tolist() == oplan.slot_mapping
         assert plan.cu_q.tolist() == oplan.cu_q
         for r, row in enumerate(oplan.block_tables):
             assert plan.block_tables[r, : len(row)].tolist() == row
         self.hit_tokens += sum(oplan.prefix_lens)
-        db = self.eng.upload(plan)
         q, kn, vn = self.bank.batch_suffix(reqs, oplan.prefix_lens)
         out = torch.empty_like(q)
         self.eng.scatter(db, kn, vn)
