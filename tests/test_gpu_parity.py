@@ -22,7 +22,7 @@ from oracle import blockhash as obh  # noqa: E402
 from oracle import kvpool as okv  # noqa: E402
 from oracle.planner import Planner, form_batches  # noqa: E402
 from workloads import get_config  # noqa: E402
-from workloads.streams import TensorBank, free_order, make_stream, stream_docqa_hit  # noqa: E402
+from workloads.streams import TensorBank, free_order, make_stream, steps_short, stream_docqa_hit  # noqa: E402
 from tests.gpu_helpers import bits, compare, print_case, sample_rows  # noqa: E402
 
 DEV = "cuda"
@@ -231,16 +231,22 @@ class Lockstep:
         self.okp, self.ovp = okv.new_pool(cfg.num_phys, cfg.num_kv_heads, cfg.head_dim)
         self.bank = TensorBank(cfg, DEV)
 
-    def batch(self, reqs, rows_fn=None, check_pool=True):
+    def batch(self, reqs, rows_fn=None, check_pool=True, native_prepare=False):
+        """native_prepare: the engine's one-call path (arckv_prepare_batch) instead of
+        plan() + upload()."""
         cfg = self.cfg
         toks = [r.tokens for r in reqs]
         oplan = self.orc.plan_batch([(obh.hash_blocks(t), len(t)) for t in toks])
-        plan = self.eng.plan(toks)
+        if native_prepare:
+            db = self.eng.prepare(toks)
+            plan = db.plan
+        else:
+            plan = self.eng.plan(toks)
+            db = self.eng.upload(plan)
         assert plan.prefix_lens.tolist() == oplan.prefix_lens
         assert plan.slot_mapping.tolist() == oplan.slot_mapping
         for r, row in enumerate(oplan.block_tables):
             assert plan.block_tables[r, : len(row)].tolist() == row
-        db = self.eng.upload(plan)
         q, kn, vn = self.bank.batch_suffix(reqs, oplan.prefix_lens)
         out = torch.empty_like(q)
         self.eng.scatter(db, kn, vn)
@@ -296,6 +302,36 @@ def test_docqa_stream_batches():
     for a, b in form_batches([r.n_tokens for r in stream], cfg.max_batch, cfg.capacity, cfg.scratch):
         _, got, ref = ls.batch(stream[a:b], rows_fn=fn)
         compare(got, ref, f"docqa batch {a}")
+
+
+def test_short32_full_batches():
+    """The short32 bench shape: 16 cached lognormal histories + 32 new tokens each."""
+    cfg = get_config("short")
+    print_case("config short32 (16 x (history + 32)), row-sampled, native prepare")
+    ls = Lockstep(cfg)
+    warm, steps = steps_short(cfg, 2, 32)
+    rng = np.random.default_rng(6)
+    for w in warm:
+        ls.batch(w, rows_fn=lambda r, p: [0, int(p.cu_q[r + 1] - p.cu_q[r]) - 1], native_prepare=True)
+    for k, b in enumerate(steps):
+        plan, got, ref = ls.batch(b, rows_fn=lambda r, p: sample_rows(32, rng, 8), native_prepare=True)
+        assert all(s == 32 for s in np.diff(plan.cu_q))
+        compare(got, ref, f"short32 step {k}")
+
+
+def test_decode_full_batch():
+    """The decode bench shape: 64 cached lognormal histories + 1 new token each (32-column
+    tiles, split key ranges), every row checked."""
+    cfg = get_config("decode")
+    print_case("config decode (64 x (history + 1)), all rows, native prepare")
+    ls = Lockstep(cfg)
+    warm, steps = steps_short(cfg, 2, 1, batch=cfg.max_batch, n_sessions=cfg.max_batch)
+    for w in warm:
+        ls.batch(w, rows_fn=lambda r, p: [int(p.cu_q[r + 1] - p.cu_q[r]) - 1], native_prepare=True)
+    for k, b in enumerate(steps):
+        plan, got, ref = ls.batch(b, native_prepare=True)
+        assert len(b) == 64 and all(s == 1 for s in np.diff(plan.cu_q))
+        compare(got, ref, f"decode step {k}")
 
 
 def test_longctx_sampled_rows():
