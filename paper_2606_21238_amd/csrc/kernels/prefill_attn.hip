@@ -546,18 +546,23 @@ __global__ __launch_bounds__(64 * NW, 1) void prefill_attn_kernel(
 
 // Merges the key-range splits of one query tile: o = sum_s 2^(lse_s - M) O_s / sum_s 2^(lse_s - M)
 // with M = max_s lse_s, per column.  Grid: (combine items, tile_cols / kCombineCols); a block
-// takes kCombineCols columns: it first turns the pieces' lse into per-column weights in LDS
-// (one round of loads), then each thread sums its columns' float4 slices over the pieces with
-// all of a group of pieces' loads in flight at once (a second round).
+// takes kCombineCols columns.  The first pieces' partial O (kCombinePre of them) and the lse
+// of up to kCombineMaxSplits pieces are all requested at once, since the partials do not
+// depend on the weights: one memory round trip instead of one for the lse, one for the
+// weights and one for the partials.  The lse then turn into per-column weights in LDS, the
+// preloaded partials are summed, and any further pieces stream with several loads in flight.
+// The sums run over the pieces in order, as a plain loop would.
 constexpr int kCombineThreads = 256;
 constexpr int kCombineCols = 32;
 constexpr int kCombineMaxSplits = 64;  // pieces weighted in LDS at a time
+constexpr int kCombinePre = 4;         // pieces loaded before their weights are known
+
 template <int D>
 __global__ __launch_bounds__(kCombineThreads) void attn_combine_kernel(
     uint16_t* __restrict__ out, const Work* __restrict__ items, const int32_t* __restrict__ cu_q,
     int n_reqs, int64_t n_q, int hq, int G, int tile_cols, const float* __restrict__ ws_o,
     const float* __restrict__ ws_lse, int64_t ws_slots) {
-  __shared__ float wt[kCombineMaxSplits][kCombineCols];
+  __shared__ float wt[kCombineMaxSplits][kCombineCols];  // lse of a batch of pieces, then weights
   __shared__ float mx[kCombineCols], inv[kCombineCols];
   const Work w = items[blockIdx.x];  // {req, kvh, col_start, slot0, n_splits}
   const int slot0 = w.kv_start, ns = w.kv_end;
@@ -568,24 +573,62 @@ __global__ __launch_bounds__(kCombineThreads) void attn_combine_kernel(
   const int ncols = (cu_q[w.req + 1] - q0) * G;
   const int c0 = blockIdx.y * kCombineCols;  // first local column of this block
   constexpr int D4 = D / 4;
-  const int tid = threadIdx.x;
-  // per-column maximum of the pieces' lse
-  if (tid < kCombineCols) {
-    float m = -INFINITY;
-    for (int s = 0; s < ns; ++s)
-      m = fmaxf(m, ws_lse[static_cast<int64_t>(slot0 + s) * tile_cols + c0 + tid]);
-    mx[tid] = m;
-  }
-  __syncthreads();
-  f32x4_t acc[kCombineCols * D4 / kCombineThreads];
   constexpr int PER = kCombineCols * D4 / kCombineThreads;  // float4 slices per thread
   static_assert(PER * kCombineThreads == kCombineCols * D4, "combine split");
+  const int tid = threadIdx.x;
+  // slice k of this thread: block column (tid + k * threads) / D4, dims 4 * ((tid + k * threads) % D4)
+  auto slice = [&](int s, int k) -> f32x4_t {
+    const int e = tid + k * kCombineThreads;
+    const float* po = ws_o + (static_cast<int64_t>(slot0 + s) * tile_cols + c0) * D;
+    return *reinterpret_cast<const f32x4_t*>(po + static_cast<int64_t>(e / D4) * D + 4 * (e % D4));
+  };
+  f32x4_t pre[kCombinePre][PER];
 #pragma unroll
-  for (int k = 0; k < PER; ++k) acc[k] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  for (int s = 0; s < kCombinePre; ++s)
+#pragma unroll
+    for (int k = 0; k < PER; ++k) pre[s][k] = s < ns ? slice(s, k) : f32x4_t{0.f, 0.f, 0.f, 0.f};
+  const int nb0 = min(kCombineMaxSplits, ns);
+  for (int e = tid; e < nb0 * kCombineCols; e += kCombineThreads) {
+    const int s = e / kCombineCols, c = e % kCombineCols;
+    wt[s][c] = ws_lse[static_cast<int64_t>(slot0 + s) * tile_cols + c0 + c];
+  }
+  __syncthreads();
+  // per column: the maximum over all pieces, then the first batch's weights and their sum
   float wsum_part = 0.f;
-  for (int sb = 0; sb < ns; sb += kCombineMaxSplits) {
+  if (tid < kCombineCols) {
+    float m = -INFINITY;
+    for (int s = 0; s < nb0; ++s) m = fmaxf(m, wt[s][tid]);
+    for (int s = nb0; s < ns; ++s)
+      m = fmaxf(m, ws_lse[static_cast<int64_t>(slot0 + s) * tile_cols + c0 + tid]);
+    mx[tid] = m;
+    for (int s = 0; s < nb0; ++s) {
+      const float l = wt[s][tid];
+      const float x = l == -INFINITY ? 0.f : fast_exp2(l - m);
+      wt[s][tid] = x;
+      wsum_part += x;
+    }
+  }
+  __syncthreads();
+  f32x4_t acc[PER];
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    acc[k] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int s = 0; s < kCombinePre; ++s)
+      if (s < ns) acc[k] += wt[s][(tid + k * kCombineThreads) / D4] * pre[s][k];
+  }
+#pragma unroll 4
+  for (int s = kCombinePre; s < nb0; ++s) {
+    f32x4_t v[PER];
+#pragma unroll
+    for (int k = 0; k < PER; ++k) v[k] = slice(s, k);
+#pragma unroll
+    for (int k = 0; k < PER; ++k) acc[k] += wt[s][(tid + k * kCombineThreads) / D4] * v[k];
+  }
+  // more than kCombineMaxSplits pieces: further batches, weighted with the same maximum
+  for (int sb = nb0; sb < ns; sb += kCombineMaxSplits) {
     const int nb = min(kCombineMaxSplits, ns - sb);
-    // weights of pieces [sb, sb + nb) for the block's columns
+    __syncthreads();  // every thread is done with the previous batch's weights
     for (int e = tid; e < nb * kCombineCols; e += kCombineThreads) {
       const int s = e / kCombineCols, c = e % kCombineCols;
       const float l = ws_lse[static_cast<int64_t>(slot0 + sb + s) * tile_cols + c0 + c];
@@ -596,17 +639,12 @@ __global__ __launch_bounds__(kCombineThreads) void attn_combine_kernel(
       for (int s = 0; s < nb; ++s) wsum_part += wt[s][tid];
 #pragma unroll 4
     for (int s = 0; s < nb; ++s) {
-      const float* po = ws_o + (static_cast<int64_t>(slot0 + sb + s) * tile_cols + c0) * D;
       f32x4_t v[PER];
 #pragma unroll
-      for (int k = 0; k < PER; ++k) {
-        const int e = tid + k * kCombineThreads;  // column e / D4, slice e % D4
-        v[k] = *reinterpret_cast<const f32x4_t*>(po + static_cast<int64_t>(e / D4) * D + 4 * (e % D4));
-      }
+      for (int k = 0; k < PER; ++k) v[k] = slice(sb + s, k);
 #pragma unroll
       for (int k = 0; k < PER; ++k) acc[k] += wt[s][(tid + k * kCombineThreads) / D4] * v[k];
     }
-    __syncthreads();
   }
   if (tid < kCombineCols) inv[tid] = wsum_part > 0.f ? 1.f / wsum_part : 0.f;
   __syncthreads();
@@ -623,10 +661,7 @@ __global__ __launch_bounds__(kCombineThreads) void attn_combine_kernel(
   }
 }
 
-#ifndef ARCKV_WIDE_NB
-#define ARCKV_WIDE_NB 1
-#endif
-constexpr int kWideNB = ARCKV_WIDE_NB;
+constexpr int kWideNB = 1;  // 32-column MFMA blocks per wave on wide tiles
 constexpr int kWideWaves = arckv::kWideCols / (32 * kWideNB);
 static_assert(kWideWaves * 32 * kWideNB == arckv::kWideCols, "wide tile width");
 

@@ -147,6 +147,7 @@ SWEEP = [
     ([(4000, 3949), (130, 78), (6, 0)], 40, 8, 128),    # 255, 260 and 30 columns
     ([(700, 600), (33, 0), (1, 0)], 10, 2, 64),
     ([(L, L - 1) for L in (1, 17, 300, 4097, 65, 2000)], 40, 8, 128),   # decode: tiny tiles
+    ([(40000, 39999)], 8, 1, 64),        # 79 pieces of one tile: the combine's second batch of 64
 ]
 
 
