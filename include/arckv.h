@@ -269,8 +269,9 @@ int32_t arckv_attention_plan(const int32_t* cu_q, const int32_t* seq_lens, int32
  * prefix_lens and hit_blocks (host, [n_reqs]) receive P and k per request.  bt_stride is the
  * smallest that fits (max ceil(n_tokens / 16)).  packed_cap must reach an upper bound that
  * depends only on the prompt lengths, heads and num_cus: if it does not, ENOSPC with the
- * bound in out->n_packed and the cache unchanged.  Other errors as for the three calls
- * (a plan error leaves the cache unchanged; the batch is in flight on success). */
+ * bound in out->n_packed and the cache unchanged.  n_reqs >= 1 and every n_tokens >= 1 (else
+ * EINVAL).  Other errors as for the three calls (a plan error leaves the cache unchanged; the
+ * batch is in flight on success, to be ended with arckv_release_batch). */
 typedef struct {
   int32_t n_reqs, bt_stride;
   int64_t off_block_tables, off_cu_q, off_seq_lens, off_slots, off_work; /* in int32 units  */
