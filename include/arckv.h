@@ -56,6 +56,7 @@ extern "C" {
 #define ARCKV_POLICY_ARC 0
 #define ARCKV_POLICY_LRU 1
 #define ARCKV_POLICY_DBL 2 /* ARC with p fixed at c/2 (Sec. 4's static two-queue variant) */
+#define ARCKV_POLICY_FRC 3 /* ARC with p fixed at cfg.frc_p (the fixed-target form FRC_p)  */
 #define ARCKV_REF_TAIL_FIRST 0
 #define ARCKV_REF_HEAD_FIRST 1
 
@@ -108,6 +109,10 @@ int32_t arckv_hash_blocks_batch(const int32_t* const* tokens, const int64_t* n_t
  * of the page its reference evicted, else the head of a FIFO free list.
  * DBL (Sec. 4: a fixed 1:1 split between the recency and the frequency queue) runs the same
  * rules with p held at c/2: ghost hits move the page and call REPLACE but do not steer p.
+ * FRC holds p at any given value in [0, c] the same way (DBL is FRC at c/2).
+ * A page is "born" in a batch when a reference of that batch creates it (a miss) or brings
+ * it back from a ghost list; with no_intra_batch_reuse, the prefix lookup of a request stops
+ * at the first such page (it is then referenced as usual, an orphan whose KV is rewritten).
  * Length-aware victims (Sec. 6 proposes weighing prompt length beside recency and
  * frequency): with victim_window W > 1, wherever a policy evicts from a resident list
  * (REPLACE, ARC's IV-A T1 drop, LRU), it takes, among the W least recently used unpinned
@@ -119,7 +124,7 @@ int32_t arckv_hash_blocks_batch(const int32_t* const* tokens, const int64_t* n_t
 typedef struct arckv_cache arckv_cache;
 
 typedef struct {
-  int32_t policy;                    /* ARCKV_POLICY_ARC, _LRU or _DBL                   */
+  int32_t policy;                    /* ARCKV_POLICY_ARC, _LRU, _DBL or _FRC             */
   int32_t ref_order;                 /* ARCKV_REF_TAIL_FIRST (default) or HEAD_FIRST     */
   int64_t capacity_blocks;           /* c >= 1: cacheable pages                          */
   int64_t num_phys_blocks;           /* pool size; >= capacity_blocks + scratch_blocks   */
@@ -129,6 +134,11 @@ typedef struct {
                                      /* are the page free list, the rest the scratch FIFO */
   int32_t victim_window;             /* W in [1, 4096] (0 = 1): length-aware victims, see */
                                      /* below; 1 = the LRU-most unpinned page            */
+  int32_t no_intra_batch_reuse;      /* 0 (default): a request may reuse blocks an earlier */
+                                     /* request of its batch created; 1: its prefix stops */
+                                     /* at such a block (engines that cache a block only  */
+                                     /* once its step has run)                            */
+  double frc_p;                      /* ARCKV_POLICY_FRC: the fixed target p, in [0, c]   */
 } arckv_cache_cfg;
 
 /* Creates a cache (host memory only).  EINVAL on a bad configuration. */

@@ -100,14 +100,18 @@ class Event:
 class ARC:
     """ARC(c) with pins and physical block placement (adaptive=False: DBL, p fixed at c/2)."""
 
-    def __init__(self, capacity: int, free_blocks, adaptive: bool = True, window: int = 1):
+    def __init__(self, capacity: int, free_blocks, adaptive: bool = True, window: int = 1,
+                 fixed_p: float | None = None):
+        """adaptive=False: the fixed-target form, p = fixed_p (c/2 when None: DBL)."""
         if capacity < 1 or window < 1:
             raise ValueError("capacity and window must be >= 1")
         self.c = int(capacity)
         self.adaptive = adaptive
         self.window = int(window)
         self.depth: dict[int, int] = {}       # block index of each key in its prompt
-        self.p = 0.0 if adaptive else self.c / 2.0
+        self.p = 0.0 if adaptive else (self.c / 2.0 if fixed_p is None else float(fixed_p))
+        if not 0.0 <= self.p <= self.c:
+            raise ValueError("fixed p must lie in [0, c]")
         # OrderedDicts in LRU -> MRU order; resident lists map key -> physical block.
         self.T1: OrderedDict[int, int] = OrderedDict()
         self.T2: OrderedDict[int, int] = OrderedDict()

@@ -10,7 +10,10 @@ Readings fixed by this project where the paper is silent:
 
 * Request order.  Requests of a batch are planned one after another; a later
   request may hit blocks an earlier request of the same batch created (the
-  scatter of the whole batch is ordered before its attention).
+  scatter of the whole batch is ordered before its attention).  With
+  ``intra_batch_reuse=False`` the prefix lookup stops at a block that a reference
+  of the current batch made resident (a miss or a ghost hit); it is then
+  referenced like any resident block (an orphan, recomputed).
 * Prefix lookup.  k = number of leading full blocks whose identity is resident
   (in T1 or T2 for ARC).  If that covers the whole prompt (16 k == L) the last
   block is recomputed (k -> k - 1) so that at least one query produces the
@@ -43,7 +46,7 @@ from __future__ import annotations
 from collections import deque
 from dataclasses import dataclass, field
 
-from .arc import ARC
+from .arc import ARC, CASE_I, LRU_HIT
 from .lru import LRU
 
 BLOCK_TOKENS = 16
@@ -101,7 +104,8 @@ def form_batches(n_tokens_list, max_batch: int, capacity: int, scratch_blocks: i
 
 class Planner:
     def __init__(self, policy: str, capacity: int, num_phys: int, scratch_blocks: int,
-                 initial_order=None, ref_order: str = "tail_first", victim_window: int = 1):
+                 initial_order=None, ref_order: str = "tail_first", victim_window: int = 1,
+                 intra_batch_reuse: bool = True, frc_p: float = 0.0):
         order = list(range(num_phys)) if initial_order is None else [int(b) for b in initial_order]
         if sorted(order) != list(range(num_phys)):
             raise PlanError("EINVAL", "initial order is not a permutation of the pool")
@@ -114,6 +118,10 @@ class Planner:
             self.cache = ARC(capacity, pages, window=victim_window)
         elif policy == "dbl":
             self.cache = ARC(capacity, pages, adaptive=False, window=victim_window)
+        elif policy == "frc":
+            if not 0.0 <= frc_p <= capacity:
+                raise PlanError("EINVAL", "frc_p outside [0, c]")
+            self.cache = ARC(capacity, pages, adaptive=False, window=victim_window, fixed_p=frc_p)
         elif policy == "lru":
             self.cache = LRU(capacity, pages, window=victim_window)
         else:
@@ -122,6 +130,8 @@ class Planner:
             raise PlanError("EINVAL", "ref_order")
         self.ref_order = ref_order
         self.capacity = capacity
+        self.intra_batch_reuse = intra_batch_reuse
+        self.born: set[int] = set()      # keys a reference of the batch made resident
         self.in_flight = False
         self.batch_scratch: list[int] = []
         self.totals = Totals()
@@ -146,7 +156,8 @@ class Planner:
         for hashes, n_tok in reqs:
             n_full = len(hashes)
             k = 0
-            while k < n_full and cache.resident(hashes[k]):
+            while k < n_full and cache.resident(hashes[k]) and \
+                    (self.intra_batch_reuse or hashes[k] not in self.born):
                 k += 1
             if BLOCK_TOKENS * k == n_tok:
                 k -= 1
@@ -156,6 +167,8 @@ class Planner:
             phys = [None] * n_full
             for i in order:
                 ev = cache.reference(hashes[i], depth=i)
+                if ev.case not in (CASE_I, LRU_HIT):      # a miss or a ghost hit
+                    self.born.add(hashes[i])
                 phys[i] = ev.phys
                 cache.pin(hashes[i])
                 self.totals.case_counts[ev.case] += 1
@@ -184,6 +197,7 @@ class Planner:
         if not self.in_flight:
             raise PlanError("ESTATE", "no batch to release")
         self.cache.unpin_all()
+        self.born.clear()
         self.scratch.extend(self.batch_scratch)
         self.batch_scratch = []
         self.in_flight = False

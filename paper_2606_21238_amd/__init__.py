@@ -96,12 +96,17 @@ class BlockCache:
     """Host ARC (or LRU) cache with physical block placement; plans batches."""
 
     def __init__(self, policy: str, capacity: int, num_phys: int, scratch: int,
-                 initial_order=None, ref_order: str = "tail_first", victim_window: int = 1):
-        """victim_window W > 1: length-aware victims (the deepest of the W least recently used
-        unpinned pages of the list a policy evicts from); 1 is the plain policy."""
+                 initial_order=None, ref_order: str = "tail_first", victim_window: int = 1,
+                 intra_batch_reuse: bool = True, frc_p: float = 0.0):
+        """policy: arc, lru, dbl (p fixed at c/2) or frc (p fixed at frc_p).
+        victim_window W > 1: length-aware victims (the deepest of the W least recently used
+        unpinned pages of the list a policy evicts from); 1 is the plain policy.
+        intra_batch_reuse False: a request's prefix stops at a block an earlier request of the
+        same batch created."""
         self._order = None if initial_order is None else np.ascontiguousarray(initial_order, dtype=np.int32)
         cfg = _lib.CacheCfg(_lib.POLICY[policy], _lib.REF_ORDER[ref_order], capacity, num_phys, scratch,
-                            None if self._order is None else _ptr(self._order, _lib.i32), victim_window)
+                            None if self._order is None else _ptr(self._order, _lib.i32), victim_window,
+                            0 if intra_batch_reuse else 1, float(frc_p))
         h = C.c_void_p()
         _lib.check(lib().arckv_cache_create(C.byref(cfg), C.byref(h)), "arckv_cache_create")
         self._h = h

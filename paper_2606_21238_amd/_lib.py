@@ -10,7 +10,7 @@ LIB_PATH = os.path.join(_PKG, "lib", "libarckv.so")
 
 OK, EINVAL, ENOSPC, EDEVICE, ESTATE, EUNSUPPORTED = 0, -1, -2, -3, -4, -5
 STATUS_NAMES = {0: "OK", -1: "EINVAL", -2: "ENOSPC", -3: "EDEVICE", -4: "ESTATE", -5: "EUNSUPPORTED"}
-POLICY = {"arc": 0, "lru": 1, "dbl": 2}
+POLICY = {"arc": 0, "lru": 1, "dbl": 2, "frc": 3}
 REF_ORDER = {"tail_first": 0, "head_first": 1}
 WORK_INTS = 8
 
@@ -21,7 +21,7 @@ P_i32, P_i64, P_u64 = C.POINTER(i32), C.POINTER(i64), C.POINTER(u64)
 class CacheCfg(C.Structure):
     _fields_ = [("policy", i32), ("ref_order", i32), ("capacity_blocks", i64),
                 ("num_phys_blocks", i64), ("scratch_blocks", i64), ("initial_free_order", P_i32),
-                ("victim_window", i32)]
+                ("victim_window", i32), ("no_intra_batch_reuse", i32), ("frc_p", f64)]
 
 
 class Req(C.Structure):

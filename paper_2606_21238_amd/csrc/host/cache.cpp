@@ -37,6 +37,7 @@ namespace {
 struct Node {
   uint64_t key = 0;
   uint64_t pin_epoch = 0;
+  uint64_t born_epoch = 0;  // batch in which a miss or a ghost hit (re)made it resident
   int32_t phys = -1;
   int32_t prev = -1, next = -1;
   int32_t list = ARCKV_LIST_NONE;
@@ -106,6 +107,7 @@ struct arckv_cache {
   int32_t policy = ARCKV_POLICY_ARC;
   int32_t ref_order = ARCKV_REF_TAIL_FIRST;
   int32_t window = 1;  // victim window (length-aware eviction when > 1)
+  bool intra_batch_reuse = true;
   int64_t c = 0;
   int64_t num_phys = 0;
   int64_t n_scratch = 0;
@@ -209,6 +211,12 @@ struct arckv_cache {
     const int32_t n = find(key);
     return n >= 0 && (nodes[n].list == ARCKV_LIST_T1 || nodes[n].list == ARCKV_LIST_T2);
   }
+  // resident and, without intra-batch reuse, not born in the batch being planned
+  bool reusable(uint64_t key) const {
+    const int32_t n = find(key);
+    return n >= 0 && (nodes[n].list == ARCKV_LIST_T1 || nodes[n].list == ARCKV_LIST_T2) &&
+           (intra_batch_reuse || nodes[n].born_epoch != epoch);
+  }
   void drop_lru(int32_t list, arckv_event& ev) {
     const int32_t n = lists[list].head;
     ev.dropped = nodes[n].key;
@@ -258,7 +266,7 @@ struct arckv_cache {
       const double b2 = static_cast<double>(lists[ARCKV_LIST_B2].size);
       const bool in_b2 = where == ARCKV_LIST_B2;
       if (policy != ARCKV_POLICY_ARC) {
-        // DBL: the target stays at c/2
+        // DBL / FRC: the target stays where it was set
       } else if (!in_b2) {
         const double d1 = b1 >= b2 ? 1.0 : b2 / b1;
         p = std::min(p + d1, static_cast<double>(c_));
@@ -269,6 +277,7 @@ struct arckv_cache {
       if (!replace(in_b2, v)) return arckv::fail(ARCKV_ENOSPC, "REPLACE: every page pinned");
       unlink(n);
       nodes[n].phys = v.phys;
+      nodes[n].born_epoch = epoch;
       push_mru(n, ARCKV_LIST_T2);
       ev.kase = in_b2 ? ARCKV_CASE_III : ARCKV_CASE_II;
     } else {                                                          // Case IV
@@ -304,6 +313,7 @@ struct arckv_cache {
         ev.kase = ARCKV_CASE_IVB;
       }
       n = new_node(x, phys);
+      nodes[n].born_epoch = epoch;
       push_mru(n, ARCKV_LIST_T1);
     }
     ev.evicted = v.from != ARCKV_LIST_NONE ? v.key : 0;
@@ -335,6 +345,7 @@ struct arckv_cache {
         if (st != ARCKV_OK) return st;
       }
       n = new_node(x, phys);
+      nodes[n].born_epoch = epoch;
       push_mru(n, ARCKV_LIST_T1);
       ev.kase = ARCKV_CASE_LRU_MISS;
     }
@@ -368,8 +379,13 @@ extern "C" int32_t arckv_cache_create(const arckv_cache_cfg* cfg, arckv_cache** 
   if (cfg == nullptr || out == nullptr) return arckv::fail(ARCKV_EINVAL, "cache_create: NULL");
   *out = nullptr;
   if (cfg->policy != ARCKV_POLICY_ARC && cfg->policy != ARCKV_POLICY_LRU &&
-      cfg->policy != ARCKV_POLICY_DBL)
+      cfg->policy != ARCKV_POLICY_DBL && cfg->policy != ARCKV_POLICY_FRC)
     return arckv::fail(ARCKV_EINVAL, "cache_create: unknown policy %d", cfg->policy);
+  if (cfg->policy == ARCKV_POLICY_FRC &&
+      !(cfg->frc_p >= 0.0 && cfg->frc_p <= static_cast<double>(cfg->capacity_blocks)))
+    return arckv::fail(ARCKV_EINVAL, "cache_create: frc_p %g not in [0, c]", cfg->frc_p);
+  if (cfg->no_intra_batch_reuse != 0 && cfg->no_intra_batch_reuse != 1)
+    return arckv::fail(ARCKV_EINVAL, "cache_create: no_intra_batch_reuse must be 0 or 1");
   if (cfg->ref_order != ARCKV_REF_TAIL_FIRST && cfg->ref_order != ARCKV_REF_HEAD_FIRST)
     return arckv::fail(ARCKV_EINVAL, "cache_create: unknown reference order");
   if (cfg->victim_window < 0 || cfg->victim_window > 4096)
@@ -396,7 +412,10 @@ extern "C" int32_t arckv_cache_create(const arckv_cache_cfg* cfg, arckv_cache** 
   auto* c = new (std::nothrow) arckv_cache();
   if (c == nullptr) return arckv::fail(ARCKV_ENOSPC, "cache_create: out of host memory");
   c->policy = cfg->policy;
-  c->p = cfg->policy == ARCKV_POLICY_DBL ? static_cast<double>(cfg->capacity_blocks) / 2.0 : 0.0;
+  c->p = cfg->policy == ARCKV_POLICY_DBL   ? static_cast<double>(cfg->capacity_blocks) / 2.0
+         : cfg->policy == ARCKV_POLICY_FRC ? cfg->frc_p
+                                           : 0.0;
+  c->intra_batch_reuse = cfg->no_intra_batch_reuse == 0;
   c->ref_order = cfg->ref_order;
   c->window = cfg->victim_window < 1 ? 1 : cfg->victim_window;
   c->c = cfg->capacity_blocks;
@@ -477,7 +496,7 @@ extern "C" int32_t arckv_plan_batch(arckv_cache* c, const arckv_req* reqs, int32
     const arckv_req& q = reqs[r];
     const int64_t nf = q.n_full;
     int64_t k = 0;
-    while (k < nf && c->resident(q.hashes[k])) ++k;
+    while (k < nf && c->reusable(q.hashes[k])) ++k;
     if (k * ARCKV_BLOCK_TOKENS == q.n_tokens) k -= 1;  // whole prompt cached: recompute last block
     for (int64_t i = 0; i < k; ++i) c->nodes[c->find(q.hashes[i])].pin_epoch = c->epoch;
     int32_t* row = plan->block_tables + static_cast<int64_t>(r) * plan->bt_stride;

@@ -36,7 +36,8 @@ class PrefillEngine:
     def __init__(self, num_q_heads: int, num_kv_heads: int, head_dim: int, capacity: int,
                  num_phys: int, scratch: int, policy: str = "arc", initial_order=None,
                  ref_order: str = "tail_first", device: str = "cuda", num_cus: int | None = None,
-                 pool_fill: int = -1, victim_window: int = 1):
+                 pool_fill: int = -1, victim_window: int = 1, intra_batch_reuse: bool = True,
+                 frc_p: float = 0.0):
         import torch
         self.hq, self.hkv, self.d = num_q_heads, num_kv_heads, head_dim
         self.scale = head_dim ** -0.5
@@ -47,7 +48,8 @@ class PrefillEngine:
                                  device=self.device)
         self.v_pool = torch.full((num_phys, num_kv_heads, head_dim, 16), pool_fill, dtype=torch.int16,
                                  device=self.device)
-        self.cache = BlockCache(policy, capacity, num_phys, scratch, initial_order, ref_order, victim_window)
+        self.cache = BlockCache(policy, capacity, num_phys, scratch, initial_order, ref_order, victim_window,
+                                intra_batch_reuse, frc_p)
         if num_cus is None:
             num_cus = torch.cuda.get_device_properties(self.device).multi_processor_count
         self.num_cus = int(num_cus)

@@ -13,6 +13,7 @@ native library -- once per (policy, cache size), and reports
 
 A policy may carry a victim window, ``arc@16``: length-aware eviction (Sec. 6 future work),
 the deepest of the 16 least recently used unpinned pages of the list a policy evicts from.
+``frc:0.25`` is the fixed-target policy FRC_p with p = 0.25 c (``dbl`` is ``frc:0.5``).
 
 Usage::
 
@@ -58,11 +59,13 @@ class Replay:
 
 
 def parse_policy(name: str):
-    """'arc' -> ('arc', 1); 'lru@16' -> ('lru', 16) (victim window)."""
+    """'arc' -> ('arc', 1, 0.0); 'lru@16' -> ('lru', 16, 0.0) (victim window);
+    'frc:0.25@4' -> ('frc', 4, 0.25) (p as a fraction of c)."""
     base, _, w = name.partition("@")
-    if base not in POLICIES:
+    base, _, frac = base.partition(":")
+    if base not in POLICIES + ("frc",) or (base == "frc") != bool(frac):
         raise ValueError(f"unknown policy {name!r}")
-    return base, int(w) if w else 1
+    return base, int(w) if w else 1, float(frac) if frac else 0.0
 
 
 def replay(hashes, lens, policy: str, capacity: int, scratch: int, max_batch: int = 1,
@@ -72,8 +75,9 @@ def replay(hashes, lens, policy: str, capacity: int, scratch: int, max_batch: in
     `policy` may carry a victim window (``arc@16``)."""
     lens = np.asarray(lens, dtype=np.int64)
     n = len(lens)
-    base, window = parse_policy(policy)
-    cache = BlockCache(base, capacity, capacity + scratch, scratch, initial_order, ref_order, window)
+    base, window, frac = parse_policy(policy)
+    cache = BlockCache(base, capacity, capacity + scratch, scratch, initial_order, ref_order, window,
+                       frc_p=frac * capacity)
     hit = np.zeros(n, dtype=np.int64)
     ends, t1, t2, p = [], [], [], []
     i = 0

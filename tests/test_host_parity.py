@@ -34,10 +34,11 @@ def test_hash_matches_oracle():
 class Pair:
     """Library cache and oracle planner driven in lockstep."""
 
-    def __init__(self, policy, c, nphys, scratch, order=None, ref_order="tail_first", window=1):
-        self.lib = ak.BlockCache(policy, c, nphys, scratch, order, ref_order, window)
+    def __init__(self, policy, c, nphys, scratch, order=None, ref_order="tail_first", window=1,
+                 reuse=True, frc_p=0.0):
+        self.lib = ak.BlockCache(policy, c, nphys, scratch, order, ref_order, window, reuse, frc_p)
         self.lib.set_log(1 << 20)
-        self.orc = Planner(policy, c, nphys, scratch, order, ref_order, window)
+        self.orc = Planner(policy, c, nphys, scratch, order, ref_order, window, reuse, frc_p)
         self.n_events = 0
 
     def run(self, token_lists):
@@ -78,16 +79,19 @@ class Pair:
         assert st["case_counts"] == t.case_counts
 
 
-@pytest.mark.parametrize("policy", ["arc", "lru", "dbl"])
+@pytest.mark.parametrize("policy", ["arc", "lru", "dbl", "frc"])
 @pytest.mark.parametrize("ref_order", ["tail_first", "head_first"])
-@pytest.mark.parametrize("seed,window", [(0, 1), (1, 1), (2, 1), (3, 2), (4, 7)])
-def test_random_streams_bit_exact(policy, ref_order, seed, window):
-    """window > 1: length-aware victims, the same decisions on both sides."""
+@pytest.mark.parametrize("seed,window,reuse", [(0, 1, True), (1, 1, True), (2, 1, False), (3, 2, True),
+                                               (4, 7, False)])
+def test_random_streams_bit_exact(policy, ref_order, seed, window, reuse):
+    """window > 1: length-aware victims; reuse False: no intra-batch prefix reuse; frc: a
+    fixed target p drawn per case.  The same decisions on both sides."""
     cfg = get_config("tiny")
     rng = np.random.default_rng(100 + seed)
     c, scratch = int(rng.integers(8, 40)), 8
     nphys = c + scratch + int(rng.integers(0, 5))
-    pair = Pair(policy, c, nphys, scratch, rng.permutation(nphys), ref_order, window)
+    frc_p = float(rng.integers(0, 2 * c + 1)) / 2     # multiples of 1/2 in [0, c]
+    pair = Pair(policy, c, nphys, scratch, rng.permutation(nphys), ref_order, window, reuse, frc_p)
     docs = [make_request(cfg, [(Source(KIND_DOC, d, 200), 0, 200)]).tokens for d in range(12)]
     pops = 1.0 / np.arange(1, 13) ** 1.1
     pops /= pops.sum()
@@ -183,6 +187,8 @@ def test_error_statuses_match_the_oracle():
         ak.BlockCache("arc", 10, 12, 4)              # pool too small for c + scratch
     with pytest.raises(ak.ArckvError):
         ak.BlockCache("arc", 4, 8, 2, initial_order=[0, 1, 2, 3, 4, 5, 6, 6])
+    with pytest.raises(ak.ArckvError):
+        ak.BlockCache("frc", 4, 8, 2, frc_p=4.5)      # p outside [0, c]
     for bad_window in (-1, 4097):
         with pytest.raises(ak.ArckvError) as e2:
             ak.BlockCache("lru", 4, 8, 2, victim_window=bad_window)
