@@ -1,9 +1,11 @@
 """PrefillEngine: the per-batch hot path wired over libarckv.
 
-hash blocks -> plan the batch on the host cache -> copy metadata to the device ->
-scatter the computed tokens' K/V -> prefix-cached prefill attention -> release.
+prepare (hash blocks, plan the batch on the host cache, plan the attention work, pack the
+metadata: one native call) -> copy metadata to the device -> [project Q/K/V] -> scatter the
+computed tokens' K/V -> prefix-cached prefill attention -> release.
 Every step is a libarckv call; this class owns the device buffers (PyTorch tensors used
-only as device memory) and the host cache handle.
+only as device memory) and the host cache handle.  plan() + upload() are the same first
+steps as separate calls.
 """
 
 from __future__ import annotations
@@ -66,6 +68,7 @@ class PrefillEngine:
 
     # ---- host steps ----------------------------------------------------------------------
     def plan(self, token_lists) -> BatchPlan:
+        """Hashes and the cache plan only (prepare() does these and the rest in one call)."""
         hashes = hash_blocks_batch(token_lists)
         return self.cache.plan_batch([(h, len(t)) for h, t in zip(hashes, token_lists)])
 
