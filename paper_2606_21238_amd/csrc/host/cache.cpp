@@ -212,8 +212,7 @@ struct arckv_cache {
     return n >= 0 && (nodes[n].list == ARCKV_LIST_T1 || nodes[n].list == ARCKV_LIST_T2);
   }
   // resident and, without intra-batch reuse, not born in the batch being planned
-  bool reusable(uint64_t key) const {
-    const int32_t n = find(key);
+  bool reusable_node(int32_t n) const {
     return n >= 0 && (nodes[n].list == ARCKV_LIST_T1 || nodes[n].list == ARCKV_LIST_T2) &&
            (intra_batch_reuse || nodes[n].born_epoch != epoch);
   }
@@ -252,9 +251,10 @@ struct arckv_cache {
     return ARCKV_OK;
   }
 
-  int32_t reference_arc(uint64_t x, arckv_event& ev) {
+  // hint: x's node when the caller already looked it up (a pinned prefix page), else -1
+  int32_t reference_arc(uint64_t x, int32_t hint, arckv_event& ev, int32_t& node_out) {
     const int64_t c_ = c;
-    int32_t n = find(x);
+    int32_t n = hint >= 0 ? hint : find(x);
     const int32_t where = n >= 0 ? nodes[n].list : ARCKV_LIST_NONE;
     Victim v;
     if (where == ARCKV_LIST_T1 || where == ARCKV_LIST_T2) {           // Case I
@@ -320,12 +320,13 @@ struct arckv_cache {
     ev.evicted_from = v.from;
     ev.phys_block = nodes[n].phys;
     nodes[n].pin_epoch = epoch;
+    node_out = n;
     return ARCKV_OK;
   }
 
   // ---- LRU --------------------------------------------------------------------------
-  int32_t reference_lru(uint64_t x, arckv_event& ev) {
-    int32_t n = find(x);
+  int32_t reference_lru(uint64_t x, int32_t hint, arckv_event& ev, int32_t& node_out) {
+    int32_t n = hint >= 0 ? hint : find(x);
     if (n >= 0) {
       unlink(n);
       push_mru(n, ARCKV_LIST_T1);
@@ -351,16 +352,18 @@ struct arckv_cache {
     }
     ev.phys_block = nodes[n].phys;
     nodes[n].pin_epoch = epoch;
+    node_out = n;
     return ARCKV_OK;
   }
 
-  int32_t reference(uint64_t x, int32_t depth, int32_t& phys_out) {
+  int32_t reference(uint64_t x, int32_t hint, int32_t depth, int32_t& phys_out) {
     arckv_event ev{};
     ev.key = x;
-    const int32_t st =
-        policy == ARCKV_POLICY_LRU ? reference_lru(x, ev) : reference_arc(x, ev);
+    int32_t n = -1;
+    const int32_t st = policy == ARCKV_POLICY_LRU ? reference_lru(x, hint, ev, n)
+                                                  : reference_arc(x, hint, ev, n);
     if (st != ARCKV_OK) return st;
-    nodes[find(x)].depth = depth;
+    nodes[n].depth = depth;
     ev.p_after = policy == ARCKV_POLICY_LRU ? 0.0 : p;
     phys_out = ev.phys_block;
     case_counts[ev.kase] += 1;
@@ -496,14 +499,21 @@ extern "C" int32_t arckv_plan_batch(arckv_cache* c, const arckv_req* reqs, int32
     const arckv_req& q = reqs[r];
     const int64_t nf = q.n_full;
     int64_t k = 0;
-    while (k < nf && c->reusable(q.hashes[k])) ++k;
+    // the prefix's nodes, looked up once: pinned below and handed to their references
+    thread_local std::vector<int32_t> prefix_node;
+    prefix_node.resize(static_cast<size_t>(nf > 0 ? nf : 1));
+    while (k < nf) {
+      const int32_t n = c->find(q.hashes[k]);
+      if (!c->reusable_node(n)) break;
+      prefix_node[k++] = n;
+    }
     if (k * ARCKV_BLOCK_TOKENS == q.n_tokens) k -= 1;  // whole prompt cached: recompute last block
-    for (int64_t i = 0; i < k; ++i) c->nodes[c->find(q.hashes[i])].pin_epoch = c->epoch;
+    for (int64_t i = 0; i < k; ++i) c->nodes[prefix_node[i]].pin_epoch = c->epoch;
     int32_t* row = plan->block_tables + static_cast<int64_t>(r) * plan->bt_stride;
     for (int64_t i = 0; i < nf; ++i) {
       const int64_t b = c->ref_order == ARCKV_REF_TAIL_FIRST ? nf - 1 - i : i;
       int32_t phys = -1;
-      const int32_t st = c->reference(q.hashes[b], static_cast<int32_t>(b), phys);
+      const int32_t st = c->reference(q.hashes[b], b < k ? prefix_node[b] : -1, static_cast<int32_t>(b), phys);
       if (st != ARCKV_OK) return st;  // unreachable with the capacity check above
       row[b] = phys;
     }
