@@ -19,8 +19,10 @@
  *    exception crosses this boundary.
  *  - Host objects are opaque and owned by the library (create/destroy pairs).
  *  - Device memory is always owned by the caller.  The library never
- *    allocates or frees device memory; device pointers are borrowed until the
- *    work queued on the given stream has completed.
+ *    allocates or frees device memory itself; device pointers are borrowed
+ *    until the work queued on the given stream has completed.  (The one
+ *    library it calls, rocBLAS in arckv_qkv_rope, keeps a per-device handle
+ *    and manages its own workspace.)
  *  - Device calls enqueue asynchronously on the caller's HIP stream (passed as
  *    void*, NULL = the null stream).  Argument checks are synchronous; a launch
  *    failure returns ARCKV_EDEVICE.  Nothing synchronises implicitly.
