@@ -238,7 +238,10 @@ int64_t arckv_pool_bytes(int64_t num_blocks, int32_t num_kv_heads, int32_t head_
 /* pool[slot[t]] <- (k_new[t], v_new[t]) for t < n_tokens, as an exact bit copy.
  * k_pool, v_pool: device, layout V1, num_blocks blocks.  k_new, v_new: device bf16
  * [n_tokens][num_kv_heads][head_dim].  slot_mapping: device int32 [n_tokens]; a slot
- * outside [0, 16 num_blocks) is skipped.  head_dim in {64, 128}.  Enqueued on stream. */
+ * outside [0, 16 num_blocks) is skipped.  The two pools and the two row arrays must be
+ * 16-byte aligned (EINVAL).  Two tokens with the same slot: one of their rows is written
+ * (callers give equal bytes, as for a block recomputed twice in one batch).  head_dim in
+ * {64, 128} (else EUNSUPPORTED).  Enqueued on stream. */
 int32_t arckv_kv_scatter(void* k_pool, void* v_pool, const void* k_new, const void* v_new,
                          const int32_t* slot_mapping, int64_t n_tokens, int64_t num_blocks,
                          int32_t num_kv_heads, int32_t head_dim, void* stream);

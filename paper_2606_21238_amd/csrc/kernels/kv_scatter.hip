@@ -6,10 +6,12 @@
 // [blocks][kv_heads][D][16] (dim-major, so that the attention kernel's P.V contraction reads
 // 8 consecutive tokens of one dimension as one 16-byte operand).
 //
-// One work-group handles 64 tokens of one KV head.  K rows are copied as 16-byte chunks
-// (consecutive lanes, consecutive chunks of one row).  V rows are staged through LDS and
-// written transposed: the 64 lanes of a wave take 64 consecutive tokens of one dimension, so
-// tokens of one block land on consecutive 2-byte addresses.  Bytes are copied, never
+// A work-group handles 64 tokens of one KV head and DPW of its head dimensions (16 for small
+// batches, so that a decode step still spreads over many work-groups; 64 otherwise, whole
+// 128-byte row segments).  K rows are copied as 16-byte chunks.  V rows are staged through
+// LDS and written transposed: where 8 consecutive tokens sit in 8 consecutive slots of one
+// block (8-aligned, the common case of a prefill), one 16-byte store writes them for one
+// dimension; otherwise each token's value is a 2-byte store.  Bytes are copied, never
 // converted: the result is bit-exact.  Slots outside the pool are skipped.
 #include <hip/hip_runtime.h>
 
@@ -19,53 +21,78 @@ namespace {
 
 constexpr int kTok = 64;
 constexpr int kThreads = 256;
+constexpr int kGroups = kTok / 8;      // 8-token groups of a work-group
 
-template <int D>
+template <int D, int DPW>
 __global__ __launch_bounds__(kThreads) void kv_scatter_kernel(
     uint16_t* __restrict__ k_pool, uint16_t* __restrict__ v_pool,
     const uint16_t* __restrict__ k_new, const uint16_t* __restrict__ v_new,
     const int32_t* __restrict__ slots, int64_t n_tokens, int64_t n_slots, int hkv) {
-  constexpr int CH = D / 8;            // 16-byte chunks per row
-  constexpr int VROW = D + 2;          // padded LDS row (in u16) so column reads spread over banks
+  constexpr int CH = DPW / 8;          // 16-byte chunks of a row slice
+  constexpr int VROW = DPW + 2;        // padded LDS row (u16): column reads spread over banks
   __shared__ uint32_t sv32[kTok * VROW / 2];
   __shared__ int32_t sslot[kTok];
+  __shared__ int32_t gbase[kGroups];   // first slot of an 8-token run, or -1
   uint16_t* sv = reinterpret_cast<uint16_t*>(sv32);
-
   const int h = blockIdx.y;
+  const int d0 = blockIdx.z * DPW;     // first dimension of the slice
   const int64_t t0 = static_cast<int64_t>(blockIdx.x) * kTok;
   const int tid = threadIdx.x;
   if (tid < kTok) {
     const int64_t t = t0 + tid;
-    int32_t s = t < n_tokens ? slots[t] : -1;
+    const int32_t s = t < n_tokens ? slots[t] : -1;
     sslot[tid] = (s >= 0 && s < n_slots) ? s : -1;
   }
   __syncthreads();
-
+  if (tid < kGroups) {
+    const int32_t s = sslot[8 * tid];
+    bool run = s >= 0 && (s & 7) == 0;
+    for (int j = 1; j < 8 && run; ++j) run = sslot[8 * tid + j] == s + j;
+    gbase[tid] = run ? s : -1;
+  }
   // K: direct 16-byte copies; V: into LDS (row = token, padded)
   for (int c = tid; c < kTok * CH; c += kThreads) {
     const int tl = c / CH, ch = c % CH;
     const int64_t t = t0 + tl;
     if (t >= n_tokens) continue;
-    const int64_t src = (t * hkv + h) * D + ch * 8;
+    const int64_t src = (t * hkv + h) * D + d0 + ch * 8;
     const int32_t s = sslot[tl];
     if (s >= 0) {
       const uint4 kv = *reinterpret_cast<const uint4*>(k_new + src);
       const int64_t blk = s >> 4;
-      *reinterpret_cast<uint4*>(k_pool + ((blk * hkv + h) * 16 + (s & 15)) * D + ch * 8) = kv;
+      *reinterpret_cast<uint4*>(k_pool + ((blk * hkv + h) * 16 + (s & 15)) * D + d0 + ch * 8) = kv;
     }
     const uint4 vv = *reinterpret_cast<const uint4*>(v_new + src);
     uint32_t* dst = sv32 + (tl * VROW + ch * 8) / 2;  // VROW and ch*8 are even: 4-byte aligned
     dst[0] = vv.x; dst[1] = vv.y; dst[2] = vv.z; dst[3] = vv.w;
   }
   __syncthreads();
-
-  // V: lane = token, loop over dimensions
-  const int tl = tid & (kTok - 1);
-  const int s = sslot[tl];
-  if (s < 0 || t0 + tl >= n_tokens) return;
-  const int64_t base = ((static_cast<int64_t>(s >> 4) * hkv + h) * D) * 16 + (s & 15);
-  for (int d = tid >> 6; d < D; d += kThreads / kTok)
-    v_pool[base + static_cast<int64_t>(d) * 16] = sv[tl * VROW + d];
+  // V: (8-token group, dimension) per thread.  Lane pairs take the two 8-token halves of a
+  // block and consecutive pairs consecutive dimensions, so that a wave's 16-byte stores cover
+  // one contiguous stretch of a block's dim-major V (32 bytes per dimension).
+  for (int e = tid; e < kGroups * DPW; e += kThreads) {
+    const int half = e & 1, rest = e >> 1;
+    const int g = 2 * (rest / DPW) + half, dl = rest % DPW, d = d0 + dl;
+    const int32_t sb = gbase[g];
+    if (sb >= 0) {
+      uint16_t v8[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) v8[j] = sv[(8 * g + j) * VROW + dl];
+      uint4 w;
+      w.x = v8[0] | (static_cast<uint32_t>(v8[1]) << 16);
+      w.y = v8[2] | (static_cast<uint32_t>(v8[3]) << 16);
+      w.z = v8[4] | (static_cast<uint32_t>(v8[5]) << 16);
+      w.w = v8[6] | (static_cast<uint32_t>(v8[7]) << 16);
+      *reinterpret_cast<uint4*>(v_pool + ((static_cast<int64_t>(sb >> 4) * hkv + h) * D + d) * 16 + (sb & 15)) = w;
+    } else {
+      for (int j = 0; j < 8; ++j) {
+        const int tl = 8 * g + j;
+        const int32_t s = sslot[tl];
+        if (s < 0 || t0 + tl >= n_tokens) continue;
+        v_pool[((static_cast<int64_t>(s >> 4) * hkv + h) * D + d) * 16 + (s & 15)] = sv[tl * VROW + dl];
+      }
+    }
+  }
 }
 
 }  // namespace
@@ -82,19 +109,29 @@ extern "C" int32_t arckv_kv_scatter(void* k_pool, void* v_pool, const void* k_ne
   if (k_pool == nullptr || v_pool == nullptr || k_new == nullptr || v_new == nullptr ||
       slot_mapping == nullptr)
     return arckv::fail(ARCKV_EINVAL, "kv_scatter: NULL pointer");
-  const dim3 grid(static_cast<unsigned>((n_tokens + kTok - 1) / kTok), num_kv_heads);
+  for (const void* p : {static_cast<const void*>(k_pool), static_cast<const void*>(v_pool), k_new, v_new})
+    if (reinterpret_cast<uintptr_t>(p) % 16 != 0)
+      return arckv::fail(ARCKV_EINVAL, "kv_scatter: pools and new rows must be 16-byte aligned");
+  // small batches (decode) split the head dimension finely to spread over more work-groups
+  const bool small = n_tokens <= 1024;
+  const int dpw = small ? 16 : 64;
+  const dim3 grid(static_cast<unsigned>((n_tokens + kTok - 1) / kTok), num_kv_heads,
+                  static_cast<unsigned>(head_dim / dpw));
   auto* st = static_cast<hipStream_t>(stream);
   auto* kp = static_cast<uint16_t*>(k_pool);
   auto* vp = static_cast<uint16_t*>(v_pool);
   auto* kn = static_cast<const uint16_t*>(k_new);
   auto* vn = static_cast<const uint16_t*>(v_new);
   const int64_t n_slots = num_blocks * 16;
-  if (head_dim == 64)
-    hipLaunchKernelGGL(kv_scatter_kernel<64>, grid, dim3(kThreads), 0, st, kp, vp, kn, vn,
-                       slot_mapping, n_tokens, n_slots, num_kv_heads);
-  else
-    hipLaunchKernelGGL(kv_scatter_kernel<128>, grid, dim3(kThreads), 0, st, kp, vp, kn, vn,
-                       slot_mapping, n_tokens, n_slots, num_kv_heads);
+#define ARCKV_SCATTER(DD, PW)                                                               \
+  hipLaunchKernelGGL((kv_scatter_kernel<DD, PW>), grid, dim3(kThreads), 0, st, kp, vp, kn, vn, \
+                     slot_mapping, n_tokens, n_slots, num_kv_heads)
+  if (head_dim == 64) {
+    if (small) ARCKV_SCATTER(64, 16); else ARCKV_SCATTER(64, 64);
+  } else {
+    if (small) ARCKV_SCATTER(128, 16); else ARCKV_SCATTER(128, 64);
+  }
+#undef ARCKV_SCATTER
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return arckv::fail(ARCKV_EDEVICE, "kv_scatter: %s", hipGetErrorString(e));
   return ARCKV_OK;

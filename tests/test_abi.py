@@ -49,6 +49,10 @@ def test_device_calls_validate_arguments_without_touching_a_device():
     assert b"tile_cols" in L.arckv_last_error()
     # nothing to do is a no-op
     assert L.arckv_kv_scatter(None, None, None, None, None, 0, 4, 2, 64, None) == _lib.OK
+    # misaligned pools or rows are refused before any launch (the addresses are never read)
+    a, m = 0x20000, 0x20008
+    assert L.arckv_kv_scatter(a, m, a, a, a, 4, 4, 2, 64, None) == _lib.EINVAL
+    assert b"aligned" in L.arckv_last_error()
 
 
 def test_missing_library_fails_loudly(tmp_path):

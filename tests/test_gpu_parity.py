@@ -66,6 +66,32 @@ def test_scatter_bit_exact(d, hkv, n):
     assert np.array_equal(bits(eng_v), vp)
 
 
+@pytest.mark.parametrize("d,hkv,n,start", [(64, 2, 1000, 0), (128, 8, 1000, 5), (128, 8, 3000, 3),
+                                           (64, 4, 2500, 8), (128, 2, 8, 0), (128, 8, 1025, 0)])
+def test_scatter_block_runs_bit_exact(d, hkv, n, start):
+    """Prefill-shaped slots (requests in consecutive slots of their blocks, starting at
+    `start` inside the first block), with a few skipped slots: 8-token runs take the 16-byte
+    stores, broken runs the 2-byte ones; both on the small- and the large-batch grid."""
+    print_case(f"scatter runs d={d} hkv={hkv} n={n} start={start}")
+    rng = np.random.default_rng(n + 7 * d + start)
+    nblk = (n + start + 15) // 16 + 9
+    table = rng.permutation(nblk)
+    j = np.arange(n) + start
+    slots = (table[j // 16] * 16 + j % 16).astype(np.int32)
+    slots[rng.integers(0, n, max(1, n // 300))] = -1
+    k_new = randn_bf16((n, hkv, d), 3 + n)
+    v_new = randn_bf16((n, hkv, d), 4 + n)
+    eng_k = torch.full((nblk, hkv, 16, d), -1, dtype=torch.int16, device=DEV)
+    eng_v = torch.full((nblk, hkv, d, 16), -1, dtype=torch.int16, device=DEV)
+    ak.kv_scatter(eng_k, eng_v, k_new, v_new, torch.from_numpy(slots).to(DEV))
+    torch.cuda.synchronize()
+    kp, vp = okv.new_pool(nblk, hkv, d)
+    keep = slots >= 0
+    okv.scatter(kp, vp, bits(k_new)[keep], bits(v_new)[keep], slots[keep])
+    assert np.array_equal(bits(eng_k), kp)
+    assert np.array_equal(bits(eng_v), vp)
+
+
 # ------------------------------------------------------------------------------------------
 # attention on directly built batches (random placement, edge lengths)
 # ------------------------------------------------------------------------------------------
