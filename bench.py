@@ -21,8 +21,9 @@ one-off documents, cache 20 % of the recurring documents; the first 2,000 reques
 next `--steps` batches are timed, and the host replays the whole stream for ARC and LRU hit
 rates).
 
-One step = one batch through the whole path: block hashing -> ARC plan -> metadata H2D ->
-KV scatter -> prefill attention -> release.  Each batch's computed-token Q/K/V are staged in
+One step = one batch through the whole path: one native call for block hashing, the ARC
+plan and the attention work plan -> metadata H2D -> [Q/K/V projection, docqa14b] -> KV
+scatter -> prefill attention (+ split combine) -> release.  Each batch's computed-token Q/K/V are staged in
 HBM before the timed region (token ids stay on the host).  Printed: one JSON line with the
 algorithmic attention TFLOP/s over the whole step time (value), suffix tokens/s, the roofline
 of the attention kernel measured with HIP events on its stream, and the CPU oracle timed on a
