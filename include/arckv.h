@@ -302,6 +302,16 @@ int32_t arckv_prepare_batch(arckv_cache* cache, const int32_t* const* tokens,
                             int32_t num_cus, int32_t* packed, int64_t packed_cap,
                             int32_t* prefix_lens, int32_t* hit_blocks, arckv_batch* out);
 
+/* arckv_prepare_batch for callers that keep their requests' chained hashes (a serving loop
+ * holding a running request's block hashes): hashes[r] holds n_tokens[r] / 16 identities
+ * (as arckv_hash_blocks gives; may be NULL when there are none); no hashing is done.  Same
+ * outputs and errors as arckv_prepare_batch. */
+int32_t arckv_prepare_batch_hashed(arckv_cache* cache, const uint64_t* const* hashes,
+                                   const int64_t* n_tokens, int32_t n_reqs,
+                                   int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                                   int32_t num_cus, int32_t* packed, int64_t packed_cap,
+                                   int32_t* prefix_lens, int32_t* hit_blocks, arckv_batch* out);
+
 /* Runs attention for one planned batch.
  * k_pool, v_pool: device, layout V1 (num_blocks blocks).  q: device bf16
  * [n_q][num_q_heads][head_dim], rows ordered by cu_q.  out: device bf16, same shape.

@@ -146,25 +146,35 @@ class BlockCache:
         return BatchPlan(bt, cu, sl, pl, hb, slots[: pc.n_slots].copy(), pc.max_q_len, pc.max_seq_len)
 
     def prepare_native(self, token_lists, num_q_heads: int, num_kv_heads: int, head_dim: int,
-                       num_cus: int, packed: np.ndarray, root: int = 0):
-        """One call of arckv_prepare_batch into `packed` (contiguous writable int32).  Returns
-        (status, info dict, prefix_lens, hit_blocks) without raising; on ENOSPC info["n_packed"]
-        is the capacity needed (the cache is then unchanged)."""
-        toks = [t if (t.dtype == np.int32 and t.flags.c_contiguous) else np.ascontiguousarray(t, dtype=np.int32)
-                for t in token_lists]
-        n = len(toks)
-        addrs = np.fromiter((t.__array_interface__["data"][0] for t in toks), dtype=np.uint64, count=n)
-        lens = np.fromiter((t.shape[0] for t in toks), dtype=np.int64, count=n)
+                       num_cus: int, packed: np.ndarray, root: int = 0, hashes=None, n_tokens=None):
+        """One call of arckv_prepare_batch into `packed` (contiguous writable int32), or, with
+        `hashes` (uint64 arrays) and `n_tokens`, of arckv_prepare_batch_hashed (token_lists is
+        then unused).  Returns (status, info dict, prefix_lens, hit_blocks) without raising; on
+        ENOSPC info["n_packed"] is the capacity needed (the cache is then unchanged)."""
+        if hashes is None:
+            seqs = [t if (t.dtype == np.int32 and t.flags.c_contiguous) else np.ascontiguousarray(t, dtype=np.int32)
+                    for t in token_lists]
+            lens = np.fromiter((t.shape[0] for t in seqs), dtype=np.int64, count=len(seqs))
+        else:
+            seqs = [h if (h.dtype == np.uint64 and h.flags.c_contiguous) else np.ascontiguousarray(h, dtype=np.uint64)
+                    for h in hashes]
+            lens = np.ascontiguousarray(n_tokens, dtype=np.int64)
+        n = len(seqs)
+        addrs = np.fromiter((t.__array_interface__["data"][0] for t in seqs), dtype=np.uint64, count=n)
         pl = np.empty(max(n, 1), dtype=np.int32)
         hb = np.empty(max(n, 1), dtype=np.int32)
         info = _lib.BatchC()
         cap = 0 if packed is None else packed.size
-        st = lib().arckv_prepare_batch(self._h, addrs.__array_interface__["data"][0],
-                                       lens.__array_interface__["data"][0], n, root, num_q_heads,
-                                       num_kv_heads, head_dim, num_cus,
-                                       None if packed is None else packed.__array_interface__["data"][0],
-                                       cap, pl.__array_interface__["data"][0],
-                                       hb.__array_interface__["data"][0], C.byref(info))
+        pk = None if packed is None else packed.__array_interface__["data"][0]
+        a, ln = addrs.__array_interface__["data"][0], lens.__array_interface__["data"][0]
+        if hashes is None:
+            st = lib().arckv_prepare_batch(self._h, a, ln, n, root, num_q_heads, num_kv_heads, head_dim,
+                                           num_cus, pk, cap, pl.__array_interface__["data"][0],
+                                           hb.__array_interface__["data"][0], C.byref(info))
+        else:
+            st = lib().arckv_prepare_batch_hashed(self._h, a, ln, n, num_q_heads, num_kv_heads, head_dim,
+                                                  num_cus, pk, cap, pl.__array_interface__["data"][0],
+                                                  hb.__array_interface__["data"][0], C.byref(info))
         d = {k: getattr(info, k) for k, _ in _lib.BatchC._fields_}
         return st, d, pl[:n], hb[:n]
 

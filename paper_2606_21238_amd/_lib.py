@@ -74,6 +74,8 @@ _SIGS = {
                                    P_i64, P_i32]),
     "arckv_prepare_batch": (i32, [vp, vp, vp, i32, u64, i32, i32, i32, i32, vp, i64, vp, vp,
                                   C.POINTER(BatchC)]),
+    "arckv_prepare_batch_hashed": (i32, [vp, vp, vp, i32, i32, i32, i32, i32, vp, i64, vp, vp,
+                                         C.POINTER(BatchC)]),
     "arckv_prefill_attention": (i32, [vp, vp, vp, vp, vp, i32, vp, vp, i32, i64, i64, vp, i64, i64,
                                       i32, i32, i32, i32, f32, vp, i64, vp]),
     "arckv_prefill_attention_timed": (i32, [vp, vp, vp, vp, vp, i32, vp, vp, i32, i64, i64, vp, i64,

@@ -1,9 +1,9 @@
-// One batch's host preparation in one call: chained block hashes of every prompt, the cache
-// plan (hits, evictions, placement) and the attention work plan, written straight into one
-// int32 buffer laid out the way the device steps read it, so that the caller's only remaining
-// work is a single host-to-device copy.  Each stage is the library's own entry point
-// (arckv_hash_blocks_batch, arckv_plan_batch, arckv_attention_plan); the results are
-// identical to calling them one by one.
+// One batch's host preparation in one call: chained block hashes of every prompt (or the
+// caller's own, for requests whose hashes it keeps), the cache plan (hits, evictions,
+// placement) and the attention work plan, written straight into one int32 buffer laid out the
+// way the device steps read it, so that the caller's only remaining work is a single
+// host-to-device copy.  Each stage is the library's own entry point (arckv_hash_blocks_batch,
+// arckv_plan_batch, arckv_attention_plan); the results are identical to calling them one by one.
 #include <algorithm>
 #include <vector>
 
@@ -24,27 +24,17 @@ int64_t work_bound(const int64_t* n_tokens, int32_t n_reqs, int32_t G, int32_t h
   return kXcds * (tiles + num_cus) + tiles;
 }
 
-}  // namespace
-
-extern "C" int32_t arckv_prepare_batch(arckv_cache* cache, const int32_t* const* tokens,
-                                       const int64_t* n_tokens, int32_t n_reqs, uint64_t root,
-                                       int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
-                                       int32_t num_cus, int32_t* packed, int64_t packed_cap,
-                                       int32_t* prefix_lens, int32_t* hit_blocks,
-                                       arckv_batch* out) {
-  if (cache == nullptr || out == nullptr || n_reqs < 1 || tokens == nullptr || n_tokens == nullptr ||
-      prefix_lens == nullptr || hit_blocks == nullptr || num_cus < 1 || num_kv_heads < 1 ||
-      num_q_heads < 1 || num_q_heads % num_kv_heads != 0)
-    return arckv::fail(ARCKV_EINVAL, "prepare_batch: bad arguments");
-  *out = arckv_batch{};
+// The common part: requests given as (hashes, n_tokens); `hashes[r]` holds n_tokens[r] / 16
+// chained identities.
+int32_t prepare_planned(arckv_cache* cache, const uint64_t* const* hashes, const int64_t* n_tokens,
+                        int32_t n_reqs, int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                        int32_t num_cus, int32_t* packed, int64_t packed_cap, int32_t* prefix_lens,
+                        int32_t* hit_blocks, arckv_batch* out) {
   const int32_t G = num_q_heads / num_kv_heads;
-  int64_t stride = 1, total_tokens = 0, total_blocks = 0;
+  int64_t stride = 1, total_tokens = 0;
   for (int32_t r = 0; r < n_reqs; ++r) {
-    if (n_tokens[r] < 1 || n_tokens[r] > INT32_MAX / 2 || tokens[r] == nullptr)
-      return arckv::fail(ARCKV_EINVAL, "prepare_batch: request %d", r);
     stride = std::max<int64_t>(stride, (n_tokens[r] + ARCKV_BLOCK_TOKENS - 1) / ARCKV_BLOCK_TOKENS);
     total_tokens += n_tokens[r];
-    total_blocks += n_tokens[r] / ARCKV_BLOCK_TOKENS;
   }
   // layout: block tables | cu_q | seq_lens | slots (at most every token) | work items
   const int64_t fixed = static_cast<int64_t>(n_reqs) * stride + 2 * static_cast<int64_t>(n_reqs) + 1;
@@ -54,18 +44,10 @@ extern "C" int32_t arckv_prepare_batch(arckv_cache* cache, const int32_t* const*
   if (packed == nullptr || packed_cap < bound)
     return arckv::fail(ARCKV_ENOSPC, "prepare_batch: packed buffer %lld ints, need up to %lld",
                        (long long)packed_cap, (long long)bound);
-
-  thread_local std::vector<uint64_t> hashes;
-  thread_local std::vector<int64_t> offsets;
   thread_local std::vector<arckv_req> reqs;
-  hashes.resize(static_cast<size_t>(std::max<int64_t>(total_blocks, 1)));
-  offsets.resize(static_cast<size_t>(n_reqs) + 1);
-  int32_t st = arckv_hash_blocks_batch(tokens, n_tokens, n_reqs, root, hashes.data(),
-                                       static_cast<int64_t>(hashes.size()), offsets.data());
-  if (st != ARCKV_OK) return st;
   reqs.resize(static_cast<size_t>(n_reqs));
   for (int32_t r = 0; r < n_reqs; ++r)
-    reqs[r] = arckv_req{hashes.data() + offsets[r], offsets[r + 1] - offsets[r], n_tokens[r]};
+    reqs[r] = arckv_req{hashes[r], n_tokens[r] / ARCKV_BLOCK_TOKENS, n_tokens[r]};
 
   out->n_reqs = n_reqs;
   out->bt_stride = static_cast<int32_t>(stride);
@@ -82,7 +64,7 @@ extern "C" int32_t arckv_prepare_batch(arckv_cache* cache, const int32_t* const*
   plan.hit_blocks = hit_blocks;
   plan.slot_mapping = packed + out->off_slots;
   plan.slot_cap = total_tokens;
-  st = arckv_plan_batch(cache, reqs.data(), n_reqs, &plan);
+  int32_t st = arckv_plan_batch(cache, reqs.data(), n_reqs, &plan);
   if (st != ARCKV_OK) return st;  // the cache is unchanged on every failure of the plan
   out->n_slots = plan.n_slots;
   out->max_q_len = plan.max_q_len;
@@ -106,4 +88,64 @@ extern "C" int32_t arckv_prepare_batch(arckv_cache* cache, const int32_t* const*
   out->tile_cols = tile_cols;
   out->n_packed = out->off_work + (n_work + n_combine) * ARCKV_WORK_INTS;
   return ARCKV_OK;
+}
+
+int32_t check_args(arckv_cache* cache, const void* seqs, const int64_t* n_tokens, int32_t n_reqs,
+                   int32_t num_q_heads, int32_t num_kv_heads, int32_t num_cus, const int32_t* prefix_lens,
+                   const int32_t* hit_blocks, arckv_batch* out) {
+  if (cache == nullptr || out == nullptr || n_reqs < 1 || seqs == nullptr || n_tokens == nullptr ||
+      prefix_lens == nullptr || hit_blocks == nullptr || num_cus < 1 || num_kv_heads < 1 ||
+      num_q_heads < 1 || num_q_heads % num_kv_heads != 0)
+    return arckv::fail(ARCKV_EINVAL, "prepare_batch: bad arguments");
+  for (int32_t r = 0; r < n_reqs; ++r)
+    if (n_tokens[r] < 1 || n_tokens[r] > INT32_MAX / 2)
+      return arckv::fail(ARCKV_EINVAL, "prepare_batch: request %d has %lld tokens", r, (long long)n_tokens[r]);
+  *out = arckv_batch{};
+  return ARCKV_OK;
+}
+
+}  // namespace
+
+extern "C" int32_t arckv_prepare_batch(arckv_cache* cache, const int32_t* const* tokens,
+                                       const int64_t* n_tokens, int32_t n_reqs, uint64_t root,
+                                       int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                                       int32_t num_cus, int32_t* packed, int64_t packed_cap,
+                                       int32_t* prefix_lens, int32_t* hit_blocks,
+                                       arckv_batch* out) {
+  int32_t st = check_args(cache, tokens, n_tokens, n_reqs, num_q_heads, num_kv_heads, num_cus,
+                          prefix_lens, hit_blocks, out);
+  if (st != ARCKV_OK) return st;
+  int64_t total_blocks = 0;
+  for (int32_t r = 0; r < n_reqs; ++r) {
+    if (tokens[r] == nullptr) return arckv::fail(ARCKV_EINVAL, "prepare_batch: request %d", r);
+    total_blocks += n_tokens[r] / ARCKV_BLOCK_TOKENS;
+  }
+  thread_local std::vector<uint64_t> hashes;
+  thread_local std::vector<int64_t> offsets;
+  thread_local std::vector<const uint64_t*> rows;
+  hashes.resize(static_cast<size_t>(std::max<int64_t>(total_blocks, 1)));
+  offsets.resize(static_cast<size_t>(n_reqs) + 1);
+  st = arckv_hash_blocks_batch(tokens, n_tokens, n_reqs, root, hashes.data(),
+                               static_cast<int64_t>(hashes.size()), offsets.data());
+  if (st != ARCKV_OK) return st;
+  rows.resize(static_cast<size_t>(n_reqs));
+  for (int32_t r = 0; r < n_reqs; ++r) rows[r] = hashes.data() + offsets[r];
+  return prepare_planned(cache, rows.data(), n_tokens, n_reqs, num_q_heads, num_kv_heads, head_dim,
+                         num_cus, packed, packed_cap, prefix_lens, hit_blocks, out);
+}
+
+extern "C" int32_t arckv_prepare_batch_hashed(arckv_cache* cache, const uint64_t* const* hashes,
+                                              const int64_t* n_tokens, int32_t n_reqs,
+                                              int32_t num_q_heads, int32_t num_kv_heads,
+                                              int32_t head_dim, int32_t num_cus, int32_t* packed,
+                                              int64_t packed_cap, int32_t* prefix_lens,
+                                              int32_t* hit_blocks, arckv_batch* out) {
+  int32_t st = check_args(cache, hashes, n_tokens, n_reqs, num_q_heads, num_kv_heads, num_cus,
+                          prefix_lens, hit_blocks, out);
+  if (st != ARCKV_OK) return st;
+  for (int32_t r = 0; r < n_reqs; ++r)
+    if (n_tokens[r] >= ARCKV_BLOCK_TOKENS && hashes[r] == nullptr)
+      return arckv::fail(ARCKV_EINVAL, "prepare_batch_hashed: request %d has no hashes", r);
+  return prepare_planned(cache, hashes, n_tokens, n_reqs, num_q_heads, num_kv_heads, head_dim,
+                         num_cus, packed, packed_cap, prefix_lens, hit_blocks, out);
 }

@@ -75,10 +75,11 @@ class PrefillEngine:
     def release(self):
         self.cache.release_batch()
 
-    def prepare(self, token_lists, stream=None) -> DeviceBatch:
+    def prepare(self, token_lists, stream=None, hashes=None, n_tokens=None) -> DeviceBatch:
         """plan() + upload() in one native call (arckv_prepare_batch): hashes, the cache plan
         and the attention work plan are written straight into the next pinned staging buffer of
-        the ring, then one asynchronous copy moves them to the device."""
+        the ring, then one asynchronous copy moves them to the device.  A caller that keeps its
+        requests' block hashes passes `hashes` and `n_tokens` instead of token lists."""
         import torch
         t = self._turn
         self._turn = (t + 1) % self._ring
@@ -86,7 +87,8 @@ class PrefillEngine:
             self._stage_ev[t].synchronize()          # the copy that last read this buffer is done
         while True:
             host = None if self._stage[t] is None else self._stage[t].numpy()
-            st, d, pl, hb = self.cache.prepare_native(token_lists, self.hq, self.hkv, self.d, self.num_cus, host)
+            st, d, pl, hb = self.cache.prepare_native(token_lists, self.hq, self.hkv, self.d, self.num_cus, host,
+                                                      hashes=hashes, n_tokens=n_tokens)
             if st == _lib.ENOSPC and (host is None or d["n_packed"] > host.size):
                 cap = max(d["n_packed"], 1 << 16) * 2
                 self._stage[t] = torch.empty(cap, dtype=torch.int32, pin_memory=True)

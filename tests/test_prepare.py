@@ -113,3 +113,28 @@ def test_packed_bound_covers_every_possible_work_plan():
         stride = int(max((lens + 15) // 16))
         used = n * stride + 2 * n + 1 + int(S.sum()) + ak.WORK_INTS * (ap.n_work + ap.n_combine)
         assert used <= bound, (used, bound, n, num_cus)
+
+
+def test_prepare_from_kept_hashes_equals_prepare_from_tokens():
+    rng = np.random.default_rng(12)
+    a = ak.BlockCache("arc", 200, 240, 16)
+    b = ak.BlockCache("arc", 200, 240, 16)
+    a.set_log(1 << 16)
+    b.set_log(1 << 16)
+    base = [rng.integers(0, 128256, int(n)).astype(np.int32) for n in (300, 700, 31, 16)]
+    kept = [ak.hash_blocks(t) for t in base]
+    packed = np.empty(1 << 16, dtype=np.int32)
+    for step in range(30):
+        pick = [int(x) for x in rng.choice(4, int(rng.integers(1, 4)), replace=False)]
+        toks = [base[i] for i in pick]
+        pa = a.prepare_batch(toks, 32, 8, 128, 256, packed)
+        pb = np.empty(1 << 16, dtype=np.int32)
+        st, d, pl, hb = b.prepare_native(None, 32, 8, 128, 256, pb,
+                                         hashes=[kept[i] for i in pick], n_tokens=[len(t) for t in toks])
+        assert st == _lib.OK
+        assert d == pa.info
+        assert np.array_equal(pb[:d["n_packed"]], pa.packed[:d["n_packed"]])
+        assert np.array_equal(pl, pa.plan.prefix_lens) and np.array_equal(hb, pa.plan.hit_blocks)
+        a.release_batch()
+        b.release_batch()
+    assert a.log() == b.log()
