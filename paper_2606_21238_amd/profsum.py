@@ -3,6 +3,7 @@
     python -m paper_2606_21238_amd.profsum <rocprofv3 -d directory> [--match REGEX]
     python -m paper_2606_21238_amd.profsum <dir> --match REGEX --last K     # timed dispatches
     python -m paper_2606_21238_amd.profsum --traffic-json OUT ...           # see the end of file
+    python -m paper_2606_21238_amd.profsum <dir> --match REGEX --counters-last K   # SQ counters
 
 Kernel stats: calls, total and average duration per kernel.  Counter collections: per
 kernel and counter, the number of dispatches and the mean value per dispatch.
@@ -111,6 +112,37 @@ def last_counter(directory: str, match: str, counter: str, last: int) -> float:
     return sum(per[d] for d in tail) / max(1, len(tail))
 
 
+def counter_names(directory: str, match: str) -> list:
+    names = []
+    for r in _dispatches(directory, "counter_collection"):
+        c = _col(r, "Counter_Name", "CounterName")
+        if re.search(match, _col(r, "Kernel_Name", "KernelName")) and c not in names:
+            names.append(c)
+    return names
+
+
+def counters_last(directory: str, match: str, last: int, xcds: int = 8, simds: int = 1024) -> str:
+    """Mean per dispatch of every counter of the kernels matching `match` over their last
+    `last` dispatches, and, when the pass holds them, the MFMA-busy fraction
+    SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE / xcds * simds): GRBM_GUI_ACTIVE counts the
+    dispatch's GPU-active cycles once per XCD, SQ_VALU_MFMA_BUSY_CYCLES the matrix-core busy
+    cycles summed over all SIMDs (MI355X: 8 XCDs, 256 CUs x 4 SIMDs)."""
+    vals = {c: last_counter(directory, match, c, last) for c in counter_names(directory, match)}
+    out = [f"# counters, mean per dispatch over the last {last} dispatches of /{match}/"]
+    out += [f"{c:34s} {v:20.1f}" for c, v in vals.items()]
+    if "SQ_VALU_MFMA_BUSY_CYCLES" in vals and vals.get("GRBM_GUI_ACTIVE"):
+        cyc = vals["GRBM_GUI_ACTIVE"] / xcds
+        out.append(f"# active cycles per XCD {cyc:.4g}; MFMA busy fraction "
+                   f"{vals['SQ_VALU_MFMA_BUSY_CYCLES'] / (cyc * simds):.4f}")
+    if "SQ_INSTS_MFMA" in vals and vals.get("SQ_INSTS_VALU"):
+        out.append(f"# non-MFMA VALU instructions per MFMA "
+                   f"{(vals['SQ_INSTS_VALU'] - vals['SQ_INSTS_MFMA']) / max(vals['SQ_INSTS_MFMA'], 1):.2f}")
+    if "SQ_VALU_MFMA_COEXEC_CYCLES" in vals and vals.get("SQ_VALU_MFMA_BUSY_CYCLES"):
+        out.append(f"# VALU issued during MFMA-busy cycles "
+                   f"{vals['SQ_VALU_MFMA_COEXEC_CYCLES'] / vals['SQ_VALU_MFMA_BUSY_CYCLES']:.4f}")
+    return "\n".join(out) + "\n"
+
+
 def traffic_entry(fetch_dir: str, write_dir: str, kernel: str, calib: str, calib_mib: int, last: int):
     """HBM bytes per launch of `kernel` from FETCH_SIZE / WRITE_SIZE (KiB per dispatch), each
     scaled by what the counter reads for the calibration kernel that reads and writes exactly
@@ -139,7 +171,10 @@ if __name__ == "__main__":
     m = opt("--match")
     last = opt("--last")
     traffic = opt("--traffic-json")
-    if traffic:
+    clast = opt("--counters-last")
+    if clast:
+        sys.stdout.write(counters_last(args[0], m or ".", int(clast)))
+    elif traffic:
         # --traffic-json OUT --workload W --kernel-source SRC --fetch-dir D1 --write-dir D2
         #   --calib-match REGEX --calib-mib N --last K --match KERNEL_REGEX
         import hashlib
