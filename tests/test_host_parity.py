@@ -14,7 +14,7 @@ from oracle import blockhash as obh
 from oracle.planner import Planner, PlanError, form_batches
 from workloads import get_config
 from workloads.streams import (Source, make_request, free_order, make_stream, stream_docqa_hit,
-                               KIND_DOC, KIND_QUESTION)
+                               KIND_DOC)
 
 
 def test_hash_matches_oracle():

@@ -9,7 +9,7 @@ with an unbounded window, pins, and the ARC invariants.
 
 import numpy as np
 
-from oracle.arc import ARC, CASE_I, CASE_II, CASE_IVA_T1DEL, CASE_IVB, FROM_T1, FROM_B1
+from oracle.arc import ARC, CASE_I, CASE_II, CASE_IVA_T1DEL, CASE_IVB, FROM_T1
 from oracle.lru import LRU
 
 A, B, C, D = 101, 102, 103, 104
