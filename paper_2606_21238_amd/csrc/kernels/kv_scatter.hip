@@ -6,22 +6,25 @@
 // [blocks][kv_heads][D][16] (dim-major, so that the attention kernel's P.V contraction reads
 // 8 consecutive tokens of one dimension as one 16-byte operand).
 //
-// A work-group handles 64 tokens of one KV head and DPW of its head dimensions (16 for small
-// batches, so that a decode step still spreads over many work-groups; 64 otherwise, whole
-// 128-byte row segments).  K rows are copied as 16-byte chunks.  V rows are staged through
-// LDS and written transposed: where 8 consecutive tokens sit in 8 consecutive slots of one
-// block (8-aligned, the common case of a prefill), one 16-byte store writes them for one
-// dimension; otherwise each token's value is a 2-byte store.  Bytes are copied, never
-// converted: the result is bit-exact.  Slots outside the pool are skipped.
+// A work-group handles 64 tokens of one KV head and DPW of its head dimensions: 16 for small
+// batches, so that a decode step still spreads over many work-groups; the whole head
+// otherwise.  K rows are copied as 16-byte chunks.  V rows are staged through LDS and written
+// dim-major.  A run is 8 tokens of the work-group whose slots are 8 consecutive slots of one
+// block starting at a multiple of 8 (most of a prefill, wherever its request starts in the
+// batch); a run's 8 values of one dimension go out as one 16-byte store, with consecutive
+// lanes on consecutive dimensions so that a wave's stores are contiguous.  Every other token
+// is written the coalesced 2-byte way: lane = token, 64 consecutive tokens of one dimension
+// per store instruction.  Bytes are copied, never converted: the result is bit-exact.  Slots
+// outside the pool are skipped.
 #include <hip/hip_runtime.h>
 
 #include "../host/internal.hpp"
 
 namespace {
 
-constexpr int kTok = 64;
+constexpr int kTok = 64;              // tokens per work-group: one wave's lanes
 constexpr int kThreads = 256;
-constexpr int kGroups = kTok / 8;      // 8-token groups of a work-group
+constexpr int kMaxRuns = kTok / 8;
 
 template <int D, int DPW>
 __global__ __launch_bounds__(kThreads) void kv_scatter_kernel(
@@ -32,7 +35,9 @@ __global__ __launch_bounds__(kThreads) void kv_scatter_kernel(
   constexpr int VROW = DPW + 2;        // padded LDS row (u16): column reads spread over banks
   __shared__ uint32_t sv32[kTok * VROW / 2];
   __shared__ int32_t sslot[kTok];
-  __shared__ int32_t gbase[kGroups];   // first slot of an 8-token run, or -1
+  __shared__ int32_t run_tok[kMaxRuns], run_slot[kMaxRuns];
+  __shared__ int32_t n_runs;
+  __shared__ uint64_t covered;         // bit t: token t belongs to a run
   uint16_t* sv = reinterpret_cast<uint16_t*>(sv32);
   const int h = blockIdx.y;
   const int d0 = blockIdx.z * DPW;     // first dimension of the slice
@@ -44,11 +49,22 @@ __global__ __launch_bounds__(kThreads) void kv_scatter_kernel(
     sslot[tid] = (s >= 0 && s < n_slots) ? s : -1;
   }
   __syncthreads();
-  if (tid < kGroups) {
-    const int32_t s = sslot[8 * tid];
-    bool run = s >= 0 && (s & 7) == 0;
-    for (int j = 1; j < 8 && run; ++j) run = sslot[8 * tid + j] == s + j;
-    gbase[tid] = run ? s : -1;
+  if (tid < kTok) {                    // wave 0: find the runs
+    const int32_t s = sslot[tid];
+    bool start = s >= 0 && (s & 7) == 0 && tid + 7 < kTok;
+    for (int j = 1; j < 8 && start; ++j) start = sslot[tid + j] == s + j;
+    const uint64_t m = __builtin_amdgcn_ballot_w64(start);
+    if (start) {
+      const int r = __builtin_popcountll(m & ((1ull << tid) - 1));  // runs never overlap
+      run_tok[r] = tid;
+      run_slot[r] = s;
+    }
+    if (tid == 0) {
+      uint64_t c = 0;
+      for (int j = 0; j < 8; ++j) c |= m << j;
+      covered = c;
+      n_runs = __builtin_popcountll(m);
+    }
   }
   // K: direct 16-byte copies; V: into LDS (row = token, padded)
   for (int c = tid; c < kTok * CH; c += kThreads) {
@@ -67,32 +83,29 @@ __global__ __launch_bounds__(kThreads) void kv_scatter_kernel(
     dst[0] = vv.x; dst[1] = vv.y; dst[2] = vv.z; dst[3] = vv.w;
   }
   __syncthreads();
-  // V: (8-token group, dimension) per thread.  Lane pairs take the two 8-token halves of a
-  // block and consecutive pairs consecutive dimensions, so that a wave's 16-byte stores cover
-  // one contiguous stretch of a block's dim-major V (32 bytes per dimension).
-  for (int e = tid; e < kGroups * DPW; e += kThreads) {
-    const int half = e & 1, rest = e >> 1;
-    const int g = 2 * (rest / DPW) + half, dl = rest % DPW, d = d0 + dl;
-    const int32_t sb = gbase[g];
-    if (sb >= 0) {
-      uint16_t v8[8];
+  // V of the runs: (run, dimension) per thread, dimensions fastest across lanes
+  const int nr = n_runs;
+  for (int e = tid; e < nr * DPW; e += kThreads) {
+    const int r = e / DPW, dl = e % DPW, d = d0 + dl;
+    const int tl = run_tok[r];
+    const int32_t sb = run_slot[r];
+    uint16_t v8[8];
 #pragma unroll
-      for (int j = 0; j < 8; ++j) v8[j] = sv[(8 * g + j) * VROW + dl];
-      uint4 w;
-      w.x = v8[0] | (static_cast<uint32_t>(v8[1]) << 16);
-      w.y = v8[2] | (static_cast<uint32_t>(v8[3]) << 16);
-      w.z = v8[4] | (static_cast<uint32_t>(v8[5]) << 16);
-      w.w = v8[6] | (static_cast<uint32_t>(v8[7]) << 16);
-      *reinterpret_cast<uint4*>(v_pool + ((static_cast<int64_t>(sb >> 4) * hkv + h) * D + d) * 16 + (sb & 15)) = w;
-    } else {
-      for (int j = 0; j < 8; ++j) {
-        const int tl = 8 * g + j;
-        const int32_t s = sslot[tl];
-        if (s < 0 || t0 + tl >= n_tokens) continue;
-        v_pool[((static_cast<int64_t>(s >> 4) * hkv + h) * D + d) * 16 + (s & 15)] = sv[tl * VROW + dl];
-      }
-    }
+    for (int j = 0; j < 8; ++j) v8[j] = sv[(tl + j) * VROW + dl];
+    uint4 w;
+    w.x = v8[0] | (static_cast<uint32_t>(v8[1]) << 16);
+    w.y = v8[2] | (static_cast<uint32_t>(v8[3]) << 16);
+    w.z = v8[4] | (static_cast<uint32_t>(v8[5]) << 16);
+    w.w = v8[6] | (static_cast<uint32_t>(v8[7]) << 16);
+    *reinterpret_cast<uint4*>(v_pool + ((static_cast<int64_t>(sb >> 4) * hkv + h) * D + d) * 16 + (sb & 15)) = w;
   }
+  // V of the other tokens: lane = token, dimensions over the waves
+  const int tl = tid & (kTok - 1);
+  const int32_t s = sslot[tl];
+  if (s < 0 || t0 + tl >= n_tokens || ((covered >> tl) & 1ull)) return;
+  const int64_t base = ((static_cast<int64_t>(s >> 4) * hkv + h) * D + d0) * 16 + (s & 15);
+  for (int d = tid >> 6; d < DPW; d += kThreads / kTok)
+    v_pool[base + static_cast<int64_t>(d) * 16] = sv[tl * VROW + d];
 }
 
 }  // namespace
@@ -114,7 +127,7 @@ extern "C" int32_t arckv_kv_scatter(void* k_pool, void* v_pool, const void* k_ne
       return arckv::fail(ARCKV_EINVAL, "kv_scatter: pools and new rows must be 16-byte aligned");
   // small batches (decode) split the head dimension finely to spread over more work-groups
   const bool small = n_tokens <= 1024;
-  const int dpw = small ? 16 : 64;
+  const int dpw = small ? 16 : head_dim;
   const dim3 grid(static_cast<unsigned>((n_tokens + kTok - 1) / kTok), num_kv_heads,
                   static_cast<unsigned>(head_dim / dpw));
   auto* st = static_cast<hipStream_t>(stream);
@@ -129,7 +142,7 @@ extern "C" int32_t arckv_kv_scatter(void* k_pool, void* v_pool, const void* k_ne
   if (head_dim == 64) {
     if (small) ARCKV_SCATTER(64, 16); else ARCKV_SCATTER(64, 64);
   } else {
-    if (small) ARCKV_SCATTER(128, 16); else ARCKV_SCATTER(128, 64);
+    if (small) ARCKV_SCATTER(128, 16); else ARCKV_SCATTER(128, 128);
   }
 #undef ARCKV_SCATTER
   const hipError_t e = hipGetLastError();
