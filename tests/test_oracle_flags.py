@@ -62,3 +62,30 @@ def test_no_intra_batch_reuse_recomputes_a_prefix_made_in_the_same_batch():
         plan = pl.plan_batch([(h, 32)])
         assert plan.hit_blocks == [1]
         pl.release_batch()
+
+
+def test_a_page_back_from_a_ghost_list_counts_as_made_in_the_batch():
+    # c = 2, one full block + a partial tail per request:
+    #   [B] -> T1 = [B]; [D] -> T1 = [B, D]; [D] again -> D to T2; [E]: |T1| + |B1| = 1 < c
+    #   with 2 pages resident, so REPLACE (|T1| = 1 > p = 0) moves B to B1.
+    # Then one batch [B + 3 tokens], [B + 5 tokens]: the first references B as a B1 ghost hit
+    # (Case II), which brings it back in this batch.  With reuse the second request hits it
+    # (k = 1); without, its prefix stops there (k = 0).
+    from oracle import blockhash as obh
+    blk = {name: np.arange(16, dtype=np.int32) + 100 * i for i, name in enumerate("BDE")}
+
+    def req(name, tail):
+        t = np.concatenate([blk[name], np.arange(tail, dtype=np.int32) + 9000 + tail])
+        return obh.hash_blocks(t), len(t)
+
+    for reuse, want in ((True, [0, 1]), (False, [0, 0])):
+        pl = Planner("arc", 2, 8, 4, intra_batch_reuse=reuse)
+        for name in "BDDE":
+            pl.plan_batch([req(name, 3)])
+            pl.release_batch()
+        hb = obh.hash_blocks(blk["B"])[0]
+        assert hb in pl.cache.B1 and not pl.cache.resident(hb)
+        plan = pl.plan_batch([req("B", 3), req("B", 5)])
+        assert plan.hit_blocks == want
+        assert pl.cache.log[-2].case == CASE_II      # the first request's reference of B
+        pl.release_batch()

@@ -100,3 +100,22 @@ def test_arc_invariants_hold_with_windows():
                 arc.reference(k, depth=k % 17)
                 arc.check_invariants()
                 assert 0.0 <= arc.p <= 12
+
+
+def test_planner_hands_each_block_its_depth():
+    # LRU, c = 3, head-first references: a 3-block prompt leaves x0, x1, x2 (depths 0, 1, 2) in
+    # LRU -> MRU order.  A new block then evicts the LRU-most page x0 with W = 1 and the deepest,
+    # x2, with W = 3.
+    from oracle import blockhash as obh
+    from oracle.planner import Planner
+    x = np.arange(48 + 1, dtype=np.int32)
+    y = np.arange(16 + 1, dtype=np.int32) + 5000
+    hx = obh.hash_blocks(x)
+    for w, gone in ((1, 0), (3, 2)):
+        pl = Planner("lru", 3, 8, 4, ref_order="head_first", victim_window=w)
+        pl.plan_batch([(hx, len(x))])
+        pl.release_batch()
+        assert list(pl.cache.L) == list(hx)
+        pl.plan_batch([(obh.hash_blocks(y), len(y))])
+        pl.release_batch()
+        assert pl.cache.log[-1].evicted == hx[gone]
