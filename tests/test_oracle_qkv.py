@@ -96,3 +96,17 @@ def test_head_split_and_value_pass_through():
 
 def test_token_positions_follow_the_suffixes():
     assert qkv.token_positions([0, 3, 3, 5], [10, 4, 2]).tolist() == [7, 8, 9, 0, 1]
+
+
+def test_projection_is_rounded_to_bf16_before_the_rotation():
+    # Worked by hand, one query head of two dims (f_0 = 1) at position 1: x = [1, 2^-8],
+    # query row 0 of W = [1, 1] gives y = 1 + 2^-8, the tie that bf16 rounds to 1.0.  The
+    # rotated pair is (y cos 1, y sin 1): from the rounded y that is (0.540302..., 0.841470...)
+    # -> bf16 1.078125 / 2 (0x3F0A) and 1.6796875 / 2 (0x3F57); the unrounded y would give
+    # 0.542413... and 0.844758... -> 0x3F0B and 0x3F58.
+    x = np.array([[0x3F80, 0x3B80]], dtype=np.uint16)           # 1.0, 2^-8
+    w = np.zeros((6, 2), dtype=np.uint16)                       # rows: q0 q1 | k0 k1 | v0 v1
+    w[0] = [0x3F80, 0x3F80]
+    (q, k, v), _ = qkv.qkv_rope(x, w, np.array([1]), 1, 1, 2, theta=10000.0)
+    assert q.reshape(-1).tolist() == [0x3F0A, 0x3F57]
+    assert k.reshape(-1).tolist() == [0, 0] and v.reshape(-1).tolist() == [0, 0]
