@@ -23,7 +23,6 @@
 // they all stream is fetched into that XCD's L2 once.
 #include <algorithm>
 #include <cmath>
-#include <unordered_map>
 #include <vector>
 
 #include "internal.hpp"
@@ -130,13 +129,20 @@ extern "C" int32_t arckv_attention_plan(const int32_t* cu_q, const int32_t* seq_
 
   // XCD-aware order: assign whole groups to XCDs (largest first, to the least-loaded XCD),
   // then emit position-major so work-group i runs on XCD i % 8; each XCD's list is longest first.
-  std::unordered_map<int64_t, int64_t> cost_of;
-  for (const Item& it : items) cost_of[it.group] += it.cost;
-  std::vector<std::pair<int64_t, int64_t>> groups(cost_of.begin(), cost_of.end());  // (group, cost)
+  const int64_t n_groups = static_cast<int64_t>(n_reqs) * num_kv_heads;  // group = req * hkv + kvh
+  std::vector<int64_t> cost_of(static_cast<size_t>(n_groups), 0);
+  std::vector<char> used(static_cast<size_t>(n_groups), 0);
+  for (const Item& it : items) {
+    cost_of[it.group] += it.cost;
+    used[it.group] = 1;
+  }
+  std::vector<std::pair<int64_t, int64_t>> groups;  // (group, cost)
+  for (int64_t g = 0; g < n_groups; ++g)
+    if (used[g]) groups.push_back({g, cost_of[g]});
   std::sort(groups.begin(), groups.end(), [](const auto& a, const auto& b) {
     return a.second != b.second ? a.second > b.second : a.first < b.first;
   });
-  std::unordered_map<int64_t, int> xcd_of;
+  std::vector<int32_t> xcd_of(static_cast<size_t>(n_groups), 0);
   int64_t load[kXcds] = {0};
   for (const auto& g : groups) {
     int best = 0;
@@ -154,18 +160,30 @@ extern "C" int32_t arckv_attention_plan(const int32_t* cu_q, const int32_t* seq_
   // items whose key ranges are within ~10 % of each other count as equally long and are kept
   // together by group, so that the work-groups running at the same time on the XCD are few
   // groups' query tiles streaming the same keys and values, which the XCD's L2 serves once.
-  std::unordered_map<int64_t, int64_t> rank_of;
+  // The sort keys (length bucket, group rank, length) are computed once per item.
+  std::vector<int64_t> rank_of(static_cast<size_t>(n_groups), 0);
   for (size_t g = 0; g < groups.size(); ++g) rank_of[groups[g].first] = static_cast<int64_t>(g);
   auto bucket = [](int64_t cost) {  // log_{1.1} of the key-range length
     return cost > 0 ? static_cast<int64_t>(std::log(static_cast<double>(cost)) / std::log(1.1)) : -1;
   };
-  for (auto& v : per_xcd)
-    std::stable_sort(v.begin(), v.end(), [&](const Item& a, const Item& b) {
-      const int64_t ba = bucket(a.cost), bb = bucket(b.cost);
-      if (ba != bb) return ba > bb;
-      const int64_t ra = rank_of[a.group], rb = rank_of[b.group];
-      return ra != rb ? ra < rb : a.cost > b.cost;
+  struct Key {
+    int64_t bucket, rank, cost;
+    int32_t idx;
+  };
+  std::vector<Key> keys;
+  std::vector<Item> sorted;
+  for (auto& v : per_xcd) {
+    keys.clear();
+    for (size_t i = 0; i < v.size(); ++i)
+      keys.push_back({bucket(v[i].cost), rank_of[v[i].group], v[i].cost, static_cast<int32_t>(i)});
+    std::stable_sort(keys.begin(), keys.end(), [](const Key& a, const Key& b) {
+      if (a.bucket != b.bucket) return a.bucket > b.bucket;
+      return a.rank != b.rank ? a.rank < b.rank : a.cost > b.cost;
     });
+    sorted.clear();
+    for (const Key& k : keys) sorted.push_back(v[k.idx]);
+    v.swap(sorted);
+  }
   size_t longest = 0;
   for (auto& v : per_xcd) longest = std::max(longest, v.size());
   std::vector<Item> ordered;

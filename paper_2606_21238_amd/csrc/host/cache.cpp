@@ -49,49 +49,54 @@ struct List {
   int64_t size = 0;
 };
 
-// identity -> node index; at most 2c + 1 live entries, table at least 4x that (power of two)
+// identity -> node index; at most 2c + 1 live entries, table at least 2x that (power of two)
 class NodeIndex {
  public:
   void init(int64_t max_entries) {
     size_t cap = 16;
-    while (cap < static_cast<size_t>(4 * max_entries + 16)) cap <<= 1;
-    keys_.assign(cap, 0);
-    vals_.assign(cap, -1);
+    while (cap < static_cast<size_t>(2 * max_entries + 16)) cap <<= 1;
+    tab_.assign(cap, Entry{});
     mask_ = cap - 1;
   }
   int32_t find(uint64_t key) const {
     for (size_t i = slot(key);; i = (i + 1) & mask_) {
-      if (vals_[i] < 0) return -1;
-      if (keys_[i] == key) return vals_[i];
+      const Entry& e = tab_[i];
+      if (e.val < 0) return -1;
+      if (e.key == key) return e.val;
     }
   }
+  // start fetching the cache line a later find(key) begins its probe at
+  void prefetch(uint64_t key) const { __builtin_prefetch(&tab_[slot(key)]); }
   void insert(uint64_t key, int32_t val) {  // key absent
     size_t i = slot(key);
-    while (vals_[i] >= 0) i = (i + 1) & mask_;
-    keys_[i] = key;
-    vals_[i] = val;
+    while (tab_[i].val >= 0) i = (i + 1) & mask_;
+    tab_[i] = Entry{key, val, 0};
   }
   void erase(uint64_t key) {  // key present
     size_t i = slot(key);
-    while (keys_[i] != key || vals_[i] < 0) i = (i + 1) & mask_;
+    while (tab_[i].key != key || tab_[i].val < 0) i = (i + 1) & mask_;
     // backward-shift: pull later entries of the probe run into the hole
-    for (size_t j = (i + 1) & mask_; vals_[j] >= 0; j = (j + 1) & mask_) {
-      const size_t home = slot(keys_[j]);
+    for (size_t j = (i + 1) & mask_; tab_[j].val >= 0; j = (j + 1) & mask_) {
+      const size_t home = slot(tab_[j].key);
       // entry j may move to the hole i iff its home is not cyclically in (i, j]
       const bool between = i <= j ? (home > i && home <= j) : (home > i || home <= j);
       if (!between) {
-        keys_[i] = keys_[j];
-        vals_[i] = vals_[j];
+        tab_[i] = tab_[j];
         i = j;
       }
     }
-    vals_[i] = -1;
+    tab_[i].val = -1;
   }
 
  private:
+  // key and value side by side: a lookup touches one cache line (four entries per line)
+  struct Entry {
+    uint64_t key = 0;
+    int32_t val = -1;
+    int32_t pad = 0;
+  };
   size_t slot(uint64_t key) const { return static_cast<size_t>((key * 0x9E3779B97F4A7C15ull) >> 20) & mask_; }
-  std::vector<uint64_t> keys_;
-  std::vector<int32_t> vals_;
+  std::vector<Entry> tab_;
   size_t mask_ = 0;
 };
 
@@ -502,11 +507,19 @@ extern "C" int32_t arckv_plan_batch(arckv_cache* c, const arckv_req* reqs, int32
     // the prefix's nodes, looked up once: pinned below and handed to their references
     thread_local std::vector<int32_t> prefix_node;
     prefix_node.resize(static_cast<size_t>(nf > 0 ? nf : 1));
-    while (k < nf) {
-      const int32_t n = c->find(q.hashes[k]);
-      if (!c->reusable_node(n)) break;
-      prefix_node[k++] = n;
+    // Lookups first, with the index lines and then the nodes fetched some blocks ahead (the
+    // table and the nodes are far larger than the caches); then the prefix is the run of
+    // leading reusable nodes.  Nothing changes state in between, so the early lookups past
+    // the first miss are only wasted work.
+    constexpr int64_t kAhead = 8;
+    for (int64_t i = 0; i < std::min(nf, kAhead); ++i) c->index.prefetch(q.hashes[i]);
+    for (int64_t i = 0; i < nf; ++i) {
+      if (i + kAhead < nf) c->index.prefetch(q.hashes[i + kAhead]);
+      const int32_t n = c->find(q.hashes[i]);
+      prefix_node[i] = n;
+      if (n >= 0) __builtin_prefetch(&c->nodes[n]);
     }
+    while (k < nf && c->reusable_node(prefix_node[k])) ++k;
     if (k * ARCKV_BLOCK_TOKENS == q.n_tokens) k -= 1;  // whole prompt cached: recompute last block
     for (int64_t i = 0; i < k; ++i) c->nodes[prefix_node[i]].pin_epoch = c->epoch;
     int32_t* row = plan->block_tables + static_cast<int64_t>(r) * plan->bt_stride;
