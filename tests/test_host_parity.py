@@ -277,3 +277,33 @@ def test_attention_plan_places_a_group_on_one_xcd():
             continue
         key = (int(it[0]), int(it[1]))
         assert xcd_of.setdefault(key, i % 8) == i % 8
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2, 3])
+def test_attention_plan_order_is_xcd_phased_and_longest_first(seed):
+    # Work-group i of a launch runs on XCD i % 8.  The order the planner emits keeps every
+    # (request, KV head) group on one XCD when there are at least 8 groups, lists each XCD's
+    # items longest first (items within ~10 % of each other may come in any order), pads with
+    # idle slots (request -1) only to keep that phase, and never ends on an idle slot.
+    rng = np.random.default_rng(seed)
+    n = int(rng.integers(6, 40))
+    S = rng.integers(1, [40, 300, 3000, 600][seed], n)
+    L = S + 16 * rng.integers(0, 600, n)
+    hkv = [8, 2, 8, 1][seed]
+    hq = hkv * [4, 8, 4, 5][seed]
+    ap = ak.attention_plan(np.concatenate([[0], np.cumsum(S)]), L, hq, hkv, 128, 256)
+    items = ap.work[: ap.n_work]
+    assert ap.n_work == 0 or items[-1][0] >= 0
+    groups = {(int(it[0]), int(it[1])) for it in items if it[0] >= 0}
+    xcd_of, last_cost = {}, [None] * 8
+    for i, it in enumerate(items):
+        req, kvh, _, a, b = (int(x) for x in it[:5])
+        if req < 0:
+            continue
+        x = i % 8
+        if len(groups) >= 8:
+            assert xcd_of.setdefault((req, kvh), x) == x
+        cost = b - a
+        if last_cost[x] is not None:
+            assert cost <= last_cost[x] * 1.1 + 1
+        last_cost[x] = cost
