@@ -138,3 +138,28 @@ def test_prepare_from_kept_hashes_equals_prepare_from_tokens():
         a.release_batch()
         b.release_batch()
     assert a.log() == b.log()
+
+
+def test_kept_hashes_may_be_lists_of_large_ints_and_must_cover_the_blocks():
+    # hashes above 2^63 passed as plain Python ints reach the library exactly, and a request
+    # whose hash array is shorter than its full blocks is refused before any state changes
+    toks = [np.arange(40, dtype=np.int32) + 7, np.arange(70, dtype=np.int32) * 3]
+    hs = [ak.hash_blocks(t) for t in toks]
+    big = [[int(x) | (1 << 63) for x in h] for h in hs]     # every identity >= 2^63
+    packed = np.zeros(1 << 16, dtype=np.int32)
+    a = ak.BlockCache("arc", 64, 80, 4)
+    b = ak.BlockCache("arc", 64, 80, 4)
+    ra = a.prepare_native(None, 8, 2, 64, 16, packed.copy(), hashes=[np.array(h, dtype=np.uint64) for h in big],
+                          n_tokens=[40, 70])
+    rb = b.prepare_native(None, 8, 2, 64, 16, packed.copy(), hashes=big, n_tokens=[40, 70])
+    assert ra[0] == rb[0] == 0 and ra[1] == rb[1]
+    assert (ra[2] == rb[2]).all() and (ra[3] == rb[3]).all()
+    a.release_batch()
+    b.release_batch()
+    ka, pa = a.snapshot(ak.LIST_T1)
+    kb, pb = b.snapshot(ak.LIST_T1)
+    assert (ka == kb).all() and (pa == pb).all() and int(big[1][-1]) in ka.tolist()
+    with pytest.raises(ValueError):
+        b.prepare_native(None, 8, 2, 64, 16, packed.copy(), hashes=[big[0], big[1][:2]], n_tokens=[40, 70])
+    kc, pc = b.snapshot(ak.LIST_T1)
+    assert (kc == kb).all() and (pc == pb).all()
