@@ -507,19 +507,25 @@ extern "C" int32_t arckv_plan_batch(arckv_cache* c, const arckv_req* reqs, int32
     // the prefix's nodes, looked up once: pinned below and handed to their references
     thread_local std::vector<int32_t> prefix_node;
     prefix_node.resize(static_cast<size_t>(nf > 0 ? nf : 1));
-    // Lookups first, with the index lines and then the nodes fetched some blocks ahead (the
-    // table and the nodes are far larger than the caches); then the prefix is the run of
-    // leading reusable nodes.  Nothing changes state in between, so the early lookups past
-    // the first miss are only wasted work.
-    constexpr int64_t kAhead = 8;
+    // Lookups run in chunks ahead of the reusability checks, with the index lines and then
+    // the nodes fetched some blocks ahead (the table and the nodes are far larger than the
+    // caches); the prefix is the run of leading reusable nodes.  Nothing changes state in
+    // between, so lookups past the first miss (at most one chunk) are only wasted work.
+    constexpr int64_t kAhead = 8, kChunk = 128;
     for (int64_t i = 0; i < std::min(nf, kAhead); ++i) c->index.prefetch(q.hashes[i]);
-    for (int64_t i = 0; i < nf; ++i) {
-      if (i + kAhead < nf) c->index.prefetch(q.hashes[i + kAhead]);
-      const int32_t n = c->find(q.hashes[i]);
-      prefix_node[i] = n;
-      if (n >= 0) __builtin_prefetch(&c->nodes[n]);
+    int64_t looked = 0;
+    while (looked < nf) {
+      const int64_t end = std::min(nf, looked + kChunk);
+      for (int64_t i = looked; i < end; ++i) {
+        if (i + kAhead < nf) c->index.prefetch(q.hashes[i + kAhead]);
+        const int32_t n = c->find(q.hashes[i]);
+        prefix_node[i] = n;
+        if (n >= 0) __builtin_prefetch(&c->nodes[n]);
+      }
+      looked = end;
+      while (k < looked && c->reusable_node(prefix_node[k])) ++k;
+      if (k < looked) break;
     }
-    while (k < nf && c->reusable_node(prefix_node[k])) ++k;
     if (k * ARCKV_BLOCK_TOKENS == q.n_tokens) k -= 1;  // whole prompt cached: recompute last block
     for (int64_t i = 0; i < k; ++i) c->nodes[prefix_node[i]].pin_epoch = c->epoch;
     int32_t* row = plan->block_tables + static_cast<int64_t>(r) * plan->bt_stride;
