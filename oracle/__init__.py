@@ -20,8 +20,9 @@ Contents, each module citing the passage of the paper it follows:
   use by the running batch.
 * ``lru`` -- the LRU baseline the paper compares against (Sec. 2, Sec. 4).
 * ``planner`` -- per-batch prefix lookup, policy references, physical block
-  placement, block tables and slot mappings (Sec. 2 "paging-style allocation";
-  Sec. 3 "the LLM engine processes the miss, regenerating the block").
+  placement, block tables and slot mappings (Sec. 2: blocks handed out by a
+  paging allocator; Sec. 3: a miss is recomputed by the engine, which writes the
+  block's KV again).
 * ``kvpool`` -- the paged pool image, the KV scatter, and the gather through a
   block table.
 * ``attention`` -- fp64 causal softmax attention of the uncached suffix over

@@ -2,8 +2,8 @@
 
 Paged attention keeps K/V in fixed-size blocks reached through a per-request
 block table (Sec. 2, "LLM Serving"); the tokens a miss recomputes are written
-into their blocks (Sec. 3, "the LLM engine processes the miss, regenerating the
-block").  Element values are bf16 bit patterns held as uint16, so every
+into their blocks (Sec. 3: the engine recomputes a missed block and writes its
+KV again).  Element values are bf16 bit patterns held as uint16, so every
 operation here is an exact copy.
 
 Pool layout (version 1, an interface shared with the library by definition):

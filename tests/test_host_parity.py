@@ -110,6 +110,73 @@ def test_random_streams_bit_exact(policy, ref_order, seed, window, reuse):
     assert pair.orc.totals.prefix_hit_tokens > 0
 
 
+def _golden_traces():
+    import json
+    import os
+    g = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "arc_traces.json")))
+    return [("arc", t) for t in g["traces"]] + [("dbl", t) for t in g["dbl_traces"]]
+
+
+@pytest.mark.parametrize("policy,tr", _golden_traces(), ids=lambda v: v if isinstance(v, str) else v["refs"])
+def test_library_replays_the_hand_derived_traces(policy, tr):
+    """The library's cache against the hand-derived ARC and DBL traces themselves (not the
+    oracle): one single-block request per batch is exactly one policy reference of its key,
+    so the decision log must list the fixture's cases, evicted and dropped pages and p."""
+    c = tr["c"]
+    cache = ak.BlockCache(policy, c, c + 1, 1)
+    cache.set_log(1 << 10)
+    for ch in tr["refs"]:
+        cache.plan_batch([(np.array([ord(ch)], dtype=np.uint64), 16)])
+        cache.release_batch()
+    log = cache.log()
+    case_names = ["I", "II", "III", "IVA", "IVA_T1DEL", "IVB"]
+    assert [case_names[e[1]] for e in log] == tr["cases"]
+    assert ["" if e[3] == 0 else chr(e[2]) for e in log] == tr["evicted"]
+    if "dropped" in tr:
+        assert ["" if e[5] == 0 else chr(e[4]) for e in log] == tr["dropped"]
+    assert [e[7] for e in log] == [float(x) for x in tr["p"]]
+    lists = [("".join(chr(k) for k in cache.snapshot(li)[0])) for li in
+             (ak.LIST_T1, ak.LIST_T2, ak.LIST_B1, ak.LIST_B2)]
+    assert lists == [tr["T1"], tr["T2"], tr["B1"], tr["B2"]]
+    assert cache.stats()["p"] == tr["p_final"]
+
+
+def _planner_cases():
+    import json
+    import os
+    g = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "planner_cases.json")))
+    return [pytest.param(c, v, id=f"{c['name']}-reuse{int(v['intra_batch_reuse'])}") for c in g["cases"]
+            for v in c.get("variants", [{"intra_batch_reuse": c.get("intra_batch_reuse", True)}])]
+
+
+@pytest.mark.parametrize("case,var", _planner_cases())
+def test_library_hand_derived_plans(case, var):
+    """The library's planner against the hand-derived plans themselves (prefix pins, scratch
+    FIFO, a B2 ghost hit as a page made in the batch)."""
+    case_names = ["I", "II", "III", "IVA", "IVA_T1DEL", "IVB"]
+    cache = ak.BlockCache(case["policy"], case["capacity"], case["num_phys"], case["scratch"],
+                          intra_batch_reuse=var["intra_batch_reuse"])
+    cache.set_log(1 << 10)
+    for bi, b in enumerate(case["batches"]):
+        n0 = len(cache.log())
+        plan = cache.plan_batch([(np.array(h, dtype=np.uint64), n) for h, n in b["reqs"]])
+        for r, row in enumerate(b["tables"]):
+            assert plan.block_tables[r, : len(row)].tolist() == row, bi
+        want = var["last_hit_blocks"] if (bi == len(case["batches"]) - 1 and "last_hit_blocks" in var) \
+            else b["hit_blocks"]
+        assert plan.hit_blocks.tolist() == want, bi
+        evs = cache.log()[n0:]
+        if "cases" in b:
+            assert [case_names[e[1]] for e in evs] == b["cases"]
+        if "dropped" in b:
+            assert [e[4] for e in evs] == b["dropped"]
+        cache.release_batch()
+    f = case["final"]
+    lists = [[int(k) for k in cache.snapshot(li)[0]] for li in (ak.LIST_T1, ak.LIST_T2, ak.LIST_B1, ak.LIST_B2)]
+    assert lists == [f["T1"], f["T2"], f["B1"], f["B2"]]
+    assert cache.stats()["p"] == f["p"]
+
+
 def test_tiny_config_host_phase():
     cfg = get_config("tiny")
     order = free_order(cfg.seed, cfg.num_phys)

@@ -148,3 +148,18 @@ def test_row_sampling_matches_full():
     part = att.prefill_attention(q[P:], kp, vp, [table], [0, L - P], [L], 0.3, rows_per_request=[rows])
     assert np.array_equal(part[rows], full[rows])
     assert np.isnan(part[1]).all()
+
+
+def test_dominant_key_beyond_the_exponential_range():
+    # A score of 6400 is far past exp's fp64 range (overflow above ~709.8); softmax is
+    # shift-invariant, so the output is still exactly that key's value: every other weight
+    # is exp(-6400) = 0.
+    rng = np.random.default_rng(14)
+    L, d = 24, 8
+    v = rand_bf16_bits(rng, (L, 1, d))
+    k = np.zeros((L, 1, d), dtype=np.uint16)
+    q = np.zeros((L, 1, d), dtype=np.uint16)
+    q[:, 0, 0] = 0x4100                       # 8.0
+    k[3, 0, 0] = 0x4100
+    o = att.request_attention(q[8:], k, v, 8, 100.0)
+    assert np.array_equal(o[:, 0], np.repeat(att.bf16_to_f64(v)[3:4, 0], L - 8, axis=0))

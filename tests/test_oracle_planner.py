@@ -162,3 +162,40 @@ def test_pool_gather_reproduces_every_visible_token():
         pl.cache.check_invariants()
     assert pl.totals.prefix_hit_tokens > 0
     assert pl.totals.case_counts[CASE_I] > 0
+
+
+def _planner_cases():
+    import json
+    import os
+    g = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "planner_cases.json")))
+    out = []
+    for case in g["cases"]:
+        for var in case.get("variants", [{"intra_batch_reuse": case.get("intra_batch_reuse", True)}]):
+            out.append(pytest.param(case, var, id=f"{case['name']}-reuse{int(var['intra_batch_reuse'])}"))
+    return out
+
+
+@pytest.mark.parametrize("case,var", _planner_cases())
+def test_hand_derived_plans(case, var):
+    """Hand-derived plans (tests/golden/planner_cases.json): prefix pages pinned before the
+    tail-first references, the scratch FIFO's order, and a B2 ghost hit counting as a page made
+    in the batch when intra-batch reuse is off."""
+    from oracle.arc import CASE_NAMES
+    pl = Planner(case["policy"], case["capacity"], case["num_phys"], case["scratch"],
+                 intra_batch_reuse=var["intra_batch_reuse"])
+    for bi, b in enumerate(case["batches"]):
+        n0 = len(pl.cache.log)
+        plan = pl.plan_batch([(list(h), n) for h, n in b["reqs"]])
+        assert plan.block_tables == b["tables"], bi
+        want_hits = var["last_hit_blocks"] if (bi == len(case["batches"]) - 1 and "last_hit_blocks" in var) \
+            else b["hit_blocks"]
+        assert plan.hit_blocks == want_hits, bi
+        evs = pl.cache.log[n0:]
+        if "cases" in b:
+            assert [CASE_NAMES[e.case] for e in evs] == b["cases"]
+        if "dropped" in b:
+            assert [e.dropped for e in evs] == b["dropped"]
+        pl.release_batch()
+    T1, T2, B1, B2, p = pl.cache.snapshot()
+    f = case["final"]
+    assert (list(T1), list(T2), list(B1), list(B2), p) == (f["T1"], f["T2"], f["B1"], f["B2"], f["p"])

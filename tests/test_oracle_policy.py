@@ -74,6 +74,8 @@ def test_arc_hand_derived_trace(tr):
     a, hits = run_arc(tr["refs"], tr["c"])
     assert [CASE_NAMES[e.case] for e in a.log] == tr["cases"]
     assert [chr(e.evicted) if e.evicted_from != FROM_NONE else "" for e in a.log] == tr["evicted"]
+    if "dropped" in tr:
+        assert [chr(e.dropped) if e.dropped_from != FROM_NONE else "" for e in a.log] == tr["dropped"]
     assert [e.p_after for e in a.log] == [float(x) for x in tr["p"]]
     assert hits == tr["hits"]
     T1, T2, B1, B2, p = a.snapshot()
