@@ -78,9 +78,10 @@ class PrefillEngine:
     def prepare(self, token_lists, stream=None, hashes=None, n_tokens=None) -> DeviceBatch:
         """plan() + upload() in one native call (arckv_prepare_batch): hashes, the cache plan
         and the attention work plan are written straight into the next pinned staging buffer of
-        the ring, then one asynchronous copy moves them to the device.  A caller that keeps its
-        requests' block hashes passes `hashes` and `n_tokens` instead of token lists."""
+        the ring, then one asynchronous copy on `stream` moves them to the device.  A caller that
+        keeps its requests' block hashes passes `hashes` and `n_tokens` instead of token lists."""
         import torch
+        ts = self._torch_stream(stream)
         t = self._turn
         self._turn = (t + 1) % self._ring
         if self._stage_ev[t] is not None:
@@ -92,16 +93,13 @@ class PrefillEngine:
             if st == _lib.ENOSPC and (host is None or d["n_packed"] > host.size):
                 cap = max(d["n_packed"], 1 << 16) * 2
                 self._stage[t] = torch.empty(cap, dtype=torch.int32, pin_memory=True)
-                self._dev_meta[t] = torch.empty(cap, dtype=torch.int32, device=self.device)
+                with torch.cuda.stream(ts):
+                    self._dev_meta[t] = torch.empty(cap, dtype=torch.int32, device=self.device)
                 continue
             _lib.check(st, "arckv_prepare_batch")
             break
         n_int = d["n_packed"]
-        dev = self._dev_meta[t][:n_int]
-        dev.copy_(self._stage[t][:n_int], non_blocking=True)
-        ev = torch.cuda.Event()
-        ev.record()
-        self._stage_ev[t] = ev
+        dev = self._copy_meta(t, n_int, ts)
         plan, ap = unpack_prepared(host, d, pl, hb)
         n, stride = d["n_reqs"], d["bt_stride"]
         bt = dev[d["off_block_tables"]:d["off_block_tables"] + n * stride].view(n, stride)
@@ -109,13 +107,14 @@ class PrefillEngine:
         sl = dev[d["off_seq_lens"]:d["off_seq_lens"] + n]
         sm = dev[d["off_slots"]:d["off_slots"] + d["n_slots"]]
         wk = dev[d["off_work"]:d["off_work"] + (d["n_work"] + d["n_combine"]) * 8].view(-1, 8)
-        if d["ws_bytes"] > self._ws.numel():
-            self._ws = torch.empty(d["ws_bytes"], dtype=torch.uint8, device=self.device)
+        self._ensure_ws(d["ws_bytes"], ts)
         return DeviceBatch(plan, bt, cu, sl, sm, wk, d["n_work"], d["n_combine"], d["ws_bytes"],
                            d["tile_cols"], int(d["n_slots"]), wk.data_ptr())
 
     def upload(self, plan: BatchPlan, stream=None) -> DeviceBatch:
+        """The metadata of a plan() result to the device, copied on `stream`."""
         import torch
+        ts = self._torch_stream(stream)
         ap = attention_plan(plan.cu_q, plan.seq_lens, self.hq, self.hkv, self.d, self.num_cus)
         parts = [plan.block_tables.ravel(), plan.cu_q, plan.seq_lens, plan.slot_mapping, ap.work.ravel()]
         n_int = sum(p.size for p in parts)
@@ -126,17 +125,14 @@ class PrefillEngine:
         if self._stage[t] is None or self._stage[t].numel() < n_int:
             cap = max(n_int, 1 << 16) * 2
             self._stage[t] = torch.empty(cap, dtype=torch.int32, pin_memory=True)
-            self._dev_meta[t] = torch.empty(cap, dtype=torch.int32, device=self.device)
+            with torch.cuda.stream(ts):
+                self._dev_meta[t] = torch.empty(cap, dtype=torch.int32, device=self.device)
         host = self._stage[t].numpy()
         o = 0
         for p in parts:
             host[o:o + p.size] = p
             o += p.size
-        dev = self._dev_meta[t][:n_int]
-        dev.copy_(self._stage[t][:n_int], non_blocking=True)
-        ev = torch.cuda.Event()
-        ev.record()
-        self._stage_ev[t] = ev
+        dev = self._copy_meta(t, n_int, ts)
         n = plan.n_reqs
         o = 0
         bt = dev[o:o + plan.block_tables.size].view(n, plan.block_tables.shape[1]); o += plan.block_tables.size
@@ -144,20 +140,52 @@ class PrefillEngine:
         sl = dev[o:o + n]; o += n
         sm = dev[o:o + len(plan.slot_mapping)]; o += len(plan.slot_mapping)
         wk = dev[o:o + ap.work.size].view(-1, 8)
-        if ap.ws_bytes > self._ws.numel():
-            self._ws = torch.empty(ap.ws_bytes, dtype=torch.uint8, device=self.device)
+        self._ensure_ws(ap.ws_bytes, ts)
         return DeviceBatch(plan, bt, cu, sl, sm, wk, ap.n_work, ap.n_combine, ap.ws_bytes, ap.tile_cols,
                            int(plan.cu_q[-1]), wk.data_ptr())
+
+    # ---- streams ---------------------------------------------------------------------------
+    # `stream` is None (torch's current stream), a torch.cuda.Stream or a raw hipStream_t
+    # handle.  The metadata copy, its event and every (re)allocation of a device buffer run on
+    # that stream, the stream the kernels then run on: the kernels are ordered after the copy,
+    # and the caching allocator hands out a replaced buffer's memory again only in that
+    # stream's order, after the kernels that read it.
+    def _torch_stream(self, stream):
+        import torch
+        if stream is None:
+            return torch.cuda.current_stream(self.device)
+        if isinstance(stream, torch.cuda.Stream):
+            return stream
+        return torch.cuda.ExternalStream(int(stream), device=self.device)
+
+    def _stream(self, stream):
+        if stream is None:
+            import torch
+            return torch.cuda.current_stream(self.device).cuda_stream
+        return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+    def _copy_meta(self, t: int, n_int: int, ts):
+        """Staging buffer t -> its device buffer on stream ts; the event marks the copy done, so
+        that the host refills the staging buffer only after the copy has read it."""
+        import torch
+        dev = self._dev_meta[t][:n_int]
+        with torch.cuda.stream(ts):
+            dev.copy_(self._stage[t][:n_int], non_blocking=True)
+            ev = torch.cuda.Event()
+            ev.record(ts)
+        self._stage_ev[t] = ev
+        return dev
+
+    def _ensure_ws(self, nbytes: int, ts):
+        if nbytes > self._ws.numel():
+            import torch
+            with torch.cuda.stream(ts):
+                self._ws = torch.empty(nbytes, dtype=torch.uint8, device=self.device)
 
     # ---- device steps --------------------------------------------------------------------
     # The engine built every device buffer itself, so these calls skip the binding's per-call
     # tensor checks and pass raw addresses straight to the C ABI (the library still validates
     # sizes); they only check the shapes of the caller's q / k / v / out.
-    def _stream(self, stream):
-        if stream is not None:
-            return int(stream)
-        import torch
-        return torch.cuda.current_stream(self.device).cuda_stream
 
     def scatter(self, db: DeviceBatch, k_new, v_new, stream=None):
         shape = (db.n_tokens, self.hkv, self.d)
@@ -184,7 +212,8 @@ class PrefillEngine:
                 raise ValueError("q / k_new / v_new must be contiguous 16-bit [n_tokens, heads, D]")
         need = 2 * t * n_out
         if self._y is None or self._y.numel() < need:
-            self._y = torch.empty(max(need, 1), dtype=torch.uint8, device=self.device)
+            with torch.cuda.stream(self._torch_stream(stream)):
+                self._y = torch.empty(max(need, 1), dtype=torch.uint8, device=self.device)
         _lib.check(lib().arckv_qkv_rope(x.data_ptr(), w_qkv.data_ptr(), t, h, self.hq, self.hkv, self.d,
                                         db.cu_q.data_ptr(), db.seq_lens.data_ptr(), db.plan.n_reqs,
                                         float(rope_theta), self._y.data_ptr(), self._y.numel(),
@@ -210,17 +239,20 @@ class PrefillEngine:
             _lib.check(lib().arckv_prefill_attention_timed(*args, *(e.cuda_event for e in events)),
                        "arckv_prefill_attention_timed")
 
-    def step(self, token_lists, qkv_for_plan, stream=None):
-        """One batch: plan, upload, scatter, attend, release.  qkv_for_plan(plan) returns the
-        computed tokens' (q, k_new, v_new) device tensors.  Returns (plan, out)."""
+    def step(self, token_lists, qkv_for_plan, stream=None, release: bool = True):
+        """One batch: plan, upload, scatter, attend, release (release=False: the caller calls
+        release()).  qkv_for_plan(plan) returns the computed tokens' (q, k_new, v_new) device
+        tensors, ready on `stream`.  Returns (plan, out), out allocated on `stream`."""
         import torch
         db = self.prepare(token_lists, stream)
         plan = db.plan
         try:
             q, k_new, v_new = qkv_for_plan(plan)
-            out = torch.empty_like(q)
+            with torch.cuda.stream(self._torch_stream(stream)):
+                out = torch.empty_like(q)
             self.scatter(db, k_new, v_new, stream)
             self.attention(db, q, out, stream)
         finally:
-            self.release()
+            if release:
+                self.release()
         return plan, out

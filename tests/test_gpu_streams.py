@@ -49,23 +49,31 @@ class StreamRun:
         self.hit_tokens = 0
         self.rows_checked = 0
 
-    def batch(self, reqs, rng=None):
+    def batch(self, reqs, rng=None, side=None, busy=None):
+        """side: run the engine's whole step (copy, scatter, attention) on this stream, after
+        queueing `busy()` (long work) on torch's default stream."""
         cfg = self.cfg
         toks = [r.tokens for r in reqs]
         oplan = self.orc.plan_batch(list(zip(obh.hash_blocks_many(toks), map(len, toks))))
-        db = self.eng.prepare(toks)          # hash + plan + work plan in one native call
-        plan = db.plan
+        q, kn, vn = self.bank.batch_suffix(reqs, oplan.prefix_lens)
+        if side is None:
+            db = self.eng.prepare(toks)          # hash + plan + work plan in one native call
+            plan = db.plan
+            out = torch.empty_like(q)
+            self.eng.scatter(db, kn, vn)
+            self.eng.attention(db, q, out)
+        else:
+            side.wait_stream(torch.cuda.current_stream())      # q / k / v were made on the default stream
+            busy()
+            plan, out = self.eng.step(toks, lambda p: (q, kn, vn), stream=side, release=False)
+            side.synchronize()
+        torch.cuda.synchronize()
         assert plan.prefix_lens.tolist() == oplan.prefix_lens
         assert plan.slot_mapping.tolist() == oplan.slot_mapping
         assert plan.cu_q.tolist() == oplan.cu_q
         for r, row in enumerate(oplan.block_tables):
             assert plan.block_tables[r, : len(row)].tolist() == row
         self.hit_tokens += sum(oplan.prefix_lens)
-        q, kn, vn = self.bank.batch_suffix(reqs, oplan.prefix_lens)
-        out = torch.empty_like(q)
-        self.eng.scatter(db, kn, vn)
-        self.eng.attention(db, q, out)
-        torch.cuda.synchronize()
         if rng is not None:
             for r, req in enumerate(reqs):
                 L, P = req.n_tokens, oplan.prefix_lens[r]
@@ -114,3 +122,28 @@ def test_trace_replay_window():
     print(f"trace: {n} batches, hit tokens {run.hit_tokens}, rows checked {run.rows_checked}", flush=True)
     # the window runs past the point where the cache is full, so evicted blocks are reused
     assert run.orc.cache.log and any(e.evicted_from for e in run.orc.cache.log)
+
+
+def test_step_on_a_side_stream_while_the_default_stream_is_busy():
+    """The engine's step on a non-default stream: the metadata copy must be ordered before the
+    kernels on that stream, not on torch's default stream, which here is held busy by a chain
+    of large matmuls queued just before each step (a copy queued behind them would let the
+    kernels read the block tables and slots of a batch four ring turns earlier)."""
+    base = get_config("multiturn")
+    reqs, cap = stream_multiturn(base)
+    cfg = sized(base, cap)
+    print_case(f"config multiturn on a side stream: first 10 batches, every batch checked")
+    run = StreamRun(cfg, 96)
+    side = torch.cuda.Stream()
+    m = torch.randn(4096, 4096, device=DEV)
+
+    def busy():
+        for _ in range(6):
+            torch.mm(m, m)
+
+    rng = np.random.default_rng(17)
+    batches = form_batches([r.n_tokens for r in reqs], cfg.max_batch, cfg.capacity, cfg.scratch)[:10]
+    for a, b in batches:
+        run.batch(reqs[a:b], rng, side=side, busy=busy)
+    print(f"side stream: {len(batches)} batches, rows checked {run.rows_checked}", flush=True)
+    assert run.rows_checked > 0 and run.hit_tokens > 0
