@@ -1,16 +1,17 @@
 #!/usr/bin/env python3
 """Benchmark: prefix-cached prefill attention + KV scatter under an ARC block cache, one MI355X.
 
-Default workload, `docqa` (document QA on a Llama-3-8B-shaped attention layer): 32 query /
-8 KV heads, head_dim 128, 16-token blocks, bf16 Q/K/V ~ N(0, 1).  A stream of batches of 8
-requests, each an 8192-token document drawn Zipf(1.1) from 64 seeded documents plus a fresh
-128-token question; the KV pool holds 25 % of all document tokens (8192 blocks); the host ARC
-cache decides which prefix blocks hit.  Warm-up steps also warm the cache (the stream
-continues across warm-up and timed steps).
+Default workload, `longctx` (long-context QA on a 70B-shaped attention layer, the largest
+configuration that fits one GPU): 64 query / 8 KV heads, head_dim 128, 16-token blocks, bf16
+Q/K/V ~ N(0, 1); 4 requests per batch, each a 32768-token document cached (ARC hits, its 2048
+blocks scattered over a 16384-block pool by a seeded free order) plus a fresh 2048-token suffix.
 
-Other workloads (`--workload`): `docqa_hit` (8 cached 8192-token documents + fresh 128-token
-questions), `longctx` (70B-shaped layer, 64/8 heads: 4 cached 32768-token documents + fresh
-2048-token suffixes), `short32|short48|short64` (16 sessions per batch adding S new tokens to
+Other workloads (`--workload`): `docqa` (document QA on a Llama-3-8B-shaped layer, 32 / 8
+heads: batches of 8 requests, each an 8192-token document drawn Zipf(1.1) from 64 seeded
+documents plus a fresh 128-token question; the KV pool holds 25 % of the document tokens and the
+host ARC cache decides which prefix blocks hit; warm-up steps also warm the cache),
+`docqa_hit` (8 cached 8192-token documents + fresh 128-token questions),
+`short32|short48|short64` (16 sessions per batch adding S new tokens to
 fully cached lognormal histories; KV-read bound), `decode` (64 sessions per batch adding one
 token each to fully cached lognormal histories, rotating over 256 sessions), `docqa14b`
 (the docqa stream on a Qwen3-14B-shaped layer, 40 / 8 heads, hidden 5120, with the Q/K/V
@@ -26,8 +27,9 @@ plan and the attention work plan -> metadata H2D -> [Q/K/V projection, docqa14b]
 scatter -> prefill attention (+ split combine) -> release.  Each batch's computed-token Q/K/V are staged in
 HBM before the timed region (token ids stay on the host).  Printed: one JSON line with the
 algorithmic attention TFLOP/s over the whole step time (value), suffix tokens/s, the roofline
-of the attention kernel measured with HIP events on its stream, and the CPU oracle timed on a
-bounded sample.
+of the attention kernel measured with HIP events on its stream, the CPU oracle timed on a
+bounded sample, and (`policy_baseline`) the pure-Python ARC and LRU planners of the oracle
+against the library's planner over the trace-replay stream's block references.
 """
 
 from __future__ import annotations
@@ -46,7 +48,7 @@ sys.path.insert(0, ROOT)
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA (published)
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E (published)
 
-DEFAULT_STEPS = {"docqa": (48, 16), "docqa14b": (48, 16), "docqa_hit": (20, 3), "longctx": (8, 2), "short32": (40, 4),
+DEFAULT_STEPS = {"docqa": (48, 16), "docqa14b": (48, 16), "docqa_hit": (20, 3), "longctx": (20, 3), "short32": (40, 4),
                  "short48": (40, 4), "short64": (40, 4), "decode": (40, 4), "multiturn": (None, None),
                  "trace": (40, None)}
 
@@ -86,15 +88,26 @@ def measured_traffic(workload: str):
         return None
 
 
-def cpu_baseline(cfg, sample, budget_s: float):
-    """Times the fp64 oracle on query rows of staged batches (bounded by budget_s seconds)."""
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(cfg, sample, budget_s: float, chunk: int = 64):
+    """Times the fp64 oracle on query rows of staged batches (bounded by budget_s seconds),
+    `chunk` suffix rows per oracle call."""
     from oracle import attention as oatt
     rows_done, flops, t_used = 0, 0.0, 0.0
     hq, d = cfg.num_q_heads, cfg.head_dim
     for (q_bits, k_bits, v_bits, P) in sample:
         S = q_bits.shape[0]
-        for r0 in range(0, S, 16):
-            rows = np.arange(r0, min(S, r0 + 16))
+        for r0 in range(0, S, chunk):
+            rows = np.arange(r0, min(S, r0 + chunk))
             t = time.perf_counter()
             oatt.request_attention(q_bits, k_bits, v_bits, P, cfg.scale, rows=rows)
             t_used += time.perf_counter() - t
@@ -103,6 +116,72 @@ def cpu_baseline(cfg, sample, budget_s: float):
             if t_used >= budget_s:
                 return rows_done, flops, t_used
     return rows_done, flops, t_used
+
+
+def policy_baseline(sample_requests: int):
+    """The oracle's pure-Python ARC and LRU planners (one core, the interpreter's) against the
+    library's planner (arckv_plan_batch) over the trace-replay stream (10,000 requests over 500
+    Zipf(1.1) documents + 30 % one-off documents, cache 20 % of the recurring documents, batches
+    of <= 16 within the capacity).  The Python planners run on the first `sample_requests`
+    requests, with block hashes from the oracle's hash (untimed); the library hashes the whole
+    stream itself (timed apart) and plans the same sample and the whole stream.  The hashes and
+    the hit decisions on the sample must agree."""
+    import paper_2606_21238_amd as ak
+    from oracle import blockhash as obh
+    from oracle.planner import Planner, form_batches
+    from workloads import get_config
+    from workloads import streams as st
+    base = get_config("trace")
+    reqs, cap = st.stream_trace(base)
+    cfg = st.sized(base, cap)
+    order = st.free_order(cfg.seed, cfg.num_phys)
+    lens = [r.n_tokens for r in reqs]
+    batches = form_batches(lens, cfg.max_batch, cfg.capacity, cfg.scratch)
+    n_sample = next((j for a, j in batches if j >= sample_requests), len(reqs))
+    t = time.perf_counter()
+    hashes = ak.hash_blocks_batch([r.tokens for r in reqs])
+    t_hash = time.perf_counter() - t
+    hl = obh.hash_blocks_many([r.tokens for r in reqs[:n_sample]])
+    hashes_match = all(h.tolist() == o for h, o in zip(hashes[:n_sample], hl))
+    refs_all = int(sum(len(h) for h in hashes))
+    refs_sample = int(sum(len(h) for h in hashes[:n_sample]))
+    out = {"stream": f"trace replay: {len(reqs)} requests, {refs_all} block references, capacity {cap} blocks",
+           "python_sample_requests": n_sample, "python_sample_references": refs_sample,
+           "python_cores": 1, "cpu_model": cpu_model(),
+           "library_hash_s_whole_stream": round(t_hash, 4), "hashes_match_on_sample": hashes_match}
+    for pol in ("arc", "lru"):
+        pl = Planner(pol, cfg.capacity, cfg.num_phys, cfg.scratch, order)
+        py_hits = []
+        t = time.perf_counter()
+        for a, b in batches:
+            if a >= n_sample:
+                break
+            py_hits += pl.plan_batch([(hl[i], lens[i]) for i in range(a, b)]).hit_blocks
+            pl.release_batch()
+        t_py = time.perf_counter() - t
+        lib = ak.BlockCache(pol, cfg.capacity, cfg.num_phys, cfg.scratch, order)
+        lib_hits, t_lib_sample = [], 0.0
+        t = time.perf_counter()
+        for a, b in batches:
+            p = lib.plan_batch([(hashes[i], lens[i]) for i in range(a, b)])
+            lib.release_batch()
+            if b <= n_sample:
+                lib_hits += p.hit_blocks.tolist()
+                t_lib_sample = time.perf_counter() - t
+        t_lib = time.perf_counter() - t
+        st_lib = lib.stats()
+        out[pol] = {
+            "python_s_sample": round(t_py, 3),
+            "python_refs_per_s": round(refs_sample / t_py, 1),
+            "python_s_whole_stream_extrapolated": round(t_py * refs_all / refs_sample, 1),
+            "library_s_sample": round(t_lib_sample, 4),
+            "library_s_whole_stream": round(t_lib, 4),
+            "library_refs_per_s": round(refs_all / t_lib, 1),
+            "speedup_on_sample": round(t_py / max(t_lib_sample, 1e-9), 1),
+            "hit_decisions_match_on_sample": py_hits == lib_hits,
+            "hit_rate_whole_stream": round(st_lib["prefix_hit_tokens"] / st_lib["prompt_tokens"], 4),
+        }
+    return out
 
 
 def split_stream(reqs, cfg, warm_requests: int):
@@ -194,12 +273,14 @@ def make_workload(name: str, steps, warmup):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--workload", default="docqa", choices=sorted(DEFAULT_STEPS))
+    ap.add_argument("--workload", default="longctx", choices=sorted(DEFAULT_STEPS))
     ap.add_argument("--steps", type=int, default=None)
     ap.add_argument("--warmup", type=int, default=None)
     ap.add_argument("--policy", default="arc", choices=["arc", "lru", "dbl"])
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle CPU time")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--policy-sample", type=int, default=1200,
+                    help="requests of the trace stream the Python planners run on (0: no policy baseline)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="run one plain copy kernel of this size first (scales HBM traffic counters)")
     args = ap.parse_args()
@@ -484,12 +565,16 @@ def main():
                         or [1])
         except Exception:
             cores = len(os.sched_getaffinity(0))
+        rate = fl / tcpu
         result["cpu_baseline"] = {
-            "value": round(fl / tcpu / 1e12, 6), "unit": "TFLOP/s",
-            "cores": int(cores), "kind": "oracle",
+            "value": round(rate / 1e12, 6), "unit": "TFLOP/s",
+            "cores": int(cores), "kind": "oracle", "cpu_model": cpu_model(),
             "sample": f"{rows} suffix query rows (all {hq} heads) of the first timed batch, fp64 numpy "
                       f"oracle, {tcpu:.1f} s",
+            "step_s_extrapolated": round(float(F[0]) / rate, 1),
         }
+    if args.policy_sample > 0 and args.workload in ("longctx", "trace"):
+        result["policy_baseline"] = policy_baseline(args.policy_sample)
     print(json.dumps(result))
 
 
