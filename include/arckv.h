@@ -45,6 +45,8 @@ extern "C" {
 
 #define ARCKV_BLOCK_TOKENS 16
 #define ARCKV_LAYOUT_V1 1
+/* largest planned workspace arckv_prefill_attention_noalloc accepts (its static scratch) */
+#define ARCKV_NOALLOC_MAX_WS_BYTES (64LL << 20)
 
 /* status codes */
 #define ARCKV_OK 0
@@ -344,6 +346,23 @@ int32_t arckv_prefill_attention_timed(const void* k_pool, const void* v_pool, co
                                       int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
                                       float scale, void* workspace, int64_t ws_bytes, void* stream,
                                       void* ev_begin, void* ev_mid, void* ev_end);
+
+/* For callers that cannot allocate device memory (code under HIP graph capture, serving
+ * loops or harnesses that forbid hipMalloc): arckv_prefill_attention with no workspace
+ * argument.  ws_bytes is the plan's workspace size (arckv_attention_plan / arckv_batch); the
+ * split partials go to a static device array of ARCKV_NOALLOC_MAX_WS_BYTES (64 MiB) per device,
+ * held until the process ends, found on this call's first use of the stream's device.  Nothing
+ * is allocated or freed.  Every call on one device shares that array: calls that overlap in
+ * time on one device race (serialise them, e.g. on one stream).  Other arguments, results and
+ * errors as arckv_prefill_attention; ENOSPC if ws_bytes > ARCKV_NOALLOC_MAX_WS_BYTES. */
+int32_t arckv_prefill_attention_noalloc(const void* k_pool, const void* v_pool, const void* q,
+                                        void* out, const int32_t* block_tables, int32_t bt_stride,
+                                        const int32_t* cu_q, const int32_t* seq_lens,
+                                        int32_t n_reqs, int64_t n_q, int64_t num_blocks,
+                                        const int32_t* work, int64_t n_work, int64_t n_combine,
+                                        int32_t tile_cols, int32_t num_q_heads,
+                                        int32_t num_kv_heads, int32_t head_dim, float scale,
+                                        int64_t ws_bytes, void* stream);
 
 /* ---------------------------------------------------------------------------------------
  * Device: the producer of the computed tokens' Q/K/V (the attention inputs of a prefill;

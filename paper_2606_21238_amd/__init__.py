@@ -18,6 +18,7 @@ from . import _lib
 from ._lib import ArckvError, SYMBOLS, WORK_INTS  # noqa: F401
 
 BLOCK_TOKENS = 16
+NOALLOC_MAX_WS_BYTES = 64 << 20     # ARCKV_NOALLOC_MAX_WS_BYTES: the static scratch of prefill_attention_noalloc
 LIST_T1, LIST_T2, LIST_B1, LIST_B2 = 1, 2, 3, 4
 
 
@@ -362,11 +363,9 @@ def unpack_prepared(packed: np.ndarray, d: dict, prefix_lens, hit_blocks):
     return plan, AttnPlan(work, d["n_work"], d["n_combine"], d["ws_bytes"], d["tile_cols"])
 
 
-def prefill_attention(k_pool, v_pool, q, out, block_tables, cu_q, seq_lens, work, n_work: int,
-                      n_combine: int, tile_cols: int, scale: float, workspace=None, ws_bytes: int = 0,
-                      stream=None):
-    """Device tensors: pools (layout V1), q/out [n_q, Hq, D] bf16, block_tables [n, stride] int32,
-    cu_q [n+1], seq_lens [n], work [n_work + n_combine, 8] int32, workspace (bytes >= ws_bytes)."""
+def _attention_args(k_pool, v_pool, q, out, block_tables, cu_q, seq_lens, work, n_work: int,
+                    n_combine: int, tile_cols: int, scale: float):
+    """Checked C arguments of the attention calls, up to (excluding) the workspace."""
     n_q, hq, d = int(q.shape[0]), int(q.shape[1]), int(q.shape[2])
     nb, hkv = int(k_pool.shape[0]), int(k_pool.shape[1])
     n_reqs = int(seq_lens.shape[0])
@@ -378,13 +377,32 @@ def prefill_attention(k_pool, v_pool, q, out, block_tables, cu_q, seq_lens, work
         raise ValueError("block_tables must be [n_reqs, stride] and cu_q [n_reqs + 1]")
     if work.dim() != 2 or int(work.shape[1]) != WORK_INTS or int(work.shape[0]) < n_work + n_combine:
         raise ValueError("work must be [>= n_work + n_combine, 8]")
+    return (_dev(k_pool, 16, "k_pool"), _dev(v_pool, 16, "v_pool"), _dev(q, 16, "q"), _dev(out, 16, "out"),
+            _dev(block_tables, 32, "block_tables"), int(block_tables.shape[1]), _dev(cu_q, 32, "cu_q"),
+            _dev(seq_lens, 32, "seq_lens"), n_reqs, n_q, nb, _dev(work, 32, "work"), n_work, n_combine,
+            int(tile_cols), hq, hkv, d, float(scale))
+
+
+def prefill_attention(k_pool, v_pool, q, out, block_tables, cu_q, seq_lens, work, n_work: int,
+                      n_combine: int, tile_cols: int, scale: float, workspace=None, ws_bytes: int = 0,
+                      stream=None):
+    """Device tensors: pools (layout V1), q/out [n_q, Hq, D] bf16, block_tables [n, stride] int32,
+    cu_q [n+1], seq_lens [n], work [n_work + n_combine, 8] int32, workspace (bytes >= ws_bytes)."""
+    args = _attention_args(k_pool, v_pool, q, out, block_tables, cu_q, seq_lens, work, n_work, n_combine,
+                           tile_cols, scale)
     if ws_bytes and (workspace is None or workspace.numel() * workspace.element_size() < ws_bytes):
         raise ValueError("workspace smaller than ws_bytes")
     ws = C.c_void_p(0) if workspace is None else _dev(workspace, None, "workspace")
-    _lib.check(lib().arckv_prefill_attention(
-        _dev(k_pool, 16, "k_pool"), _dev(v_pool, 16, "v_pool"), _dev(q, 16, "q"), _dev(out, 16, "out"),
-        _dev(block_tables, 32, "block_tables"), int(block_tables.shape[1]), _dev(cu_q, 32, "cu_q"),
-        _dev(seq_lens, 32, "seq_lens"), int(seq_lens.shape[0]), n_q, int(k_pool.shape[0]),
-        _dev(work, 32, "work"), n_work, n_combine, int(tile_cols), hq, hkv, d, float(scale), ws,
-        int(ws_bytes),
-        C.c_void_p(_stream(stream))), "arckv_prefill_attention")
+    _lib.check(lib().arckv_prefill_attention(*args, ws, int(ws_bytes), C.c_void_p(_stream(stream))),
+               "arckv_prefill_attention")
+
+
+def prefill_attention_noalloc(k_pool, v_pool, q, out, block_tables, cu_q, seq_lens, work, n_work: int,
+                              n_combine: int, tile_cols: int, scale: float, ws_bytes: int = 0, stream=None):
+    """prefill_attention without a workspace: the library's static per-device scratch holds the
+    split partials (ws_bytes: the plan's size, at most NOALLOC_MAX_WS_BYTES).  Calls that overlap
+    in time on one device must not be issued (they share the scratch)."""
+    args = _attention_args(k_pool, v_pool, q, out, block_tables, cu_q, seq_lens, work, n_work, n_combine,
+                           tile_cols, scale)
+    _lib.check(lib().arckv_prefill_attention_noalloc(*args, int(ws_bytes), C.c_void_p(_stream(stream))),
+               "arckv_prefill_attention_noalloc")

@@ -80,6 +80,8 @@ _SIGS = {
                                       i32, i32, i32, i32, f32, vp, i64, vp]),
     "arckv_prefill_attention_timed": (i32, [vp, vp, vp, vp, vp, i32, vp, vp, i32, i64, i64, vp, i64,
                                             i64, i32, i32, i32, i32, f32, vp, i64, vp, vp, vp, vp]),
+    "arckv_prefill_attention_noalloc": (i32, [vp, vp, vp, vp, vp, i32, vp, vp, i32, i64, i64, vp, i64,
+                                              i64, i32, i32, i32, i32, f32, i64, vp]),
 }
 
 SYMBOLS = tuple(_SIGS)

@@ -37,6 +37,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cmath>
+#include <mutex>
 #include <type_traits>
 
 #include "../host/internal.hpp"
@@ -812,4 +813,72 @@ extern "C" int32_t arckv_prefill_attention_timed(
                            num_kv_heads, head_dim, scale, workspace, ws_bytes, stream,
                            static_cast<hipEvent_t>(ev_begin), static_cast<hipEvent_t>(ev_mid),
                            static_cast<hipEvent_t>(ev_end));
+}
+
+// ---- the entry point that allocates nothing -------------------------------------------------
+// The split pieces' partials go to a file-scope device array instead of a caller workspace.
+// Each device holds its own copy (for as long as the process runs); its address is looked up
+// once per device with hipGetSymbolAddress, with that device current, and kept: in host code
+// the array's name is only a host-side stand-in, never a device address.  Every call on one
+// device shares that device's copy, so calls that overlap in time on one device race.  Nothing
+// in it needs clearing: every split piece writes its own slot before the combine reads it.
+namespace {
+
+constexpr int64_t kStaticScratchBytes = ARCKV_NOALLOC_MAX_WS_BYTES;
+static_assert(kStaticScratchBytes % 256 == 0, "scratch size");
+static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// Address of `scratch` on the device the stream belongs to (the current device for the null
+// stream), looked up on the first call for that device.
+int32_t device_scratch(hipStream_t st, void** ptr) {
+  int cur = -1;
+  if (hipGetDevice(&cur) != hipSuccess)
+    return arckv::fail(ARCKV_EDEVICE, "prefill_attention_noalloc: hipGetDevice failed");
+  int dev = cur;
+  if (st != nullptr && hipStreamGetDevice(st, &dev) != hipSuccess)
+    return arckv::fail(ARCKV_EDEVICE, "prefill_attention_noalloc: hipStreamGetDevice failed");
+  if (dev < 0 || dev >= kMaxDevices)
+    return arckv::fail(ARCKV_EUNSUPPORTED, "prefill_attention_noalloc: device %d >= %d", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    if (dev != cur && hipSetDevice(dev) != hipSuccess)
+      return arckv::fail(ARCKV_EDEVICE, "prefill_attention_noalloc: hipSetDevice(%d) failed", dev);
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (dev != cur) (void)hipSetDevice(cur);
+    if (e != hipSuccess || p == nullptr)
+      return arckv::fail(ARCKV_EDEVICE, "prefill_attention_noalloc: hipGetSymbolAddress: %s",
+                         hipGetErrorString(e));
+    g_scratch_ptr[dev] = p;
+  }
+  *ptr = g_scratch_ptr[dev];
+  return ARCKV_OK;
+}
+
+}  // namespace
+
+extern "C" int32_t arckv_prefill_attention_noalloc(
+    const void* k_pool, const void* v_pool, const void* q, void* out, const int32_t* block_tables,
+    int32_t bt_stride, const int32_t* cu_q, const int32_t* seq_lens, int32_t n_reqs, int64_t n_q,
+    int64_t num_blocks, const int32_t* work, int64_t n_work, int64_t n_combine, int32_t tile_cols,
+    int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim, float scale, int64_t ws_bytes,
+    void* stream) {
+  if (ws_bytes < 0 || ws_bytes > kStaticScratchBytes)
+    return arckv::fail(ARCKV_ENOSPC,
+                       "prefill_attention_noalloc: the plan needs %lld bytes of workspace; the static "
+                       "scratch holds %lld",
+                       static_cast<long long>(ws_bytes), static_cast<long long>(kStaticScratchBytes));
+  void* ws = nullptr;
+  if (ws_bytes > 0) {
+    const int32_t rc = device_scratch(static_cast<hipStream_t>(stream), &ws);
+    if (rc != ARCKV_OK) return rc;
+  }
+  return prefill_attention(k_pool, v_pool, q, out, block_tables, bt_stride, cu_q, seq_lens, n_reqs,
+                           n_q, num_blocks, work, n_work, n_combine, tile_cols, num_q_heads,
+                           num_kv_heads, head_dim, scale, ws, ws_bytes, stream, nullptr, nullptr,
+                           nullptr);
 }
