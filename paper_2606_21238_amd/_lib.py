@@ -97,11 +97,13 @@ class ArckvError(RuntimeError):
 
 
 def load(path: str | None = None):
-    """Loads libarckv.so (built in-tree).  Raises if it has not been built: there is no fallback."""
+    """Loads libarckv.so (built in-tree; the environment variable ARCKV_LIBRARY names another
+    build of it, e.g. the sanitizer build of the host code).  Raises if it has not been built:
+    there is no fallback."""
     global _lib
     if _lib is not None and path is None:
         return _lib
-    p = path or LIB_PATH
+    p = path or os.environ.get("ARCKV_LIBRARY") or LIB_PATH
     try:
         # torch ships its own libamdhip64.so.7; loading it first makes libarckv bind to that same
         # runtime (one HIP runtime per process; two copies do not share devices or streams)

@@ -42,19 +42,31 @@ def _run(cmd):
     return out
 
 
-def build(verbose: bool = False) -> str:
-    os.makedirs(BUILD, exist_ok=True)
+SANITIZE = ["-fsanitize=address,undefined", "-fno-sanitize-recover=undefined", "-fno-omit-frame-pointer"]
+ASAN_BUILD = os.path.join(PKG, "_build_sanitize")
+ASAN_LIB = os.path.join(LIBDIR, "libarckv_sanitize.so")
+
+
+def build(verbose: bool = False, sanitize: bool = False) -> str:
+    """sanitize: the host C++ (hashing, cache, planner, batch preparation) instrumented with
+    AddressSanitizer and UndefinedBehaviorSanitizer, into lib/libarckv_sanitize.so, for CPU tests
+    (load it with ARCKV_LIBRARY and the sanitizer runtimes preloaded).  The HIP sources are
+    built as usual, with no sanitizer: device code is never instrumented."""
+    build_dir = ASAN_BUILD if sanitize else BUILD
+    out_lib = ASAN_LIB if sanitize else LIB
+    os.makedirs(build_dir, exist_ok=True)
     os.makedirs(LIBDIR, exist_ok=True)
     hipcc = _hipcc()
     common = ["-O3", "-fPIC", "-std=c++17", "-Wall", f"-I{INCLUDE}", f"-I{os.path.join(CSRC, 'host')}"]
+    host_flags = ["-O1", "-g", *SANITIZE] if sanitize else []
     jobs = []
     objs = []
     for src in HOST_SRC:
-        obj = os.path.join(BUILD, os.path.basename(src) + ".o")
-        jobs.append(["g++", *common, "-c", os.path.join(CSRC, src), "-o", obj])
+        obj = os.path.join(build_dir, os.path.basename(src) + ".o")
+        jobs.append(["g++", *common, *host_flags, "-c", os.path.join(CSRC, src), "-o", obj])
         objs.append(obj)
     for src in HIP_SRC:
-        obj = os.path.join(BUILD, os.path.basename(src) + ".o")
+        obj = os.path.join(build_dir, os.path.basename(src) + ".o")
         jobs.append([hipcc, f"--offload-arch={ARCH}", *common,
                      # no packed fp32 VALU ops are ever generated: some of their forms have given wrong results on gfx950
                      "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
@@ -66,12 +78,17 @@ def build(verbose: bool = False) -> str:
         for o in outs:
             if o.strip():
                 print(o)
-    tmp = LIB + ".tmp"
-    # rocBLAS for the one plain GEMM (the Q/K/V projection)
-    _run([hipcc, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-lrocblas", "-o", tmp])
-    os.replace(tmp, LIB)
-    return LIB
+    tmp = out_lib + ".tmp"
+    if sanitize:
+        # linked by g++ (no HIP source on this line), with the sanitizer runtimes
+        _run(["g++", "-shared", "-fPIC", *SANITIZE, *objs, "-L/opt/rocm/lib", "-lamdhip64", "-lrocblas",
+              f"-Wl,-rpath,/opt/rocm/lib", "-o", tmp])
+    else:
+        # rocBLAS for the one plain GEMM (the Q/K/V projection)
+        _run([hipcc, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-lrocblas", "-o", tmp])
+    os.replace(tmp, out_lib)
+    return out_lib
 
 
 if __name__ == "__main__":
-    print(build(verbose="-v" in sys.argv))
+    print(build(verbose="-v" in sys.argv, sanitize="--sanitize" in sys.argv))
