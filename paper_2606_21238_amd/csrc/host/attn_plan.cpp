@@ -17,6 +17,9 @@
 // of all key tiles (e.g. one long history in a decode batch) is cut to that share, so that it
 // does not set the length of the launch.
 //
+// No item covers more than kMaxItemKeys keys (65536): a longer range is cut the same way, so the
+// attention kernel can hold an item's block-table entries in LDS.
+//
 // Items are ordered longest key range first so the longest ones start first, and the order
 // is interleaved over the 8 XCDs (work-groups are dispatched round-robin over XCDs, each with
 // its own L2): all tiles of one (request, KV head) group land on the same XCD, so the K/V
@@ -106,6 +109,7 @@ extern "C" int32_t arckv_attention_plan(const int32_t* cu_q, const int32_t* seq_
     } else {
       cap = share;  // several rounds: no item longer than one compute unit's share
     }
+    cap = std::min<int64_t>(cap, arckv::kMaxItemKeys / kKeyTile);
   }
 
   std::vector<Item> items, combines;

@@ -17,6 +17,9 @@ constexpr int kWaveCols = 32;
 constexpr int kWideCols = 8 * kWaveCols;
 constexpr int kNarrowCols = 4 * kWaveCols;
 constexpr int kTinyCols = kWaveCols;
+// Longest key range of one attention work item: longer ranges are split into pieces (merged by
+// the combine), so that the item's block-table entries (kMaxItemKeys / 16) fit in LDS.
+constexpr int kMaxItemKeys = 65536;
 
 // Records a thread-local message for arckv_last_error() and returns `code`.
 int32_t fail(int32_t code, const char* fmt, ...) __attribute__((format(printf, 2, 3)));

@@ -14,14 +14,19 @@ namespace {
 // Upper bound on work items + combine items of arckv_attention_plan for prompts of these
 // lengths: a tile is at most 256 columns of one (request, KV head), or one per (request, KV
 // head) when the batch uses narrower tiles (every request then fits one); key-range splits
-// add at most num_cus pieces; the XCD-phase padding of the ordered list at most multiplies
-// the pieces by the XCD count; there is at most one combine item per tile.
+// add at most num_cus pieces, or, where the cap on one item's keys (kMaxItemKeys) cuts finer,
+// at most ceil(L / kMaxItemKeys) pieces per tile of a request of L tokens; the XCD-phase
+// padding of the ordered list at most multiplies the pieces by the XCD count; there is at most
+// one combine item per tile.
 int64_t work_bound(const int64_t* n_tokens, int32_t n_reqs, int32_t G, int32_t hkv, int32_t num_cus) {
-  int64_t tiles = 0;
-  for (int32_t r = 0; r < n_reqs; ++r)
-    tiles += hkv * std::max<int64_t>(1, (n_tokens[r] * G + arckv::kWideCols - 1) / arckv::kWideCols);
+  int64_t tiles = 0, capped = 0;
+  for (int32_t r = 0; r < n_reqs; ++r) {
+    const int64_t t = hkv * std::max<int64_t>(1, (n_tokens[r] * G + arckv::kWideCols - 1) / arckv::kWideCols);
+    tiles += t;
+    capped += t * ((n_tokens[r] + arckv::kMaxItemKeys - 1) / arckv::kMaxItemKeys);
+  }
   constexpr int64_t kXcds = 8;
-  return kXcds * (tiles + num_cus) + tiles;
+  return kXcds * (tiles + num_cus + capped) + tiles;
 }
 
 // The common part: requests given as (hashes, n_tokens); `hashes[r]` holds n_tokens[r] / 16

@@ -545,6 +545,405 @@ __global__ __launch_bounds__(64 * NW, 1) void prefill_attn_kernel(
   }
 }
 
+// Wide tiles (256 columns, 8 waves of 32 columns), scheduled as a ping-pong.  Every wave runs
+// the same step on tile j as two halves:
+//   V(j): mask (diagonal tiles), column max, lazy rescale of O, exponentials -> P(j), row sums
+//   M(j): O += V(j) P(j)  (16 MFMAs), then S(j+1) = K(j+1) Q^T  (16 MFMAs)
+// Waves 0-3 run half a step ahead of waves 4-7 (a workgroup barrier ends every half step), and
+// waves w and w + 4 share a SIMD, so on every SIMD one wave's exponentials run while the other
+// wave's MFMAs do.  S is single-buffered (V(j) consumes S(j) before M(j) writes S(j+1)); the
+// registers this frees hold the LDS operands of the MFMA phase four MFMAs ahead of their use.
+//
+// Half steps are numbered globally: group 0 (waves 0-3) runs M(-1) = S(0) in half step 0, then
+// V(j) in 2j+1 and M(j) in 2j+2; group 1 runs the same one half step later.  Each wave issues
+// its pieces of tile t during its M(t-3) (tiles 0-2 before the loop), one load every few MFMAs
+// (half step 2t-4 for group 0, 2t-3 for group 1), and they must be complete by the end of half
+// step 2t-1, the barrier before tile t's first reader (group 0's M(t-1)).  They overwrite the
+// ring stage of tile t-4, whose last reader (group 1's M(t-4)) ran in half step 2t-5.  The block
+// numbers come from a copy of the item's block-table slice in LDS, read one tile ahead.
+template <int D, int G>
+__global__ __launch_bounds__(512, 1) void prefill_attn_pp_kernel(
+    const uint16_t* __restrict__ k_pool, const uint16_t* __restrict__ v_pool,
+    const uint16_t* __restrict__ q, uint16_t* __restrict__ out,
+    const int32_t* __restrict__ block_tables, int bt_stride,
+    const int32_t* __restrict__ cu_q, const int32_t* __restrict__ seq_lens, int n_reqs,
+    const Work* __restrict__ work, int64_t n_q, int64_t num_blocks, int hq, int hkv,
+    float scale_log2, float* __restrict__ ws_o, float* __restrict__ ws_lse, int64_t ws_slots) {
+  constexpr int kThreads = 512;
+  constexpr int kCols = arckv::kWideCols;
+  static_assert(kCols == 8 * 32, "8 waves of 32 columns");
+  constexpr int KSTEPS = D / 16;                 // k-steps of Q.K^T
+  constexpr int DM = D / 32;                     // 32-row blocks of O^T
+  constexpr int TILE = kBK * D * 2;              // bytes of one K (or V) tile
+  constexpr int NLD = TILE / (kThreads * 16);    // 16-byte direct loads per thread per tile
+  constexpr int LDB = kThreads * 16;             // bytes one load instruction moves per WG
+  constexpr int BLK_BYTES = 16 * D * 2;          // one block of one head, K or V
+  constexpr int NOP = 4 * DM + 2 * KSTEPS;       // MFMAs of a full M phase
+  constexpr int PD = 4;                          // LDS operands in flight ahead of their MFMA
+  static_assert(NLD >= 1 && TILE % LDB == 0, "tile must be a multiple of one WG-wide load");
+  constexpr int kTbl = arckv::kMaxItemKeys / 16;  // block-table entries of one work item
+  __shared__ __attribute__((aligned(1024))) char smem[kStages * 2 * TILE];  // stage s: K, then V
+  __shared__ int32_t tbl[kTbl];
+
+  const Work w = work[blockIdx.x];
+  if (w.req < 0 || w.req >= n_reqs || w.kvh < 0 || w.kvh >= hkv || w.col_start < 0) return;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int grp = wave >> 2;
+  const int l32 = lane & 31, hg = lane >> 5;
+  const int q0 = cu_q[w.req];
+  const int S = cu_q[w.req + 1] - q0;
+  const int L = seq_lens[w.req];
+  const int P = L - S;
+  const int ncols = S * G;
+  const int32_t* bt = block_tables + static_cast<int64_t>(w.req) * bt_stride;
+  const int nblk = min((L + 15) >> 4, bt_stride);
+
+  // ---- this lane's query column and its Q^T operands ------------------------------------
+  const int col = w.col_start + wave * 32 + l32;
+  const int tok = col / G, g = col % G;
+  const bool cval = col < ncols && (q0 + tok) < n_q;
+  const int pos = cval ? P + tok : -1;
+  bf16x8_t qf[KSTEPS];
+  {
+    const int64_t qrow = static_cast<int64_t>(q0 + tok) * hq + w.kvh * G + g;
+#pragma unroll
+    for (int ks = 0; ks < KSTEPS; ++ks)
+      qf[ks] = cval ? *reinterpret_cast<const bf16x8_t*>(q + qrow * D + ks * 16 + hg * 8) : bf16x8_t{};
+  }
+
+  const int last_col = min(w.col_start + kCols, ncols) - 1;
+  const int wg_max_pos = P + last_col / G;
+  const int wg_min_pos = P + w.col_start / G;
+  const int kv_lo = max(w.kv_start, 0);
+  const int kv_hi = min(w.kv_end, wg_max_pos + 1);
+  const int ntiles = kv_hi > kv_lo ? (kv_hi - kv_lo + kBK - 1) / kBK : 0;
+
+  // ---- direct global -> LDS tile loads (as in prefill_attn_kernel) -----------------------
+  int k_off[NLD], v_off[NLD], blk_of[NLD];
+#pragma unroll
+  for (int i = 0; i < NLD; ++i) {
+    const int posb = i * LDB + wave * 1024 + lane * 16;
+    const int r = posb / (2 * D), p = (posb % (2 * D)) / 16;
+    blk_of[i] = posb / BLK_BYTES;
+    k_off[i] = (r & 15) * D + ((p ^ fk<D>(r)) * 8);
+    const int qv = posb % BLK_BYTES, d = qv / 32, h = ((qv / 16) & 1) ^ sv(d);
+    v_off[i] = d * 16 + h * 8;
+  }
+  const int64_t head_k = static_cast<int64_t>(w.kvh) * 16 * D;
+  const int64_t blk_stride = static_cast<int64_t>(hkv) * 16 * D;
+  // The item's block-table entries (blocks b_lo .. b_lo + n_tbl - 1) are copied to LDS once:
+  // the loop then looks them up there.  Scalar loads of the table inside the loop would force
+  // a wait for the scalar memory round trip at every tile (and, while one is in flight, full
+  // waits on every LDS operand read, since scalar loads may return out of order).  The host
+  // plan keeps every item within kMaxItemKeys keys, so n_tbl <= kTbl.
+  const int b_lo = kv_lo >> 4;
+  const int n_tbl = max(0, min(min(nblk - b_lo, ntiles * (kBK / 16)), kTbl));
+  constexpr int kTblPer = kTbl / kThreads;
+  int32_t tbl_v[kTblPer];
+#pragma unroll
+  for (int k = 0; k < kTblPer; ++k) {
+    const int e = tid + k * kThreads;
+    tbl_v[k] = e < n_tbl ? bt[b_lo + e] : 0;
+  }
+  // Lane i < NLD of next_v holds the physical block of the next tile's piece i, looked up one
+  // tile ahead with a lane-dependent address (so it stays in a vector register and its LDS
+  // read has long returned when readlane takes it).
+  const int blk_lane = blk_of[lane % NLD];
+  int32_t next_v = 0;
+  auto fetch_next = [&](int tile) {
+    const int b = ((tile * kBK) >> 4) + blk_lane;   // relative to b_lo
+    next_v = b < n_tbl ? tbl[b] : 0;
+  };
+  auto issue = [&](int tile, const int32_t (&ph)[NLD]) {
+    char* st = smem + (tile % kStages) * 2 * TILE;
+#pragma unroll
+    for (int i = 0; i < NLD; ++i) {
+      const int32_t pb = (ph[i] < 0 || ph[i] >= num_blocks) ? 0 : ph[i];  // never used unmasked
+      const int64_t base = static_cast<int64_t>(pb) * blk_stride + head_k;
+      load_lds16(k_pool + base + k_off[i], (lds_void*)(st + i * LDB + wave * 1024));
+      load_lds16(v_pool + base + v_off[i], (lds_void*)(st + TILE + i * LDB + wave * 1024));
+    }
+  };
+  // tiles issued before the table is in LDS read their entries from the global table
+  auto load_tile_global = [&](int tile) {
+    int32_t ph[NLD];
+#pragma unroll
+    for (int i = 0; i < NLD; ++i) {
+      const int b = b_lo + ((tile * kBK) >> 4) + blk_of[i];
+      ph[i] = b < nblk ? bt[b] : 0;
+    }
+    issue(tile, ph);
+  };
+  auto load_tile = [&](int tile) {
+    int32_t ph[NLD];
+#pragma unroll
+    for (int i = 0; i < NLD; ++i) ph[i] = __builtin_amdgcn_readlane(next_v, i);
+    fetch_next(tile + 1);
+    issue(tile, ph);
+  };
+
+  f32x16_t o[DM];
+#pragma unroll
+  for (int md = 0; md < DM; ++md) o[md] = f32x16_t{};
+  f32x16_t sacc[2];                 // S^T of one tile: 2 blocks of 32 keys x this wave's columns
+  uint32_t pw[4][4];                // P^T operands: 4 blocks of 16 keys, bf16 pairs
+  float m_run = -INFINITY, l_run = 0.f;
+
+  // ---- V phase ----------------------------------------------------------------------------
+  // S^T register r of key block mb holds key t0 + 32 mb + 16 (r / 8) + 8 hg + r % 8
+  auto v_phase = [&](int j, auto masked) {
+    const int t0 = kv_lo + j * kBK;
+    if constexpr (decltype(masked)::value) {   // diagonal or prompt-end tile
+#pragma unroll
+      for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int key = t0 + mb * 32 + 16 * (r >> 3) + 8 * hg + (r & 7);
+          sacc[mb][r] = key > pos ? -INFINITY : sacc[mb][r];
+        }
+    }
+    float m = -INFINITY;
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) m = fmaxf(m, sacc[mb][r]);
+    const float mx = max_halves(m) * scale_log2;
+    const bool pending = __builtin_amdgcn_ballot_w64(mx > m_run + kLazy) != 0;   // wave-uniform
+    if (pending) {
+      const float m_new = fmaxf(m_run, mx);
+      const float alpha = m_new == -INFINITY ? 1.f : fast_exp2(m_run - m_new);
+      m_run = m_new;
+      l_run *= alpha;
+#pragma unroll
+      for (int md = 0; md < DM; ++md) o[md] *= alpha;
+    }
+    const float mu = m_run == -INFINITY ? 0.f : m_run;
+    float lsum = 0.f;
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+      for (int half = 0; half < 2; ++half)
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) {
+          const f32x2_t two = {fast_exp2(fmaf(sacc[mb][8 * half + 2 * jj], scale_log2, -mu)),
+                               fast_exp2(fmaf(sacc[mb][8 * half + 2 * jj + 1], scale_log2, -mu))};
+          lsum += two[0];
+          lsum += two[1];
+          pw[2 * mb + half][jj] = __builtin_bit_cast(uint32_t, __builtin_convertvector(two, bf16x2_t));
+        }
+    l_run += lsum;
+  };
+  // keys >= L of the last tile may hold stale bytes (even NaN patterns): zero their V in LDS
+  // (group 0 only, 256 threads; published by the barrier that ends the half step)
+  auto zero_v_tail = [&](int tile, int t0) {
+    uint16_t* vb = reinterpret_cast<uint16_t*>(smem + (tile % kStages) * 2 * TILE + TILE);
+    for (int e = tid; e < kBK * D; e += kThreads / 2) {
+      const int key = e & (kBK - 1), d = e / kBK;
+      if (t0 + key >= L) {
+        const int blk = key >> 4, kk = key & 15;
+        const int h = ((kk >> 3) ^ sv(d));
+        vb[(blk * BLK_BYTES + d * 32 + h * 16) / 2 + (kk & 7)] = 0;
+      }
+    }
+  };
+
+  // ---- M phase: operand n < 4 DM is V^T of (key block n / DM, dim block n % DM) for P.V;
+  // the rest are K rows of (k-step (n - 4 DM) / 2, key block n % 2) for S = K Q^T -----------
+  // with_load: this wave's 2 NLD direct loads of tile load_t are issued one every
+  // N / (2 NLD) MFMAs instead of back to back: all waves issuing theirs right after a barrier
+  // queue behind each other at the load unit (about 16 cycles per 1 KiB instruction).
+  auto m_phase = [&](int j, auto with_s, auto with_load, int load_t) {
+    constexpr bool WITH_S = decltype(with_s)::value;
+    constexpr bool WITH_LOAD = decltype(with_load)::value;
+    constexpr int N = WITH_S ? NOP : 4 * DM;
+    const char* vb = smem + (j % kStages) * 2 * TILE + TILE;
+    const char* kb = smem + ((j + 1) % kStages) * 2 * TILE;
+    const int vlane = l32 * 32 + ((hg ^ sv(l32)) * 16);          // sv(md * 32 + l32) == sv(l32)
+    auto op_at = [&](int n) -> bf16x8_t {
+      if (n < 4 * DM) {
+        const int sp = n / DM, md = n % DM;
+        return *reinterpret_cast<const bf16x8_t*>(vb + sp * BLK_BYTES + md * 1024 + vlane);
+      }
+      const int ks = (n - 4 * DM) / 2, mb = (n - 4 * DM) % 2;
+      const int r = mb * 32 + pi_row(l32);
+      const int c = 2 * ks + hg;
+      return *reinterpret_cast<const bf16x8_t*>(kb + r * 2 * D + ((c ^ fk<D>(r)) * 16));
+    };
+    const uint16_t* ld_src[2 * NLD];
+    lds_void* ld_dst[2 * NLD];
+    if constexpr (WITH_LOAD) {
+      char* st = smem + (load_t % kStages) * 2 * TILE;
+#pragma unroll
+      for (int i = 0; i < NLD; ++i) {
+        const int32_t ph = __builtin_amdgcn_readlane(next_v, i);
+        const int32_t pb = (ph < 0 || ph >= num_blocks) ? 0 : ph;  // never used unmasked
+        const int64_t base = static_cast<int64_t>(pb) * blk_stride + head_k;
+        ld_src[2 * i] = k_pool + base + k_off[i];
+        ld_dst[2 * i] = (lds_void*)(st + i * LDB + wave * 1024);
+        ld_src[2 * i + 1] = v_pool + base + v_off[i];
+        ld_dst[2 * i + 1] = (lds_void*)(st + TILE + i * LDB + wave * 1024);
+      }
+      fetch_next(load_t + 1);
+    }
+    constexpr int LD_EVERY = N / (2 * NLD);
+    bf16x8_t opv[N];
+#pragma unroll
+    for (int n = 0; n < PD; ++n) opv[n] = op_at(n);
+#pragma unroll
+    for (int n = 0; n < N; ++n) {
+      if constexpr (WITH_LOAD)
+        if (n % LD_EVERY == LD_EVERY / 2) load_lds16(ld_src[n / LD_EVERY], ld_dst[n / LD_EVERY]);
+      if (n + PD < N) opv[n + PD] = op_at(n + PD);
+      if (n < 4 * DM) {
+        const int sp = n / DM, md = n % DM;
+        const u32x4_t w4 = {pw[sp][0], pw[sp][1], pw[sp][2], pw[sp][3]};
+        o[md] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(opv[n], __builtin_bit_cast(bf16x8_t, w4), o[md], 0, 0, 0);
+      } else {
+        const int ks = (n - 4 * DM) / 2, mb = (n - 4 * DM) % 2;
+        sacc[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(opv[n], qf[ks], ks == 0 ? f32x16_t{} : sacc[mb], 0, 0, 0);
+      }
+    }
+    // keep the operand reads PD ahead: DS reads, then one MFMA and one read at a time
+    __builtin_amdgcn_sched_group_barrier(0x100, PD, 0);
+#pragma unroll
+    for (int n = 0; n < N - PD; ++n) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, PD, 0);
+  };
+  // S(0) of M(-1): K(0) Q^T only
+  auto s_first = [&]() {
+    const char* kb = smem;
+#pragma unroll
+    for (int ks = 0; ks < KSTEPS; ++ks)
+#pragma unroll
+      for (int mb = 0; mb < 2; ++mb) {
+        const int r = mb * 32 + pi_row(l32);
+        const int c = 2 * ks + hg;
+        const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(kb + r * 2 * D + ((c ^ fk<D>(r)) * 16));
+        sacc[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[ks], ks == 0 ? f32x16_t{} : sacc[mb], 0, 0, 0);
+      }
+  };
+
+  // ---- the half-step pipeline -------------------------------------------------------------
+  // wait_tile: this wave's loads of tile t are complete (the only loads that may still be in
+  // flight are those of tile t + 1, if it was issued), its LDS reads have returned, then the
+  // workgroup barrier publishes every wave's part of the tile.
+  // A barrier orders memory operations only: pure register arithmetic could still be moved
+  // across it (the exponentials of V(j) sunk next to their use in M(j), which would put both
+  // phases into one half step).  These empty volatile statements consume each phase's
+  // results, so the results are computed before the barrier that ends the phase.
+  auto pin_v = [&]() {
+#pragma unroll
+    for (int sp = 0; sp < 4; ++sp)
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) asm volatile("" ::"v"(pw[sp][jj]));
+    asm volatile("" ::"v"(l_run), "v"(m_run));
+  };
+  auto pin_m = [&]() {
+#pragma unroll
+    for (int md = 0; md < DM; ++md) asm volatile("" ::"v"(o[md][0]));
+    asm volatile("" ::"v"(sacc[0][0]), "v"(sacc[1][0]));
+  };
+  auto barrier_plain = [&]() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); };
+  auto barrier_wait = [&](int) {   // the one tile issued after the awaited one may be in flight
+    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(2 * NLD) : "memory");
+  };
+  if (ntiles > 0) {
+    for (int t = 0; t < kStages - 1; ++t)
+      if (t < ntiles) load_tile_global(t);
+  }
+  // the table, Q loads and tiles 0..2: one vmcnt(0) covers them all (tile 0 is read in half
+  // step 0); the barrier also publishes the table
+  __builtin_amdgcn_s_waitcnt(0x0F70);
+#pragma unroll
+  for (int k = 0; k < kTblPer; ++k) {
+    const int e = tid + k * kThreads;
+    if (e < n_tbl) tbl[e] = tbl_v[k];
+  }
+  __syncthreads();
+  fetch_next(kStages - 1);
+  if (ntiles > 0) {
+    const int e_tile = (L - kv_lo + kBK - 1) / kBK - 1;   // the tile holding key L - 1
+    if (grp == 1) barrier_plain();                      // half step 0: group 1 waits
+    s_first();                                           // M(-1)
+    pin_m();
+    if (grp == 1) barrier_wait(1); else barrier_plain(); // group 1's M(-1) ends half step 1
+    auto step = [&](int j, auto masked) {
+      // ---- V(j): half step 2j + 1 (group 0) / 2j + 2 (group 1)
+      if constexpr (decltype(masked)::value)
+        if (grp == 0 && j == e_tile) zero_v_tail(j, kv_lo + j * kBK);
+      v_phase(j, masked);
+      pin_v();
+      if (grp == 0) barrier_wait(j + 1); else barrier_plain();
+      // ---- M(j): half step 2j + 2 (group 0) / 2j + 3 (group 1)
+      // Every M phase issues one tile's loads, so that the waits count the same loads in every
+      // step: past the key range (j + 3 >= ntiles) the loads fetch block 0 into the stage of
+      // tile j - 1, which no wave reads any more.  On the last tile S(j+1) multiplies stale LDS;
+      // it is never used.
+      m_phase(j, std::true_type{}, std::true_type{}, j + 3);
+      pin_m();
+      if (grp == 0) barrier_plain();
+      else if (j + 1 < ntiles) barrier_wait(j + 2);
+    };
+    // tiles that need the causal / prompt-end mask form a suffix of the key range
+    auto tile_masked = [&](int t) {
+      const int t0 = kv_lo + t * kBK;
+      return (t0 + kBK - 1 > wg_min_pos) || (t0 + kBK > L);
+    };
+    int n_plain = ntiles;
+    {
+      int lo = 0, hi = ntiles;  // first masked tile, else ntiles
+      while (lo < hi) {
+        const int mid = (lo + hi) >> 1;
+        if (tile_masked(mid)) hi = mid; else lo = mid + 1;
+      }
+      n_plain = lo;
+    }
+    int j = 0;
+    for (; j < n_plain; ++j) step(j, std::false_type{});
+    for (; j < ntiles; ++j) step(j, std::true_type{});
+    // no load may still write this workgroup's LDS when it ends
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  }
+
+  // ---- epilogue: O^T register r of block md holds dim 32 md + 8 (r / 4) + 4 hg + r % 4 ------
+  const float lt = sum_halves(l_run);
+  const float inv = lt > 0.f ? 1.f / lt : 0.f;
+  const float lse = lt > 0.f ? m_run + __log2f(lt) : -INFINITY;
+#pragma unroll
+  for (int md = 0; md < DM; ++md) o[md] *= inv;
+  if (!cval) return;
+  if (w.slot < 0) {
+    uint16_t* dst = out + (static_cast<int64_t>(q0 + tok) * hq + w.kvh * G + g) * D;
+#pragma unroll
+    for (int md = 0; md < DM; ++md)
+#pragma unroll
+      for (int r4 = 0; r4 < 4; ++r4) {
+        f32x4_t v;
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) v[jj] = o[md][4 * r4 + jj];
+        *reinterpret_cast<bf16x4_t*>(dst + md * 32 + 8 * r4 + 4 * hg) = __builtin_convertvector(v, bf16x4_t);
+      }
+    return;
+  }
+  if (w.slot >= ws_slots) return;
+  const int local = wave * 32 + l32;
+  float* po = ws_o + (static_cast<int64_t>(w.slot) * kCols + local) * D;
+#pragma unroll
+  for (int md = 0; md < DM; ++md)
+#pragma unroll
+    for (int r4 = 0; r4 < 4; ++r4) {
+      f32x4_t v;
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) v[jj] = o[md][4 * r4 + jj];
+      *reinterpret_cast<f32x4_t*>(po + md * 32 + 8 * r4 + 4 * hg) = v;
+    }
+  if (hg == 0) ws_lse[static_cast<int64_t>(w.slot) * kCols + local] = lse;
+}
+
 // Merges the key-range splits of one query tile: o = sum_s 2^(lse_s - M) O_s / sum_s 2^(lse_s - M)
 // with M = max_s lse_s, per column.  Grid: (combine items, tile_cols / kCombineCols); a block
 // takes kCombineCols columns.  The first pieces' partial O (kCombinePre of them) and the lse
@@ -733,9 +1132,9 @@ int32_t prefill_attention(const void* k_pool, const void* v_pool, const void* q,
 #define ARCKV_LAUNCH(DD, GG)                                                                   \
   do {                                                                                         \
     if (tile_cols == arckv::kWideCols)                                                         \
-      launch_attn<DD, GG, kWideWaves, kWideNB, 1>(grid, st, kp, vp, qp, op, block_tables, bt_stride, cu_q, seq_lens, \
-                             n_reqs, wk, n_q, num_blocks, num_q_heads, num_kv_heads,           \
-                             scale_log2, ws_o, ws_lse, ws_slots);                              \
+      hipLaunchKernelGGL((prefill_attn_pp_kernel<DD, GG>), grid, dim3(512), 0, st, kp, vp, qp, op, \
+                         block_tables, bt_stride, cu_q, seq_lens, n_reqs, wk, n_q, num_blocks, \
+                         num_q_heads, num_kv_heads, scale_log2, ws_o, ws_lse, ws_slots);      \
     else if (tile_cols == arckv::kTinyCols)                                                    \
       launch_attn<DD, GG, 2, 1, 2>(grid, st, kp, vp, qp, op, block_tables, bt_stride, cu_q, seq_lens, \
                              n_reqs, wk, n_q, num_blocks, num_q_heads, num_kv_heads,           \
