@@ -71,7 +71,7 @@ def scatter_bytes(S, hkv, d):
     return float(np.sum(8.0 * np.asarray(S, dtype=np.float64) * hkv * d))
 
 
-def measured_traffic(workload: str):
+def measured_traffic(workload: str, kernel: str):
     """HBM bytes per prefill_attn launch (FETCH_SIZE + WRITE_SIZE, calibrated against a plain
     copy kernel) from the committed profile of this workload, or None when there is none or it
     was taken on a different version of the kernel source."""
@@ -83,6 +83,8 @@ def measured_traffic(workload: str):
         if data.get("kernel_source_sha256") != hashlib.sha256(open(src, "rb").read()).hexdigest():
             return None
         e = data["workloads"][workload]
+        if e.get("kernel", kernel) != kernel:
+            return None
         return round(e["fetch_bytes_per_launch"] + e["write_bytes_per_launch"], 1)
     except (OSError, KeyError, ValueError):
         return None
@@ -432,13 +434,14 @@ def main():
     for key in host_t:
         host_t[key] = 0.0
     torch.cuda.synchronize()
-    plans, n_work = [], []
+    plans, n_work, widths = [], [], []
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for k in range(steps):
         plan, db = step(n_untimed + k, events[k])
         plans.append(plan)
         n_work.append((db.n_work, db.n_combine))
+        widths.append(db.tile_cols)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
 
@@ -467,7 +470,8 @@ def main():
         per_launch = float(np.mean(B))
     hit = lambda a, b: (a["prefix_hit_tokens"] - b["prefix_hit_tokens"]) / max(
         1, a["prompt_tokens"] - b["prompt_tokens"])
-    traffic = measured_traffic(args.workload)
+    kernel_name = "prefill_attn_pp_kernel" if widths and max(widths) == 256 else "prefill_attn_kernel"
+    traffic = measured_traffic(args.workload, kernel_name)
 
     result = {
         "metric": "prefix-cached prefill attn TFLOP/s & % MI355X roofline; suffix tokens/s",
@@ -491,7 +495,7 @@ def main():
         "suffix_tokens_per_s": round(suffix_tokens / wall, 1),
         "roofline": {
             "bound": bound,
-            "kernel": "prefill_attn_kernel",
+            "kernel": kernel_name,   # 256-column tiles run the ping-pong kernel, narrower ones the key-half kernel
             "achieved": round(achieved, 2),
             "peak": peak,
             "unit": unit,

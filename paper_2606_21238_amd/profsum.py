@@ -176,13 +176,15 @@ if __name__ == "__main__":
         sys.stdout.write(counters_last(args[0], m or ".", int(clast)))
     elif traffic:
         # --traffic-json OUT --workload W --kernel-source SRC --fetch-dir D1 --write-dir D2
-        #   --calib-match REGEX --calib-mib N --last K --match KERNEL_REGEX
+        #   --calib-match REGEX --calib-mib N --last K --match KERNEL_REGEX [--kernel-name NAME]
         import hashlib
         import json
         w = opt("--workload")
         src = opt("--kernel-source")
+        kname = opt("--kernel-name")
         entry = traffic_entry(opt("--fetch-dir"), opt("--write-dir"), m, opt("--calib-match"),
                               int(opt("--calib-mib")), int(last))
+        entry["kernel"] = kname or m
         sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
         data = json.load(open(traffic)) if os.path.exists(traffic) else {}
         if data.get("kernel_source_sha256") != sha:

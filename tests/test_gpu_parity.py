@@ -190,6 +190,21 @@ def test_attention_sweep(case, num_cus):
         assert (ap.work[: ap.n_work, 5] >= 0).any()
 
 
+def test_attention_beyond_the_item_key_cap():
+    # 70000 keys: every tile's range exceeds one item's 65536-key cap, so the plan splits it and
+    # the combine merges the pieces (wide tiles on the ping-pong kernel); sampled rows
+    hq, hkv, d = 16, 2, 128
+    reqs = [(70000, 69800)]
+    print_case(f"key cap {reqs} hq={hq} hkv={hkv} d={d}")
+    b = build_batch(reqs, hq, hkv, d, seed=880)
+    got, ap = run_attention(b, hq, hkv, d, 256)
+    assert ap.n_combine > 0 and ap.tile_cols == 256
+    rng = np.random.default_rng(8)
+    rows = [sample_rows(200, rng, 24)]
+    ref = oracle_out(b, hq, hkv, d, rows)
+    compare(got, ref, "beyond the key cap")
+
+
 def test_split_merges_reuse_one_workspace():
     # split plans of different shapes in a row on one workspace (stale partials of an earlier
     # call must not leak into a later one)

@@ -335,6 +335,19 @@ def test_attention_plan_covers_every_tile_once():
     attention_plan_coverage([0, 51, 103], [4000, 103], 40, 8, 128, 256)
 
 
+def test_attention_plan_caps_the_keys_of_one_item():
+    """No work item covers more than 65536 keys (the attention kernel keeps an item's block-table
+    slice in LDS): long key ranges are split even where the tiles alone would fill the CUs."""
+    for cu, L, hq, hkv, cus in (([0, 2048, 4096], [140000, 100000], 64, 8, 256),   # plenty of tiles
+                                ([0, 16], [300000], 32, 8, 256),                    # one short suffix
+                                ([0, 1, 2], [70000, 65600], 8, 1, 4)):               # decode-like
+        ap = attention_plan_coverage(cu, L, hq, hkv, 128, cus)
+        w = ap.work[: ap.n_work]
+        live = w[:, 0] >= 0
+        assert (w[live, 4] - w[live, 3] <= 65536).all()
+        assert ap.n_combine > 0
+
+
 def test_attention_plan_places_a_group_on_one_xcd():
     cu = np.cumsum([0] + [2048] * 4).tolist()
     ap = ak.attention_plan(cu, [34816] * 4, 64, 8, 128, 256)
