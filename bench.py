@@ -531,7 +531,7 @@ def main():
 
     if layer:
         result["layer"] = {
-            "what": "per step: Q/K/V projection (rocBLAS GEMM + rotary/split kernel), KV scatter, "
+            "what": "per step: Q/K/V projection (fused bf16 MFMA GEMM + rotary epilogue), KV scatter, "
                     "attention, combine; value counts projection + attention flops",
             "projection_tflops": round(float(np.sum(proj_f)) / float(np.sum(t_proj)) / 1e12, 2),
             "projection_frac_of_bf16_peak": round(float(np.sum(proj_f)) / float(np.sum(t_proj)) / 1e12

@@ -20,9 +20,8 @@
  *  - Host objects are opaque and owned by the library (create/destroy pairs).
  *  - Device memory is always owned by the caller.  The library never
  *    allocates or frees device memory itself; device pointers are borrowed
- *    until the work queued on the given stream has completed.  (The one
- *    library it calls, rocBLAS in arckv_qkv_rope, keeps a per-device handle
- *    and manages its own workspace.)
+ *    until the work queued on the given stream has completed.  The library
+ *    links no other GPU library: every device step is a kernel of its own.
  *  - Device calls enqueue asynchronously on the caller's HIP stream (passed as
  *    void*, NULL = the null stream).  Argument checks are synchronous; a launch
  *    failure returns ARCKV_EDEVICE.  Nothing synchronises implicitly.
@@ -55,6 +54,7 @@ extern "C" {
 #define ARCKV_EDEVICE (-3)      /* a HIP call failed (message holds the HIP error)      */
 #define ARCKV_ESTATE (-4)       /* call order violated (plan/release)                   */
 #define ARCKV_EUNSUPPORTED (-5) /* head_dim / group size / block size not supported     */
+#define ARCKV_ECOLLISION (-6)   /* two different blocks share one identity (check mode)  */
 
 /* policies and reference order */
 #define ARCKV_POLICY_ARC 0
@@ -103,6 +103,22 @@ int32_t arckv_hash_blocks_batch(const int32_t* const* tokens, const int64_t* n_t
                                 int32_t n_seqs, uint64_t root, uint64_t* out, int64_t out_cap,
                                 int64_t* offsets);
 
+/* Block digests for collision checks: a second chained 64-bit value per full block, from a
+ * different function than the identity (splitmix64's finaliser, Steele, Lea and Flood 2014,
+ * applied per token): d_i = F(d_{i-1}, tokens of block i), d_{-1} = F0(root).  Two blocks
+ * with the same identity but different token prefixes have equal digests only by a second,
+ * independent accident.  Same arguments and errors as arckv_hash_blocks.  The cache keeps
+ * them when created with check_blocks (see arckv_plan_batch). */
+int32_t arckv_digest_blocks(const int32_t* tokens, int64_t n_tokens, uint64_t root,
+                            uint64_t* out, int64_t out_cap, int64_t* n_full);
+
+/* TEST ONLY.  Every identity the library computes from now on (arckv_hash_blocks, _batch,
+ * arckv_prepare_batch) is ANDed with mask, process-wide; the chains themselves run
+ * unmasked.  A narrow mask forces identity collisions, which lets tests exercise the
+ * check mode.  ~0 (the default) restores normal identities.  *previous (may be NULL)
+ * receives the mask in force before the call.  Not for serving. */
+int32_t arckv_test_set_hash_mask(uint64_t mask, uint64_t* previous);
+
 /* ---------------------------------------------------------------------------------------
  * Block cache: ARC(c) or LRU over block identities, with physical placement (host).
  * ARC per Sec. 3 / Fig. 2 (resident T1 "seen once", T2 "seen again", ghost lists B1/B2,
@@ -143,17 +159,21 @@ typedef struct {
                                      /* at such a block (engines that cache a block only  */
                                      /* once its step has run)                            */
   double frc_p;                      /* ARCKV_POLICY_FRC: the fixed target p, in [0, c]   */
+  int32_t check_blocks;              /* 0 (default) or 1: resident pages keep each block's */
+                                     /* digest and every plan verifies digests (below)     */
 } arckv_cache_cfg;
 
 /* Creates a cache (host memory only).  EINVAL on a bad configuration. */
 int32_t arckv_cache_create(const arckv_cache_cfg* cfg, arckv_cache** out);
 int32_t arckv_cache_destroy(arckv_cache* cache);
 
-/* One request of a batch: its chained hashes (n_full = n_tokens / 16) and length. */
+/* One request of a batch: its chained hashes (n_full = n_tokens / 16) and length, and
+ * optionally its block digests (arckv_digest_blocks, n_full of them; NULL = unchecked). */
 typedef struct {
   const uint64_t* hashes;
   int64_t n_full;
   int64_t n_tokens;
+  const uint64_t* digests;
 } arckv_req;
 
 /* Caller-allocated host output arrays of arckv_plan_batch, with their capacities. */
@@ -186,7 +206,13 @@ int32_t arckv_next_batch(const int64_t* n_tokens, int32_t n_avail, int32_t max_b
  *  slots of tokens [P, L).  A later request may hit blocks an earlier one created.
  * ESTATE if a batch is in flight; ENOSPC if the batch needs more than c full blocks, more
  * scratch blocks than free, or outputs exceed their capacities (state is then unchanged);
- * EINVAL on inconsistent requests. */
+ * EINVAL on inconsistent requests.
+ * Check mode (cfg.check_blocks = 1), for the requests that carry digests: before any state
+ * changes, every block whose identity is resident must carry the digest stored with that page
+ * (when one is stored), and blocks of the batch that share an identity must share the digest;
+ * otherwise ECOLLISION (message: request, block, identity) and nothing changes.  Every page
+ * a checked request references then stores its digest.  Without check mode a collision goes
+ * unnoticed: the page's KV would be reused for different tokens. */
 int32_t arckv_plan_batch(arckv_cache* cache, const arckv_req* reqs, int32_t n_reqs,
                          arckv_plan* plan);
 
@@ -288,7 +314,9 @@ int32_t arckv_attention_plan(const int32_t* cu_q, const int32_t* seq_lens, int32
  * depends only on the prompt lengths, heads and num_cus: if it does not, ENOSPC with the
  * bound in out->n_packed and the cache unchanged.  n_reqs >= 1 and every n_tokens >= 1 (else
  * EINVAL).  Other errors as for the three calls (a plan error leaves the cache unchanged; the
- * batch is in flight on success, to be ended with arckv_release_batch). */
+ * batch is in flight on success, to be ended with arckv_release_batch).  With a cache in
+ * check mode the block digests (arckv_digest_blocks, same root) are computed too and every
+ * request is checked (ECOLLISION as for arckv_plan_batch). */
 typedef struct {
   int32_t n_reqs, bt_stride;
   int64_t off_block_tables, off_cu_q, off_seq_lens, off_slots, off_work; /* in int32 units  */
@@ -307,7 +335,8 @@ int32_t arckv_prepare_batch(arckv_cache* cache, const int32_t* const* tokens,
 /* arckv_prepare_batch for callers that keep their requests' chained hashes (a serving loop
  * holding a running request's block hashes): hashes[r] holds n_tokens[r] / 16 identities
  * (as arckv_hash_blocks gives; may be NULL when there are none); no hashing is done.  Same
- * outputs and errors as arckv_prepare_batch. */
+ * outputs and errors as arckv_prepare_batch; the requests carry no digests, so check mode
+ * does not verify them (their pages' stored digests are left as they were). */
 int32_t arckv_prepare_batch_hashed(arckv_cache* cache, const uint64_t* const* hashes,
                                    const int64_t* n_tokens, int32_t n_reqs,
                                    int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
@@ -368,7 +397,7 @@ int32_t arckv_prefill_attention_noalloc(const void* k_pool, const void* v_pool, 
  * Device: the producer of the computed tokens' Q/K/V (the attention inputs of a prefill;
  * Sec. 4 serves Qwen3-14B, whose public configuration fixes the details): projection of the
  * hidden states and rotary position embedding.
- *   y = x W^T (rocBLAS, bf16 in and out, fp32 accumulate), then for every query and key head
+ *   y = x W^T (bf16 in, fp32 accumulate, y rounded to bf16), then for every query and key head
  *   at the token's absolute position p (request r's suffix token i: L_r - S_r + i) and
  *   i < head_dim / 2, angle a = p * rope_theta^(-2 i / head_dim):
  *   out[i] = u[i] cos a - u[i + D/2] sin a,  out[i + D/2] = u[i + D/2] cos a + u[i] sin a
@@ -377,17 +406,19 @@ int32_t arckv_prefill_attention_noalloc(const void* k_pool, const void* v_pool, 
  * x: device bf16 [n_tokens][hidden], rows ordered by cu_q.  w_qkv: device bf16
  * [(num_q_heads + 2 num_kv_heads) head_dim][hidden] (query heads, then key heads, then value
  * heads).  cu_q [n_reqs + 1], seq_lens [n_reqs]: device, as for the attention call
- * (n_tokens = cu_q[n_reqs]).  y_workspace: device, >= 2 n_tokens (num_q_heads + 2
- * num_kv_heads) head_dim bytes, caller-owned.  q_out: device bf16 [n_tokens][num_q_heads]
+ * (n_tokens = cu_q[n_reqs]).  workspace: device, >= 4 n_tokens head_dim bytes (the (cos, sin)
+ * pairs of every token as fp32), caller-owned.  q_out: device bf16 [n_tokens][num_q_heads]
  * [head_dim]; k_out, v_out: device bf16 [n_tokens][num_kv_heads][head_dim] (the layout
- * arckv_kv_scatter takes).  y_workspace, q_out, k_out and v_out must be 16-byte aligned.
- * Stream-ordered on `stream`.  head_dim in {64, 128}: else EUNSUPPORTED; EINVAL on bad sizes,
- * NULL or misaligned pointers or rope_theta <= 1; ENOSPC if the workspace is too small;
- * EDEVICE if rocBLAS or a launch fails.  n_tokens = 0 is a no-op. */
+ * arckv_kv_scatter takes).  x, w_qkv, workspace, q_out, k_out and v_out must be 16-byte
+ * aligned.  One fused kernel (GEMM tile + rotation in its epilogue) after a small table
+ * pass; y never goes to memory.  Stream-ordered on `stream`.  head_dim in {64, 128}, hidden a
+ * multiple of 32 (at most 2^22) and (num_q_heads + 2 num_kv_heads) head_dim a multiple of 128: else
+ * EUNSUPPORTED; EINVAL on bad sizes, NULL or misaligned pointers or rope_theta <= 1; ENOSPC if
+ * the workspace is too small; EDEVICE if a launch fails.  n_tokens = 0 is a no-op. */
 int32_t arckv_qkv_rope(const void* x, const void* w_qkv, int64_t n_tokens, int32_t hidden,
                        int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
                        const int32_t* cu_q, const int32_t* seq_lens, int32_t n_reqs,
-                       double rope_theta, void* y_workspace, int64_t ws_bytes, void* q_out,
+                       double rope_theta, void* workspace, int64_t ws_bytes, void* q_out,
                        void* k_out, void* v_out, void* stream);
 
 #ifdef __cplusplus

@@ -44,6 +44,36 @@ def hash_blocks(tokens, root: int = 0) -> np.ndarray:
     return out
 
 
+def digest_blocks(tokens, root: int = 0) -> np.ndarray:
+    """Chained block digests (uint64) for collision checks: an independent second hash of
+    every full 16-token block (arckv_digest_blocks)."""
+    t = np.ascontiguousarray(tokens, dtype=np.int32)
+    out = np.empty(len(t) // BLOCK_TOKENS, dtype=np.uint64)
+    nf = _lib.i64()
+    _lib.check(lib().arckv_digest_blocks(_ptr(t, _lib.i32), len(t), C.c_uint64(root), _ptr(out, _lib.u64),
+                                         len(out), C.byref(nf)), "arckv_digest_blocks")
+    return out
+
+
+class forced_identity_mask:
+    """TEST ONLY: while active, every block identity the library computes is ANDed with
+    `mask` (arckv_test_set_hash_mask), which forces identity collisions."""
+
+    def __init__(self, mask: int):
+        self.mask = int(mask)
+        self._prev = None
+
+    def __enter__(self):
+        prev = _lib.u64()
+        _lib.check(lib().arckv_test_set_hash_mask(C.c_uint64(self.mask), C.byref(prev)), "arckv_test_set_hash_mask")
+        self._prev = int(prev.value)
+        return self
+
+    def __exit__(self, *exc):
+        lib().arckv_test_set_hash_mask(C.c_uint64(self._prev), None)
+        return False
+
+
 def hash_blocks_batch(token_lists, root: int = 0):
     """Chained identities of several sequences in one call -> list of uint64 arrays (views)."""
     toks = [np.ascontiguousarray(t, dtype=np.int32) for t in token_lists]
@@ -98,16 +128,18 @@ class BlockCache:
 
     def __init__(self, policy: str, capacity: int, num_phys: int, scratch: int,
                  initial_order=None, ref_order: str = "tail_first", victim_window: int = 1,
-                 intra_batch_reuse: bool = True, frc_p: float = 0.0):
+                 intra_batch_reuse: bool = True, frc_p: float = 0.0, check_blocks: bool = False):
         """policy: arc, lru, dbl (p fixed at c/2) or frc (p fixed at frc_p).
         victim_window W > 1: length-aware victims (the deepest of the W least recently used
         unpinned pages of the list a policy evicts from); 1 is the plain policy.
         intra_batch_reuse False: a request's prefix stops at a block an earlier request of the
-        same batch created."""
+        same batch created.
+        check_blocks True: check mode (pages keep block digests; plans verify them and raise
+        ArckvError ECOLLISION when two different blocks share an identity)."""
         self._order = None if initial_order is None else np.ascontiguousarray(initial_order, dtype=np.int32)
         cfg = _lib.CacheCfg(_lib.POLICY[policy], _lib.REF_ORDER[ref_order], capacity, num_phys, scratch,
                             None if self._order is None else _ptr(self._order, _lib.i32), victim_window,
-                            0 if intra_batch_reuse else 1, float(frc_p))
+                            0 if intra_batch_reuse else 1, float(frc_p), 1 if check_blocks else 0)
         h = C.c_void_p()
         _lib.check(lib().arckv_cache_create(C.byref(cfg), C.byref(h)), "arckv_cache_create")
         self._h = h
@@ -126,13 +158,17 @@ class BlockCache:
             pass
 
     def plan_batch(self, reqs, bt_stride: int | None = None) -> BatchPlan:
-        """reqs: sequence of (hashes uint64 array, n_tokens)."""
+        """reqs: sequence of (hashes uint64 array, n_tokens) or (hashes, n_tokens, digests)."""
         n = len(reqs)
-        keep = [np.ascontiguousarray(h, dtype=np.uint64) for h, _ in reqs]
+        keep = [np.ascontiguousarray(rq[0], dtype=np.uint64) for rq in reqs]
+        dig = [None if len(rq) < 3 or rq[2] is None else np.ascontiguousarray(rq[2], dtype=np.uint64)
+               for rq in reqs]
         arr = (_lib.Req * max(n, 1))()
-        for i, ((_, nt), h) in enumerate(zip(reqs, keep)):
-            arr[i] = _lib.Req(_ptr(h, _lib.u64), len(h), int(nt))
-        lens = [int(nt) for _, nt in reqs]
+        for i, (rq, h, d) in enumerate(zip(reqs, keep, dig)):
+            if d is not None and len(d) != len(h):
+                raise ValueError(f"request {i}: {len(d)} digests for {len(h)} blocks")
+            arr[i] = _lib.Req(_ptr(h, _lib.u64), len(h), int(rq[1]), None if d is None else _ptr(d, _lib.u64))
+        lens = [int(rq[1]) for rq in reqs]
         stride = bt_stride or max([(x + BLOCK_TOKENS - 1) // BLOCK_TOKENS for x in lens] + [1])
         bt = np.empty((n, stride), dtype=np.int32)
         cu = np.empty(n + 1, dtype=np.int32)
@@ -301,7 +337,7 @@ def qkv_rope(x, w_qkv, cu_q, seq_lens, num_q_heads: int, num_kv_heads: int, rope
              q_out, k_out, v_out, workspace, stream=None):
     """Projection + rotary embedding of the computed tokens (arckv_qkv_rope).  Device tensors:
     x [T, H] bf16, w_qkv [(Hq + 2 Hkv) D, H] bf16, cu_q [n+1], seq_lens [n] int32, q_out
-    [T, Hq, D], k_out / v_out [T, Hkv, D] bf16, workspace >= 2 T (Hq + 2 Hkv) D bytes."""
+    [T, Hq, D], k_out / v_out [T, Hkv, D] bf16, workspace >= 4 T D bytes (the rotary table)."""
     t, h = int(x.shape[0]), int(x.shape[1])
     d = int(q_out.shape[2])
     n_out = (num_q_heads + 2 * num_kv_heads) * d

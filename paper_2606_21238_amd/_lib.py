@@ -8,8 +8,9 @@ import os
 _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "lib", "libarckv.so")
 
-OK, EINVAL, ENOSPC, EDEVICE, ESTATE, EUNSUPPORTED = 0, -1, -2, -3, -4, -5
-STATUS_NAMES = {0: "OK", -1: "EINVAL", -2: "ENOSPC", -3: "EDEVICE", -4: "ESTATE", -5: "EUNSUPPORTED"}
+OK, EINVAL, ENOSPC, EDEVICE, ESTATE, EUNSUPPORTED, ECOLLISION = 0, -1, -2, -3, -4, -5, -6
+STATUS_NAMES = {0: "OK", -1: "EINVAL", -2: "ENOSPC", -3: "EDEVICE", -4: "ESTATE", -5: "EUNSUPPORTED",
+                -6: "ECOLLISION"}
 POLICY = {"arc": 0, "lru": 1, "dbl": 2, "frc": 3}
 REF_ORDER = {"tail_first": 0, "head_first": 1}
 WORK_INTS = 8
@@ -21,11 +22,12 @@ P_i32, P_i64, P_u64 = C.POINTER(i32), C.POINTER(i64), C.POINTER(u64)
 class CacheCfg(C.Structure):
     _fields_ = [("policy", i32), ("ref_order", i32), ("capacity_blocks", i64),
                 ("num_phys_blocks", i64), ("scratch_blocks", i64), ("initial_free_order", P_i32),
-                ("victim_window", i32), ("no_intra_batch_reuse", i32), ("frc_p", f64)]
+                ("victim_window", i32), ("no_intra_batch_reuse", i32), ("frc_p", f64),
+                ("check_blocks", i32)]
 
 
 class Req(C.Structure):
-    _fields_ = [("hashes", P_u64), ("n_full", i64), ("n_tokens", i64)]
+    _fields_ = [("hashes", P_u64), ("n_full", i64), ("n_tokens", i64), ("digests", P_u64)]
 
 
 class PlanC(C.Structure):
@@ -58,6 +60,8 @@ _SIGS = {
     "arckv_version": (i32, []),
     "arckv_hash_blocks": (i32, [P_i32, i64, u64, P_u64, i64, P_i64]),
     "arckv_hash_blocks_batch": (i32, [C.POINTER(P_i32), P_i64, i32, u64, P_u64, i64, P_i64]),
+    "arckv_digest_blocks": (i32, [P_i32, i64, u64, P_u64, i64, P_i64]),
+    "arckv_test_set_hash_mask": (i32, [u64, P_u64]),
     "arckv_cache_create": (i32, [C.POINTER(CacheCfg), C.POINTER(vp)]),
     "arckv_cache_destroy": (i32, [vp]),
     "arckv_next_batch": (i32, [P_i64, i32, i32, i64, i64, P_i32]),

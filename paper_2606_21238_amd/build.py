@@ -81,11 +81,10 @@ def build(verbose: bool = False, sanitize: bool = False) -> str:
     tmp = out_lib + ".tmp"
     if sanitize:
         # linked by g++ (no HIP source on this line), with the sanitizer runtimes
-        _run(["g++", "-shared", "-fPIC", *SANITIZE, *objs, "-L/opt/rocm/lib", "-lamdhip64", "-lrocblas",
+        _run(["g++", "-shared", "-fPIC", *SANITIZE, *objs, "-L/opt/rocm/lib", "-lamdhip64",
               f"-Wl,-rpath,/opt/rocm/lib", "-o", tmp])
     else:
-        # rocBLAS for the one plain GEMM (the Q/K/V projection)
-        _run([hipcc, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-lrocblas", "-o", tmp])
+        _run([hipcc, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp])
     os.replace(tmp, out_lib)
     return out_lib
 

@@ -5,6 +5,11 @@
 // Sec. 2), so its identity chains in the parent's identity:
 //   h_i = FNV-1a-64(le64(h_{i-1}) || le32(tok[16 i]) .. le32(tok[16 i + 15])),  h_{-1} = root.
 // FNV-1a-64: offset basis 0xcbf29ce484222325, prime 0x100000001b3, per byte h ^= b, h *= prime.
+//
+// Block digests (collision checks) chain the same way through a different function: per token
+// d <- M(d + golden + token) with M the splitmix64 finaliser (Steele, Lea and Flood, "Fast
+// splittable pseudorandom number generators", 2014); d_{-1} = M(root ^ seed).
+#include <atomic>
 #include <cstring>
 
 #include "internal.hpp"
@@ -15,6 +20,25 @@ constexpr uint64_t kFnvOffset = 0xcbf29ce484222325ull;
 constexpr uint64_t kFnvPrime = 0x100000001b3ull;
 
 inline uint64_t mix_byte(uint64_t h, uint8_t b) { return (h ^ b) * kFnvPrime; }
+
+// identities are ANDed with this (test-only override; all ones otherwise)
+std::atomic<uint64_t> g_identity_mask{~0ull};
+
+constexpr uint64_t kGolden = 0x9E3779B97F4A7C15ull;
+constexpr uint64_t kDigestSeed = 0xD1B54A32D192ED03ull;
+
+inline uint64_t splitmix_final(uint64_t z) {
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+
+inline uint64_t digest_block(uint64_t parent, const int32_t* tok) {
+  uint64_t d = parent;
+  for (int t = 0; t < ARCKV_BLOCK_TOKENS; ++t)
+    d = splitmix_final(d + kGolden + static_cast<uint32_t>(tok[t]));
+  return d;
+}
 
 inline uint64_t hash_block(uint64_t parent, const int32_t* tok) {
   uint64_t h = kFnvOffset;
@@ -37,11 +61,35 @@ extern "C" int32_t arckv_hash_blocks(const int32_t* tokens, int64_t n_tokens, ui
   if (nf > out_cap || (nf > 0 && out == nullptr))
     return arckv::fail(ARCKV_ENOSPC, "hash_blocks: %lld blocks, capacity %lld",
                        (long long)nf, (long long)out_cap);
+  const uint64_t mask = g_identity_mask.load(std::memory_order_relaxed);
   uint64_t h = root;
   for (int64_t i = 0; i < nf; ++i) {
     h = hash_block(h, tokens + i * ARCKV_BLOCK_TOKENS);
-    out[i] = h;
+    out[i] = h & mask;
   }
+  return ARCKV_OK;
+}
+
+extern "C" int32_t arckv_digest_blocks(const int32_t* tokens, int64_t n_tokens, uint64_t root,
+                                       uint64_t* out, int64_t out_cap, int64_t* n_full) {
+  if (n_tokens < 0 || n_full == nullptr || (n_tokens > 0 && tokens == nullptr))
+    return arckv::fail(ARCKV_EINVAL, "digest_blocks: bad arguments");
+  const int64_t nf = n_tokens / ARCKV_BLOCK_TOKENS;
+  *n_full = nf;
+  if (nf > out_cap || (nf > 0 && out == nullptr))
+    return arckv::fail(ARCKV_ENOSPC, "digest_blocks: %lld blocks, capacity %lld",
+                       (long long)nf, (long long)out_cap);
+  uint64_t d = splitmix_final(root ^ kDigestSeed);
+  for (int64_t i = 0; i < nf; ++i) {
+    d = digest_block(d, tokens + i * ARCKV_BLOCK_TOKENS);
+    out[i] = d;
+  }
+  return ARCKV_OK;
+}
+
+extern "C" int32_t arckv_test_set_hash_mask(uint64_t mask, uint64_t* previous) {
+  const uint64_t old = g_identity_mask.exchange(mask);
+  if (previous != nullptr) *previous = old;
   return ARCKV_OK;
 }
 
@@ -88,6 +136,7 @@ extern "C" int32_t arckv_hash_blocks_batch(const int32_t* const* tokens, const i
     busy += seq[l] >= 0;
   }
   static const int32_t kZeros[ARCKV_BLOCK_TOKENS] = {};
+  const uint64_t mask = g_identity_mask.load(std::memory_order_relaxed);
   while (busy > 0) {
     uint64_t x[kLanes];
     const int32_t* t16[kLanes];
@@ -106,7 +155,7 @@ extern "C" int32_t arckv_hash_blocks_batch(const int32_t* const* tokens, const i
     for (int l = 0; l < kLanes; ++l) {
       if (seq[l] < 0) continue;
       h[l] = x[l];
-      *dst[l]++ = x[l];
+      *dst[l]++ = x[l] & mask;
       tok[l] += ARCKV_BLOCK_TOKENS;
       if (--left[l] == 0) {
         refill(l);

@@ -22,12 +22,18 @@
 // ghost list then receives the page); a new page takes the evicted page's physical block or
 // the head of a FIFO free list; partial last blocks use a separate scratch FIFO.
 //
+// Check mode (a safety net; the paper identifies blocks by hash alone): every resident page
+// also keeps the block's digest, an independent second hash; before a plan changes anything,
+// each block of a checked request whose identity is resident must match the stored digest, and
+// blocks of the batch that share an identity must share the digest.
+//
 // Lists are intrusive doubly linked lists over a node array (head = LRU, tail = MRU) with an
 // open-addressing index from identity to node (linear probing, backward-shift deletion, no
 // per-entry allocation), so every reference is O(1) apart from skipping pinned pages at the
 // LRU end.
 #include <algorithm>
 #include <deque>
+#include <unordered_map>
 #include <vector>
 
 #include "internal.hpp"
@@ -42,6 +48,7 @@ struct Node {
   int32_t prev = -1, next = -1;
   int32_t list = ARCKV_LIST_NONE;
   int32_t depth = 0;  // block index of the page in the prompt that last referenced it
+  uint64_t digest = 0;  // check mode: digest of the block whose KV the page holds (0: unknown)
 };
 
 struct List {
@@ -113,6 +120,7 @@ struct arckv_cache {
   int32_t ref_order = ARCKV_REF_TAIL_FIRST;
   int32_t window = 1;  // victim window (length-aware eviction when > 1)
   bool intra_batch_reuse = true;
+  bool check_blocks = false;
   int64_t c = 0;
   int64_t num_phys = 0;
   int64_t n_scratch = 0;
@@ -361,7 +369,8 @@ struct arckv_cache {
     return ARCKV_OK;
   }
 
-  int32_t reference(uint64_t x, int32_t hint, int32_t depth, int32_t& phys_out) {
+  // digest: the block's digest in check mode, else 0 (unknown)
+  int32_t reference(uint64_t x, int32_t hint, int32_t depth, uint64_t digest, int32_t& phys_out) {
     arckv_event ev{};
     ev.key = x;
     int32_t n = -1;
@@ -369,6 +378,10 @@ struct arckv_cache {
                                                   : reference_arc(x, hint, ev, n);
     if (st != ARCKV_OK) return st;
     nodes[n].depth = depth;
+    // a hit keeps the KV (and the digest, unless this reference knows it); any other case
+    // (re)writes the page's KV for this block
+    const bool hit = ev.kase == ARCKV_CASE_I || ev.kase == ARCKV_CASE_LRU_HIT;
+    if (!hit || digest != 0) nodes[n].digest = digest;
     ev.p_after = policy == ARCKV_POLICY_LRU ? 0.0 : p;
     phys_out = ev.phys_block;
     case_counts[ev.kase] += 1;
@@ -396,6 +409,8 @@ extern "C" int32_t arckv_cache_create(const arckv_cache_cfg* cfg, arckv_cache** 
     return arckv::fail(ARCKV_EINVAL, "cache_create: no_intra_batch_reuse must be 0 or 1");
   if (cfg->ref_order != ARCKV_REF_TAIL_FIRST && cfg->ref_order != ARCKV_REF_HEAD_FIRST)
     return arckv::fail(ARCKV_EINVAL, "cache_create: unknown reference order");
+  if (cfg->check_blocks != 0 && cfg->check_blocks != 1)
+    return arckv::fail(ARCKV_EINVAL, "cache_create: check_blocks must be 0 or 1");
   if (cfg->victim_window < 0 || cfg->victim_window > 4096)
     return arckv::fail(ARCKV_EINVAL, "cache_create: victim window %d not in [0, 4096]", cfg->victim_window);
   if (cfg->capacity_blocks < 1 || cfg->scratch_blocks < 0 || cfg->num_phys_blocks > INT32_MAX / 16 ||
@@ -424,6 +439,7 @@ extern "C" int32_t arckv_cache_create(const arckv_cache_cfg* cfg, arckv_cache** 
          : cfg->policy == ARCKV_POLICY_FRC ? cfg->frc_p
                                            : 0.0;
   c->intra_batch_reuse = cfg->no_intra_batch_reuse == 0;
+  c->check_blocks = cfg->check_blocks == 1;
   c->ref_order = cfg->ref_order;
   c->window = cfg->victim_window < 1 ? 1 : cfg->victim_window;
   c->c = cfg->capacity_blocks;
@@ -495,6 +511,36 @@ extern "C" int32_t arckv_plan_batch(arckv_cache* c, const arckv_req* reqs, int32
   if (total_tokens > plan->slot_cap || total_tokens > INT32_MAX)
     return arckv::fail(ARCKV_ENOSPC, "plan_batch: slot capacity %lld < %lld prompt tokens",
                        (long long)plan->slot_cap, (long long)total_tokens);
+  if (c->check_blocks) {
+    // identity -> (digest, request, block) of its first occurrence in the batch
+    struct First { uint64_t digest; int32_t req; int64_t block; };
+    thread_local std::unordered_map<uint64_t, First> first;
+    first.clear();
+    for (int32_t r = 0; r < n_reqs; ++r) {
+      const arckv_req& q = reqs[r];
+      if (q.digests == nullptr) continue;
+      for (int64_t i = 0; i < q.n_full; ++i) {
+        const uint64_t key = q.hashes[i], dg = q.digests[i];
+        const auto ins = first.emplace(key, First{dg, r, i});
+        if (!ins.second) {
+          const First& f = ins.first->second;
+          if (f.digest != dg)
+            return arckv::fail(ARCKV_ECOLLISION,
+                               "plan_batch: identity %016llx: request %d block %lld and request %d "
+                               "block %lld are different blocks",
+                               (unsigned long long)key, f.req, (long long)f.block, r, (long long)i);
+          continue;
+        }
+        const int32_t n = c->find(key);
+        if (n >= 0 && (c->nodes[n].list == ARCKV_LIST_T1 || c->nodes[n].list == ARCKV_LIST_T2) &&
+            c->nodes[n].digest != 0 && c->nodes[n].digest != dg)
+          return arckv::fail(ARCKV_ECOLLISION,
+                             "plan_batch: identity %016llx: request %d block %lld differs from the "
+                             "resident page (physical block %d)",
+                             (unsigned long long)key, r, (long long)i, c->nodes[n].phys);
+      }
+    }
+  }
 
   c->in_flight = true;  // pins of this batch are live from here until release
   int64_t n_slots = 0;
@@ -532,7 +578,8 @@ extern "C" int32_t arckv_plan_batch(arckv_cache* c, const arckv_req* reqs, int32
     for (int64_t i = 0; i < nf; ++i) {
       const int64_t b = c->ref_order == ARCKV_REF_TAIL_FIRST ? nf - 1 - i : i;
       int32_t phys = -1;
-      const int32_t st = c->reference(q.hashes[b], b < k ? prefix_node[b] : -1, static_cast<int32_t>(b), phys);
+      const uint64_t dg = c->check_blocks && q.digests != nullptr ? q.digests[b] : 0;
+      const int32_t st = c->reference(q.hashes[b], b < k ? prefix_node[b] : -1, static_cast<int32_t>(b), dg, phys);
       if (st != ARCKV_OK) return st;  // unreachable with the capacity check above
       row[b] = phys;
     }
@@ -626,3 +673,5 @@ extern "C" int32_t arckv_cache_snapshot(const arckv_cache* c, int32_t list, uint
   }
   return ARCKV_OK;
 }
+
+bool arckv::cache_checks_blocks(const arckv_cache* c) { return c != nullptr && c->check_blocks; }

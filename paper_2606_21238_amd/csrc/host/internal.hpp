@@ -21,6 +21,9 @@ constexpr int kTinyCols = kWaveCols;
 // the combine), so that the item's block-table entries (kMaxItemKeys / 16) fit in LDS.
 constexpr int kMaxItemKeys = 65536;
 
+// Whether the cache was created in check mode (block digests verified by every plan).
+bool cache_checks_blocks(const arckv_cache* c);
+
 // Records a thread-local message for arckv_last_error() and returns `code`.
 int32_t fail(int32_t code, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
 void clear_error();

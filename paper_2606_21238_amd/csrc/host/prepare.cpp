@@ -30,8 +30,9 @@ int64_t work_bound(const int64_t* n_tokens, int32_t n_reqs, int32_t G, int32_t h
 }
 
 // The common part: requests given as (hashes, n_tokens); `hashes[r]` holds n_tokens[r] / 16
-// chained identities.
-int32_t prepare_planned(arckv_cache* cache, const uint64_t* const* hashes, const int64_t* n_tokens,
+// chained identities, `digests` (NULL: none) as many block digests per request.
+int32_t prepare_planned(arckv_cache* cache, const uint64_t* const* hashes, const uint64_t* const* digests,
+                        const int64_t* n_tokens,
                         int32_t n_reqs, int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
                         int32_t num_cus, int32_t* packed, int64_t packed_cap, int32_t* prefix_lens,
                         int32_t* hit_blocks, arckv_batch* out) {
@@ -52,7 +53,8 @@ int32_t prepare_planned(arckv_cache* cache, const uint64_t* const* hashes, const
   thread_local std::vector<arckv_req> reqs;
   reqs.resize(static_cast<size_t>(n_reqs));
   for (int32_t r = 0; r < n_reqs; ++r)
-    reqs[r] = arckv_req{hashes[r], n_tokens[r] / ARCKV_BLOCK_TOKENS, n_tokens[r]};
+    reqs[r] = arckv_req{hashes[r], n_tokens[r] / ARCKV_BLOCK_TOKENS, n_tokens[r],
+                        digests != nullptr ? digests[r] : nullptr};
 
   out->n_reqs = n_reqs;
   out->bt_stride = static_cast<int32_t>(stride);
@@ -135,8 +137,22 @@ extern "C" int32_t arckv_prepare_batch(arckv_cache* cache, const int32_t* const*
   if (st != ARCKV_OK) return st;
   rows.resize(static_cast<size_t>(n_reqs));
   for (int32_t r = 0; r < n_reqs; ++r) rows[r] = hashes.data() + offsets[r];
-  return prepare_planned(cache, rows.data(), n_tokens, n_reqs, num_q_heads, num_kv_heads, head_dim,
-                         num_cus, packed, packed_cap, prefix_lens, hit_blocks, out);
+  thread_local std::vector<uint64_t> digests;
+  thread_local std::vector<const uint64_t*> drows;
+  if (arckv::cache_checks_blocks(cache)) {   // check mode: the blocks' digests as well
+    digests.resize(hashes.size());
+    drows.resize(static_cast<size_t>(n_reqs));
+    for (int32_t r = 0; r < n_reqs; ++r) {
+      int64_t nf = 0;
+      st = arckv_digest_blocks(tokens[r], n_tokens[r], root, digests.data() + offsets[r],
+                               offsets[r + 1] - offsets[r], &nf);
+      if (st != ARCKV_OK) return st;
+      drows[r] = digests.data() + offsets[r];
+    }
+  }
+  return prepare_planned(cache, rows.data(), arckv::cache_checks_blocks(cache) ? drows.data() : nullptr,
+                         n_tokens, n_reqs, num_q_heads, num_kv_heads, head_dim, num_cus, packed,
+                         packed_cap, prefix_lens, hit_blocks, out);
 }
 
 extern "C" int32_t arckv_prepare_batch_hashed(arckv_cache* cache, const uint64_t* const* hashes,
@@ -151,6 +167,6 @@ extern "C" int32_t arckv_prepare_batch_hashed(arckv_cache* cache, const uint64_t
   for (int32_t r = 0; r < n_reqs; ++r)
     if (n_tokens[r] >= ARCKV_BLOCK_TOKENS && hashes[r] == nullptr)
       return arckv::fail(ARCKV_EINVAL, "prepare_batch_hashed: request %d has no hashes", r);
-  return prepare_planned(cache, hashes, n_tokens, n_reqs, num_q_heads, num_kv_heads, head_dim,
+  return prepare_planned(cache, hashes, nullptr, n_tokens, n_reqs, num_q_heads, num_kv_heads, head_dim,
                          num_cus, packed, packed_cap, prefix_lens, hit_blocks, out);
 }

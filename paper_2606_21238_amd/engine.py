@@ -56,7 +56,7 @@ class PrefillEngine:
             num_cus = torch.cuda.get_device_properties(self.device).multi_processor_count
         self.num_cus = int(num_cus)
         self._ws = torch.empty(0, dtype=torch.uint8, device=self.device)
-        self._y = None          # projection output of the batch (arckv_qkv_rope workspace)
+        self._y = None          # rotary (cos, sin) table of the batch (arckv_qkv_rope workspace)
         # a ring of reusable pinned staging buffers and device metadata buffers, with the events
         # that mark their copies done: the host may prepare up to four batches ahead of the GPU
         # (a slow host step is then absorbed), and no pinned memory is allocated per batch
@@ -210,7 +210,7 @@ class PrefillEngine:
         for a, c in ((q, self.hq), (k_new, self.hkv), (v_new, self.hkv)):
             if tuple(a.shape) != (t, c, self.d) or not a.is_contiguous() or a.element_size() != 2:
                 raise ValueError("q / k_new / v_new must be contiguous 16-bit [n_tokens, heads, D]")
-        need = 2 * t * n_out
+        need = 4 * t * self.d
         if self._y is None or self._y.numel() < need:
             with torch.cuda.stream(self._torch_stream(stream)):
                 self._y = torch.empty(max(need, 1), dtype=torch.uint8, device=self.device)

@@ -68,7 +68,15 @@ def test_qkv_rope_validates_arguments_without_touching_a_device():
     assert L.arckv_qkv_rope(*args(128, 1.0e6)) == _lib.EINVAL          # NULL pointers
     assert b"NULL" in L.arckv_last_error()
     assert L.arckv_qkv_rope(*args(128, 1.0e6, t=0)) == _lib.OK         # nothing to do
+    # the fused kernel's tiling: hidden in steps of 32, outputs in steps of 128
+    assert L.arckv_qkv_rope(None, None, 4, 48, 4, 2, 128, None, None, 1, 1.0e6, None, 0, None, None, None,
+                            None) == _lib.EUNSUPPORTED
+    assert L.arckv_qkv_rope(None, None, 4, 64, 5, 1, 64, None, None, 1, 1.0e6, None, 0, None, None, None,
+                            None) == _lib.EUNSUPPORTED
     # misaligned outputs are refused before any device work (the addresses are never read)
     a, m = 0x10000, 0x10002
     assert L.arckv_qkv_rope(a, a, 4, 64, 4, 2, 128, a, a, 1, 1.0e6, a, 1 << 20, a, m, a, None) == _lib.EINVAL
     assert b"aligned" in L.arckv_last_error()
+    # the workspace holds 4 tokens x 64 (cos, sin) pairs of fp32: one byte short is refused
+    assert L.arckv_qkv_rope(a, a, 4, 64, 4, 2, 128, a, a, 1, 1.0e6, a, 4 * 4 * 128 - 1, a, a, a,
+                            None) == _lib.ENOSPC

@@ -49,7 +49,7 @@ def run(reqs, hidden, hq, hkv, d, seed):
     q = torch.empty((T, hq, d), dtype=torch.bfloat16, device=DEV)
     k = torch.empty((T, hkv, d), dtype=torch.bfloat16, device=DEV)
     v = torch.empty((T, hkv, d), dtype=torch.bfloat16, device=DEV)
-    ws = torch.empty(2 * T * (hq + 2 * hkv) * d, dtype=torch.uint8, device=DEV)
+    ws = torch.empty(4 * T * d, dtype=torch.uint8, device=DEV)          # the exact table size
     ak.qkv_rope(x, w, torch.from_numpy(cu).to(DEV), torch.from_numpy(sl).to(DEV), hq, hkv, THETA,
                 q, k, v, ws)
     torch.cuda.synchronize()
@@ -90,6 +90,9 @@ def check(r, hq, hkv, d):
     ([(129, 1), (64, 63)], 256, 16, 2, 64),
     ([(8320, 8192), (2100, 2048)], 5120, 40, 8, 128),                  # Qwen3-14B layer shape
     ([(3, 0), (9, 6)], 128, 4, 4, 128),                                # 6 tokens: a ragged group
+    ([(1300, 0), (400, 300)], 256, 5, 1, 128),     # 6 x 3.5 tiles: a half output tile, ragged tokens
+    ([(600, 0)], 96, 4, 1, 64),                    # 3 stages of H (short ring), 1.5 output tiles
+    ([(300, 0), (70, 0)], 32, 2, 1, 64),           # one stage of H
 ])
 def test_qkv_rope_matches_oracle(reqs, hidden, hq, hkv, d):
     print_case(f"qkv_rope {reqs} hidden={hidden} hq={hq} hkv={hkv} d={d}")
