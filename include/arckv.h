@@ -291,8 +291,8 @@ int32_t arckv_kv_scatter(void* k_pool, void* v_pool, const void* k_new, const vo
  * ARCKV_WORK_INTS * work_cap entries or NULL to query sizes.
  * Outputs: *n_work attention items, *n_combine combine items (both stored in work, the
  * combine items after the attention items), *ws_bytes device workspace needed, *tile_cols
- * the tile width (256; 128 when every request has at most 128 columns; 32 when every
- * request has at most 32, e.g. decode batches of one token per request).
+ * the tile width (256; 128 when every request has at most 128 columns, e.g. short suffixes
+ * and decode batches of one token per request).
  * ENOSPC if n_work + n_combine > work_cap (sizes still reported). */
 #define ARCKV_WORK_INTS 8
 int32_t arckv_attention_plan(const int32_t* cu_q, const int32_t* seq_lens, int32_t n_reqs,

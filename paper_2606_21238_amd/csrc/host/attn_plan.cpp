@@ -5,8 +5,8 @@
 // item streams serve all G heads of its group at once.  The key range of a tile ends at the
 // last visible key of its last column (causal: suffix token i of a request with P cached
 // tokens sees keys 0..P+i).  Tiles are 256 columns wide, 128 when no request of the batch has
-// more than 128 columns (short suffixes) and 32 when none has more than 32 (decode-like
-// batches), so that work-groups compute on few empty columns.  When a batch has fewer tiles than compute units (short suffixes over long cached
+// more than 128 columns (short suffixes, decode-like batches), so that work-groups compute on
+// fewer empty columns.  When a batch has fewer tiles than compute units (short suffixes over long cached
 // prefixes), tiles are split along the key range so that the whole batch runs as one round of
 // at most one item per compute unit: the smallest cap on key tiles per item (at least 8, i.e.
 // 512 keys) for which the pieces fit, each tile cut into equal pieces under the cap.  Split
@@ -65,9 +65,7 @@ extern "C" int32_t arckv_attention_plan(const int32_t* cu_q, const int32_t* seq_
   int64_t max_cols = 0;
   for (int32_t r = 0; r < n_reqs; ++r)
     max_cols = std::max<int64_t>(max_cols, (static_cast<int64_t>(cu_q[r + 1]) - cu_q[r]) * G);
-  const int kCols = max_cols <= arckv::kTinyCols     ? arckv::kTinyCols
-                    : max_cols <= arckv::kNarrowCols ? arckv::kNarrowCols
-                                                     : arckv::kWideCols;
+  const int kCols = max_cols <= arckv::kNarrowCols ? arckv::kNarrowCols : arckv::kWideCols;
   *tile_cols = kCols;
 
   struct Tile { int32_t req, kvh, col_start, kv_end; };

@@ -10,13 +10,12 @@
 namespace arckv {
 
 // Query columns (token x query head of one KV group) per attention work-group, shared by the
-// host work plan and the kernel: wide tiles (8 waves x 32 columns), narrow tiles for short
-// suffixes (4 x 32 columns, the 8 waves split over the keys of each K/V tile) and tiny tiles
-// for decode-like batches (32 columns, 2 waves split over the keys).
+// host work plan and the kernel: wide tiles (8 waves x 32 columns) and narrow tiles for short
+// suffixes and decode-like batches (4 x 32 columns, the 8 waves split over the keys of each
+// K/V tile).
 constexpr int kWaveCols = 32;
 constexpr int kWideCols = 8 * kWaveCols;
 constexpr int kNarrowCols = 4 * kWaveCols;
-constexpr int kTinyCols = kWaveCols;
 // Longest key range of one attention work item: longer ranges are split into pieces (merged by
 // the combine), so that the item's block-table entries (kMaxItemKeys / 16) fit in LDS.
 constexpr int kMaxItemKeys = 65536;

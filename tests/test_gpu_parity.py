@@ -162,7 +162,7 @@ SWEEP = [
     ([(L, L - 1) for L in (1, 2, 17, 64, 65, 300, 1024, 2049, 4097, 777, 33, 16)], 32, 8, 128),
     ([(L, L - 2) for L in (2, 3, 40, 129, 1500, 3001)], 16, 2, 64),
     # G = 4 at d = 64; column counts on and just past each tile width (32, 128, 256 columns)
-    ([(900, 892), (70, 62)], 8, 2, 64),                 # 32 columns: tiny tiles
+    ([(900, 892), (70, 62)], 8, 2, 64),                 # 32 columns (narrow tiles)
     ([(900, 891), (77, 68)], 8, 2, 64),                 # 36 columns: narrow tiles
     ([(700, 668), (1000, 968)], 16, 4, 64),             # 128 columns: narrow tiles
     ([(700, 667), (64, 31)], 16, 4, 64),                # 132 columns: wide tiles
@@ -172,7 +172,7 @@ SWEEP = [
     ([(1040, 1024), (300, 16), (77, 0)], 40, 8, 128),
     ([(4000, 3949), (130, 78), (6, 0)], 40, 8, 128),    # 255, 260 and 30 columns
     ([(700, 600), (33, 0), (1, 0)], 10, 2, 64),
-    ([(L, L - 1) for L in (1, 17, 300, 4097, 65, 2000)], 40, 8, 128),   # decode: tiny tiles
+    ([(L, L - 1) for L in (1, 17, 300, 4097, 65, 2000)], 40, 8, 128),   # decode (narrow tiles)
     ([(40000, 39999)], 8, 1, 64),        # 79 pieces of one tile: the combine's second batch of 64
 ]
 

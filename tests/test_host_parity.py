@@ -267,7 +267,7 @@ def attention_plan_coverage(cu_q, seq_lens, hq, hkv, d, num_cus):
     g = hq // hkv
     tc = ap.tile_cols
     max_cols = max(int(cu_q[r + 1] - cu_q[r]) * g for r in range(len(seq_lens)))
-    assert tc == (32 if max_cols <= 32 else 128 if max_cols <= 128 else 256)
+    assert tc == (128 if max_cols <= 128 else 256)
     items = ap.work[: ap.n_work]
     comb = ap.work[ap.n_work: ap.n_work + ap.n_combine]
     cover, n_live, n_slots, max_piece = {}, 0, 0, 0

@@ -45,7 +45,7 @@ CASES = [
     ([(9000, 8872), (4000, 3872)], 32, 8, 128, 256),                   # wide tiles, 32 MiB of partials
     ([(5000, 4990), (3000, 2990), (2100, 2068)], 32, 8, 128, 100000),  # narrow tiles
     ([(1040, 1024), (600, 500)], 32, 8, 128, 256),
-    ([(L, L - 1) for L in (300, 4097, 2000, 65)], 40, 8, 128, 256),    # decode-like: tiny tiles
+    ([(L, L - 1) for L in (300, 4097, 2000, 65)], 40, 8, 128, 256),    # decode-like batch
 ]
 
 
