@@ -884,19 +884,21 @@ __global__ __launch_bounds__(512, 1) void prefill_attn_pp_kernel(
   auto barrier_wait = [&](int) {   // the one tile issued after the awaited one may be in flight
     asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(2 * NLD) : "memory");
   };
-  if (ntiles > 0) {
-    for (int t = 0; t < kStages - 1; ++t)
-      if (t < ntiles) load_tile_global(t);
-  }
-  // the table, Q loads and tiles 0..2: one vmcnt(0) covers them all (tile 0 is read in half
-  // step 0); the barrier also publishes the table
+  // The table, the Q loads and tile 0 (read in half step 0): one vmcnt(0) covers them (an
+  // instruction the compiler's wait insertion understands, so it adds none of its own before
+  // Q is used).  Tiles 1 and 2 go out after it, to arrive while S(0) is computed: the waits
+  // in the loop already leave one tile in flight beyond the one a phase reads.  The barrier
+  // publishes the table without waiting for those loads.
+  if (ntiles > 0) load_tile_global(0);
   __builtin_amdgcn_s_waitcnt(0x0F70);
+  for (int t = 1; t < kStages - 1; ++t)
+    if (t < ntiles) load_tile_global(t);
 #pragma unroll
   for (int k = 0; k < kTblPer; ++k) {
     const int e = tid + k * kThreads;
     if (e < n_tbl) tbl[e] = tbl_v[k];
   }
-  __syncthreads();
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
   fetch_next(kStages - 1);
   if (ntiles > 0) {
     const int e_tile = (L - kv_lo + kBK - 1) / kBK - 1;   // the tile holding key L - 1

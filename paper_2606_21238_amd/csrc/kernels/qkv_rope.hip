@@ -27,6 +27,7 @@
 // L_r - S_r + i).
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 
 #include "../host/internal.hpp"
@@ -66,27 +67,37 @@ __device__ __forceinline__ void load_lds16(const void* base, uint32_t ofs, lds_v
                : "memory", "m0");
 }
 
-// (cos, sin) of every token's D/2 rotary angles: tab[t][i], i < D/2.
+// (cos, sin) of every token's D/2 rotary angles: tab[t][i], i < D/2.  A work-group computes
+// the D/2 frequencies once (fp64 pow) and then walks tokens grid-stride, 256 / (D/2) at a
+// time; the angle p f is reduced mod 2 pi in fp64 (k = floor(a / 2 pi), a - 2 pi k in one
+// fma), then fp32 sine and cosine.
+constexpr int kTableBlocks = 1024;
 template <int D>
 __global__ __launch_bounds__(256) void rope_table_kernel(int64_t n_tokens, const int32_t* __restrict__ cu_q,
                                                           const int32_t* __restrict__ seq_lens, int n_reqs,
                                                           double theta, float2* __restrict__ tab) {
   constexpr int HALF = D / 2;
-  const int64_t e = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
-  if (e >= n_tokens * HALF) return;
-  const int64_t t = e / HALF;
-  const int i = static_cast<int>(e % HALF);
-  int lo = 0, hi = n_reqs - 1;            // request of token t: the last r with cu_q[r] <= t
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) / 2;
-    if (cu_q[mid] <= t) lo = mid; else hi = mid - 1;
+  constexpr int kTokPer = 256 / HALF;     // tokens per pass of the work-group
+  constexpr double kTwoPi = 6.283185307179586476925;
+  __shared__ double freq[HALF];
+  if (threadIdx.x < HALF) freq[threadIdx.x] = std::pow(theta, -2.0 * static_cast<int>(threadIdx.x) / D);
+  __syncthreads();
+  const int i = threadIdx.x % HALF;
+  const double f = freq[i];
+  for (int64_t t = static_cast<int64_t>(blockIdx.x) * kTokPer + threadIdx.x / HALF; t < n_tokens;
+       t += static_cast<int64_t>(gridDim.x) * kTokPer) {
+    int lo = 0, hi = n_reqs - 1;          // request of token t: the last r with cu_q[r] <= t
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) / 2;
+      if (cu_q[mid] <= t) lo = mid; else hi = mid - 1;
+    }
+    const int64_t p = static_cast<int64_t>(seq_lens[lo]) - (cu_q[lo + 1] - cu_q[lo]) + (t - cu_q[lo]);
+    const double a = static_cast<double>(p) * f;
+    const double r = std::fma(-std::floor(a / kTwoPi), kTwoPi, a);
+    float sn, cs;
+    sincosf(static_cast<float>(r), &sn, &cs);
+    tab[t * HALF + i] = make_float2(cs, sn);
   }
-  const int64_t p = static_cast<int64_t>(seq_lens[lo]) - (cu_q[lo + 1] - cu_q[lo]) + (t - cu_q[lo]);
-  const double f = std::pow(theta, -2.0 * i / D);
-  const double a = std::fmod(static_cast<double>(p) * f, 6.283185307179586476925);
-  float s, c;
-  sincosf(static_cast<float>(a), &s, &c);
-  tab[e] = make_float2(c, s);
 }
 
 template <int D>
@@ -283,7 +294,7 @@ extern "C" int32_t arckv_qkv_rope(const void* x, const void* w_qkv, int64_t n_to
                        (long long)tab_bytes);
   auto* s = static_cast<hipStream_t>(stream);
   auto* tab = static_cast<float2*>(workspace);
-  const dim3 tgrid(static_cast<unsigned>((n_tokens * (head_dim / 2) + 255) / 256));
+  const dim3 tgrid(static_cast<unsigned>(std::min<int64_t>(kTableBlocks, (n_tokens * (head_dim / 2) + 255) / 256)));
   const int64_t n_tiles_n = (n_out + kTN - 1) / kTN;
   const dim3 grid(static_cast<unsigned>(n_tiles_n * ((n_tokens + kTM - 1) / kTM)));
   auto* xp = static_cast<const uint16_t*>(x);
