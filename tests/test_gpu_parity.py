@@ -346,23 +346,25 @@ def test_docqa_stream_batches():
         compare(got, ref, f"docqa batch {a}")
 
 
-def test_short32_full_batches():
-    """The short32 bench shape: 16 cached lognormal histories + 32 new tokens each."""
+@pytest.mark.parametrize("S", [32, 48, 64])
+def test_short_full_batches(S):
+    """The short32 / short48 / short64 bench shapes: 16 cached lognormal histories + S new
+    tokens each (128-column tiles at S = 32, 256-column tiles above)."""
     cfg = get_config("short")
-    print_case("config short32 (16 x (history + 32)), row-sampled, native prepare")
+    print_case(f"config short{S} (16 x (history + {S})), row-sampled, native prepare")
     ls = Lockstep(cfg)
-    warm, steps = steps_short(cfg, 2, 32)
-    rng = np.random.default_rng(6)
+    warm, steps = steps_short(cfg, 2, S)
+    rng = np.random.default_rng(6 + S)
     for w in warm:
         ls.batch(w, rows_fn=lambda r, p: [0, int(p.cu_q[r + 1] - p.cu_q[r]) - 1], native_prepare=True)
     for k, b in enumerate(steps):
-        plan, got, ref = ls.batch(b, rows_fn=lambda r, p: sample_rows(32, rng, 8), native_prepare=True)
-        assert all(s == 32 for s in np.diff(plan.cu_q))
-        compare(got, ref, f"short32 step {k}")
+        plan, got, ref = ls.batch(b, rows_fn=lambda r, p: sample_rows(S, rng, 8), native_prepare=True)
+        assert all(s == S for s in np.diff(plan.cu_q))
+        compare(got, ref, f"short{S} step {k}")
 
 
 def test_decode_full_batch():
-    """The decode bench shape: 64 cached lognormal histories + 1 new token each (32-column
+    """The decode bench shape: 64 cached lognormal histories + 1 new token each (128-column
     tiles, split key ranges), every row checked."""
     cfg = get_config("decode")
     print_case("config decode (64 x (history + 1)), all rows, native prepare")

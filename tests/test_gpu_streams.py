@@ -107,15 +107,15 @@ def test_multiturn_stream():
     base = get_config("multiturn")
     reqs, cap = stream_multiturn(base)
     cfg = sized(base, cap)
-    print_case(f"config multiturn: {len(reqs)} requests, capacity {cap} blocks, checks 1 batch in 8")
-    run, n = run_stream(cfg, reqs, 8, 96, seed=31)
+    print_case(f"config multiturn: {len(reqs)} requests, capacity {cap} blocks, checks 1 batch in 4")
+    run, n = run_stream(cfg, reqs, 4, 96, seed=31)
     print(f"multiturn: {n} batches, hit tokens {run.hit_tokens}, rows checked {run.rows_checked}", flush=True)
     assert run.hit_tokens > 0
 
 
 def test_trace_replay_window():
     base = get_config("trace")
-    reqs, cap = stream_trace(base, 640)
+    reqs, cap = stream_trace(base, 1280)
     cfg = sized(base, cap)
     print_case(f"config trace: first {len(reqs)} requests, capacity {cap} blocks, checks 1 batch in 5")
     run, n = run_stream(cfg, reqs, 5, 48, seed=51)
