@@ -80,6 +80,23 @@ extern "C" {
 #define ARCKV_LIST_B1 3
 #define ARCKV_LIST_B2 4
 
+/* Device checks (a debug build: paper_2606_21238_amd.build with checked=True writes
+ * lib/libarckv_checked.so, its kernels compiled with ARCKV_DEVICE_CHECKS).  Where a kernel
+ * clamps or skips an out-of-range index it also records the kind, per device:
+ *   ARCKV_CHECK_SLOT   a KV scatter slot outside [0, 16 num_blocks) (the token is skipped);
+ *   ARCKV_CHECK_BLOCK  an attention block-table entry outside [0, num_blocks) among the blocks
+ *                      of a request (block 0 is read in its place);
+ *   ARCKV_CHECK_WORK   an attention or combine work item naming no request, KV head or
+ *                      column of the batch (skipped; the idle items of a plan are not this).
+ * arckv_device_checks waits for `stream`, stores the OR of the kinds recorded on the current
+ * device since the last reset and the number of records (a bad index may be recorded by
+ * several waves), and clears them when reset != 0 (not for use under graph capture).  In a
+ * build without device checks it returns EUNSUPPORTED; nothing in the kernels traps. */
+#define ARCKV_CHECK_SLOT 1
+#define ARCKV_CHECK_BLOCK 2
+#define ARCKV_CHECK_WORK 4
+int32_t arckv_device_checks(int32_t* bits, int64_t* count, int32_t reset, void* stream);
+
 /* Thread-local message describing the last failing call on this thread. */
 const char* arckv_last_error(void);
 /* Library ABI version (the pool layout version is ARCKV_LAYOUT_V1). */

@@ -316,6 +316,18 @@ def _dev(t, dtype_bits: int | None = None, name: str = "tensor"):
     return C.c_void_p(t.data_ptr())
 
 
+def device_checks(reset: bool = True, stream=None, library=None):
+    """(bits, count) of the out-of-range indices the kernels recorded on the current device
+    (arckv_device_checks; CHECK_SLOT | CHECK_BLOCK | CHECK_WORK) and clears them if `reset`.
+    `library`: a handle from _lib.load() of the checked build (lib/libarckv_checked.so);
+    default the loaded library.  Raises EUNSUPPORTED for a build without device checks."""
+    L = library or lib()
+    bits, count = _lib.i32(), _lib.i64()
+    _lib.check(L.arckv_device_checks(C.byref(bits), C.byref(count), 1 if reset else 0,
+                                     C.c_void_p(_stream(stream))), "arckv_device_checks")
+    return int(bits.value), int(count.value)
+
+
 def kv_scatter(k_pool, v_pool, k_new, v_new, slot_mapping, stream=None):
     """pool[slot[t]] <- (k_new[t], v_new[t]); pools [blocks, Hkv, 16, D] / [blocks, Hkv, D, 16]."""
     nb, hkv = int(k_pool.shape[0]), int(k_pool.shape[1])

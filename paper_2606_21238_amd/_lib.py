@@ -14,6 +14,7 @@ STATUS_NAMES = {0: "OK", -1: "EINVAL", -2: "ENOSPC", -3: "EDEVICE", -4: "ESTATE"
 POLICY = {"arc": 0, "lru": 1, "dbl": 2, "frc": 3}
 REF_ORDER = {"tail_first": 0, "head_first": 1}
 WORK_INTS = 8
+CHECK_SLOT, CHECK_BLOCK, CHECK_WORK = 1, 2, 4
 
 i32, i64, u64, f32, f64, vp = C.c_int32, C.c_int64, C.c_uint64, C.c_float, C.c_double, C.c_void_p
 P_i32, P_i64, P_u64 = C.POINTER(i32), C.POINTER(i64), C.POINTER(u64)
@@ -61,6 +62,7 @@ _SIGS = {
     "arckv_hash_blocks": (i32, [P_i32, i64, u64, P_u64, i64, P_i64]),
     "arckv_hash_blocks_batch": (i32, [C.POINTER(P_i32), P_i64, i32, u64, P_u64, i64, P_i64]),
     "arckv_digest_blocks": (i32, [P_i32, i64, u64, P_u64, i64, P_i64]),
+    "arckv_device_checks": (i32, [C.POINTER(i32), P_i64, i32, vp]),
     "arckv_test_set_hash_mask": (i32, [u64, P_u64]),
     "arckv_cache_create": (i32, [C.POINTER(CacheCfg), C.POINTER(vp)]),
     "arckv_cache_destroy": (i32, [vp]),

@@ -45,15 +45,20 @@ def _run(cmd):
 SANITIZE = ["-fsanitize=address,undefined", "-fno-sanitize-recover=undefined", "-fno-omit-frame-pointer"]
 ASAN_BUILD = os.path.join(PKG, "_build_sanitize")
 ASAN_LIB = os.path.join(LIBDIR, "libarckv_sanitize.so")
+CHECKED_BUILD = os.path.join(PKG, "_build_checked")
+CHECKED_LIB = os.path.join(LIBDIR, "libarckv_checked.so")
 
 
-def build(verbose: bool = False, sanitize: bool = False) -> str:
+def build(verbose: bool = False, sanitize: bool = False, checked: bool = False) -> str:
     """sanitize: the host C++ (hashing, cache, planner, batch preparation) instrumented with
     AddressSanitizer and UndefinedBehaviorSanitizer, into lib/libarckv_sanitize.so, for CPU tests
     (load it with ARCKV_LIBRARY and the sanitizer runtimes preloaded).  The HIP sources are
-    built as usual, with no sanitizer: device code is never instrumented."""
-    build_dir = ASAN_BUILD if sanitize else BUILD
-    out_lib = ASAN_LIB if sanitize else LIB
+    built as usual, with no sanitizer: device code is never instrumented.
+    checked: the kernels with device checks (ARCKV_DEVICE_CHECKS: out-of-range indices they
+    clamp or skip are recorded, see arckv_device_checks), into lib/libarckv_checked.so."""
+    assert not (sanitize and checked)
+    build_dir = ASAN_BUILD if sanitize else CHECKED_BUILD if checked else BUILD
+    out_lib = ASAN_LIB if sanitize else CHECKED_LIB if checked else LIB
     os.makedirs(build_dir, exist_ok=True)
     os.makedirs(LIBDIR, exist_ok=True)
     hipcc = _hipcc()
@@ -67,7 +72,7 @@ def build(verbose: bool = False, sanitize: bool = False) -> str:
         objs.append(obj)
     for src in HIP_SRC:
         obj = os.path.join(build_dir, os.path.basename(src) + ".o")
-        jobs.append([hipcc, f"--offload-arch={ARCH}", *common,
+        jobs.append([hipcc, f"--offload-arch={ARCH}", *common, *(["-DARCKV_DEVICE_CHECKS"] if checked else []),
                      # no packed fp32 VALU ops are ever generated: some of their forms have given wrong results on gfx950
                      "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
                      "-c", os.path.join(CSRC, src), "-o", obj])
@@ -90,4 +95,4 @@ def build(verbose: bool = False, sanitize: bool = False) -> str:
 
 
 if __name__ == "__main__":
-    print(build(verbose="-v" in sys.argv, sanitize="--sanitize" in sys.argv))
+    print(build(verbose="-v" in sys.argv, sanitize="--sanitize" in sys.argv, checked="--checked" in sys.argv))

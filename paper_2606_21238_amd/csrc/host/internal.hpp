@@ -23,6 +23,14 @@ constexpr int kMaxItemKeys = 65536;
 // Whether the cache was created in check mode (block digests verified by every plan).
 bool cache_checks_blocks(const arckv_cache* c);
 
+// Device checks (a build with ARCKV_DEVICE_CHECKS defined): a kernel that clamps or skips an
+// out-of-range index also records it in a per-device word pair of its source file (bits OR-ed,
+// occurrences counted).  Each kernel source provides a reader: it waits for `stream`, reads
+// the pair of the current device and, if reset, clears it.  Without device checks they return
+// ARCKV_EUNSUPPORTED.
+int32_t read_scatter_checks(void* stream, bool reset, uint32_t* bits, uint32_t* count);
+int32_t read_attention_checks(void* stream, bool reset, uint32_t* bits, uint32_t* count);
+
 // Records a thread-local message for arckv_last_error() and returns `code`.
 int32_t fail(int32_t code, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
 void clear_error();

@@ -19,6 +19,7 @@
 #include <hip/hip_runtime.h>
 
 #include "../host/internal.hpp"
+#include "device_checks.hpp"
 
 namespace {
 
@@ -46,6 +47,7 @@ __global__ __launch_bounds__(kThreads) void kv_scatter_kernel(
   if (tid < kTok) {
     const int64_t t = t0 + tid;
     const int32_t s = t < n_tokens ? slots[t] : -1;
+    ARCKV_CHECK_LANE(t < n_tokens && !(s >= 0 && s < n_slots), ARCKV_CHECK_SLOT);
     sslot[tid] = (s >= 0 && s < n_slots) ? s : -1;
   }
   __syncthreads();
@@ -109,6 +111,8 @@ __global__ __launch_bounds__(kThreads) void kv_scatter_kernel(
 }
 
 }  // namespace
+
+ARCKV_DEFINE_CHECK_READER(read_scatter_checks)
 
 extern "C" int32_t arckv_kv_scatter(void* k_pool, void* v_pool, const void* k_new,
                                     const void* v_new, const int32_t* slot_mapping,

@@ -43,6 +43,7 @@
 #include <type_traits>
 
 #include "../host/internal.hpp"
+#include "device_checks.hpp"
 
 namespace {
 
@@ -147,6 +148,9 @@ __global__ __launch_bounds__(64 * NW, 1) void prefill_attn_kernel(
   if (n_q <= 0) return;
 
   const Work w = work[blockIdx.x];
+  // an idle item (request -1) pads the XCD phase; anything else out of range is malformed
+  ARCKV_CHECK_WAVE(w.req >= n_reqs || (w.req >= 0 && (w.kvh < 0 || w.kvh >= hkv || w.col_start < 0)),
+                   ARCKV_CHECK_WORK);
   if (w.req < 0 || w.req >= n_reqs || w.kvh < 0 || w.kvh >= hkv || w.col_start < 0) return;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -243,6 +247,7 @@ __global__ __launch_bounds__(64 * NW, 1) void prefill_attn_kernel(
     fetch_ph(tile + 1);
 #pragma unroll
     for (int i = 0; i < NLD; ++i) {
+      ARCKV_CHECK_WAVE(ph[i] < 0 || ph[i] >= num_blocks, ARCKV_CHECK_BLOCK);
       const int32_t pb = (ph[i] < 0 || ph[i] >= num_blocks) ? 0 : ph[i];  // never used unmasked
       const int64_t base = static_cast<int64_t>(pb) * blk_stride + head_k;
       load_lds16(k_pool + base + k_off[i], (lds_void*)(st + i * LDB + wave * 1024));
@@ -619,6 +624,9 @@ __global__ __launch_bounds__(512, 1) void prefill_attn_pp_kernel(
   __shared__ int32_t tbl[kTbl];
 
   const Work w = work[blockIdx.x];
+  // an idle item (request -1) pads the XCD phase; anything else out of range is malformed
+  ARCKV_CHECK_WAVE(w.req >= n_reqs || (w.req >= 0 && (w.kvh < 0 || w.kvh >= hkv || w.col_start < 0)),
+                   ARCKV_CHECK_WORK);
   if (w.req < 0 || w.req >= n_reqs || w.kvh < 0 || w.kvh >= hkv || w.col_start < 0) return;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -692,6 +700,7 @@ __global__ __launch_bounds__(512, 1) void prefill_attn_pp_kernel(
     char* st = smem + (tile % kStages) * 2 * TILE;
 #pragma unroll
     for (int i = 0; i < NLD; ++i) {
+      ARCKV_CHECK_WAVE(ph[i] < 0 || ph[i] >= num_blocks, ARCKV_CHECK_BLOCK);
       const int32_t pb = (ph[i] < 0 || ph[i] >= num_blocks) ? 0 : ph[i];  // never used unmasked
       const int64_t base = static_cast<int64_t>(pb) * blk_stride + head_k;
       load_lds16(k_pool + base + k_off[i], (lds_void*)(st + i * LDB + wave * 1024));
@@ -810,6 +819,7 @@ __global__ __launch_bounds__(512, 1) void prefill_attn_pp_kernel(
 #pragma unroll
       for (int i = 0; i < NLD; ++i) {
         const int32_t ph = __builtin_amdgcn_readlane(next_v, i);
+        ARCKV_CHECK_WAVE(ph < 0 || ph >= num_blocks, ARCKV_CHECK_BLOCK);
         const int32_t pb = (ph < 0 || ph >= num_blocks) ? 0 : ph;  // never used unmasked
         const int64_t base = static_cast<int64_t>(pb) * blk_stride + head_k;
         ld_src[2 * i] = k_pool + base + k_off[i];
@@ -1001,9 +1011,10 @@ __global__ __launch_bounds__(kCombineThreads) void attn_combine_kernel(
   __shared__ float mx[kCombineCols], inv[kCombineCols];
   const Work w = items[blockIdx.x];  // {req, kvh, col_start, slot0, n_splits}
   const int slot0 = w.kv_start, ns = w.kv_end;
-  if (w.req < 0 || w.req >= n_reqs || w.kvh < 0 || (w.kvh + 1) * G > hq || w.col_start < 0 ||
-      slot0 < 0 || ns < 1 || slot0 + ns > ws_slots)
-    return;
+  const bool bad = w.req < 0 || w.req >= n_reqs || w.kvh < 0 || (w.kvh + 1) * G > hq || w.col_start < 0 ||
+                  slot0 < 0 || ns < 1 || slot0 + ns > ws_slots;
+  ARCKV_CHECK_WAVE(bad, ARCKV_CHECK_WORK);
+  if (bad) return;
   const int q0 = cu_q[w.req];
   const int ncols = (cu_q[w.req + 1] - q0) * G;
   const int c0 = blockIdx.y * kCombineCols;  // first local column of this block
@@ -1216,6 +1227,20 @@ int32_t prefill_attention(const void* k_pool, const void* v_pool, const void* q,
 }
 
 }  // namespace
+
+ARCKV_DEFINE_CHECK_READER(read_attention_checks)
+
+extern "C" int32_t arckv_device_checks(int32_t* bits, int64_t* count, int32_t reset, void* stream) {
+  if (bits == nullptr || count == nullptr) return arckv::fail(ARCKV_EINVAL, "device_checks: NULL output");
+  uint32_t b1 = 0, c1 = 0, b2 = 0, c2 = 0;
+  int32_t st = arckv::read_scatter_checks(stream, reset != 0, &b1, &c1);
+  if (st != ARCKV_OK) return st;
+  st = arckv::read_attention_checks(stream, reset != 0, &b2, &c2);
+  if (st != ARCKV_OK) return st;
+  *bits = static_cast<int32_t>(b1 | b2);
+  *count = static_cast<int64_t>(c1) + c2;
+  return ARCKV_OK;
+}
 
 extern "C" int32_t arckv_prefill_attention(const void* k_pool, const void* v_pool, const void* q,
                                            void* out, const int32_t* block_tables,

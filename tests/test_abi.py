@@ -80,3 +80,15 @@ def test_qkv_rope_validates_arguments_without_touching_a_device():
     # the workspace holds 4 tokens x 64 (cos, sin) pairs of fp32: one byte short is refused
     assert L.arckv_qkv_rope(a, a, 4, 64, 4, 2, 128, a, a, 1, 1.0e6, a, 4 * 4 * 128 - 1, a, a, a,
                             None) == _lib.ENOSPC
+
+
+def test_device_checks_only_in_the_checked_build():
+    """The product build has no device checks (EUNSUPPORTED, no GPU touched); the checked
+    debug build exists beside it and exports the same calls."""
+    bits, count = _lib.i32(), _lib.i64()
+    assert ak.lib().arckv_device_checks(bits, count, 0, None) == _lib.EUNSUPPORTED
+    assert b"without" in ak.lib().arckv_last_error()
+    from paper_2606_21238_amd.build import CHECKED_LIB
+    chk = _lib.load(CHECKED_LIB)
+    for name in _lib._SIGS:
+        assert hasattr(chk, name), name
