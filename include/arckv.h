@@ -273,6 +273,21 @@ int32_t arckv_cache_log_count(const arckv_cache* cache, int64_t* n);
 int32_t arckv_cache_snapshot(const arckv_cache* cache, int32_t list, uint64_t* keys,
                              int32_t* phys, int64_t cap, int64_t* n);
 
+/* Checkpoint / resume, so that a long replay (e.g. the 10,000-request trace) can stop and go
+ * on.  arckv_cache_save writes the whole state of a cache with no batch in flight into buf
+ * (host, caller-owned, cap bytes): its configuration, p, the four lists from LRU to MRU with
+ * each entry's identity, physical block, prompt depth and digest, the page free list, the
+ * scratch FIFO and the counters, as a self-contained image of little-endian 64-bit words.
+ * *n receives the image size in bytes (buf = NULL: size only).  ESTATE if a batch is in
+ * flight; ENOSPC if cap < *n.  arckv_cache_restore creates a cache from such an image; every
+ * later call on it behaves exactly as on the cache that was saved (the same decisions,
+ * placements, plans and statistics).  The decision-log buffer is not part of the state, nor
+ * are the device pools: their physical block numbers are what the image refers to, so a caller
+ * that checkpoints a serving process keeps the pools (or copies of them) beside the image.
+ * EINVAL if the image is malformed or inconsistent (nothing is created then). */
+int32_t arckv_cache_save(const arckv_cache* cache, void* buf, int64_t cap, int64_t* n);
+int32_t arckv_cache_restore(const void* buf, int64_t n, arckv_cache** out);
+
 /* ---------------------------------------------------------------------------------------
  * Device: KV scatter (Sec. 3: the engine processes a miss by regenerating the block).
  * ------------------------------------------------------------------------------------- */

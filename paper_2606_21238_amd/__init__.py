@@ -20,6 +20,8 @@ from ._lib import ArckvError, SYMBOLS, WORK_INTS  # noqa: F401
 BLOCK_TOKENS = 16
 NOALLOC_MAX_WS_BYTES = 64 << 20     # ARCKV_NOALLOC_MAX_WS_BYTES: the static scratch of prefill_attention_noalloc
 LIST_T1, LIST_T2, LIST_B1, LIST_B2 = 1, 2, 3, 4
+# ARCKV_CASE_*: indices of stats()["case_counts"] and Event.kase
+CASE_I, CASE_II, CASE_III, CASE_IVA, CASE_IVA_T1DEL, CASE_IVB, CASE_LRU_HIT, CASE_LRU_MISS = range(8)
 
 
 def lib():
@@ -145,6 +147,29 @@ class BlockCache:
         self._h = h
         self._log = None
         self.capacity = capacity
+
+    def save(self) -> bytes:
+        """The cache's whole state between batches as a byte image (arckv_cache_save)."""
+        n = _lib.i64()
+        _lib.check(lib().arckv_cache_save(self._h, None, 0, C.byref(n)), "arckv_cache_save")
+        buf = C.create_string_buffer(n.value)
+        _lib.check(lib().arckv_cache_save(self._h, buf, n.value, C.byref(n)), "arckv_cache_save")
+        return buf.raw[: n.value]
+
+    @classmethod
+    def restore(cls, image: bytes) -> "BlockCache":
+        """A cache that continues exactly where the saved one stopped (arckv_cache_restore)."""
+        h = C.c_void_p()
+        buf = C.create_string_buffer(bytes(image), len(image))
+        _lib.check(lib().arckv_cache_restore(buf, len(image), C.byref(h)), "arckv_cache_restore")
+        self = cls.__new__(cls)
+        self._order = None
+        self._h = h
+        self._log = None
+        st = _lib.Stats()
+        _lib.check(lib().arckv_cache_stats(h, C.byref(st)), "arckv_cache_stats")
+        self.capacity = int(st.capacity)
+        return self
 
     def close(self):
         if getattr(self, "_h", None) is not None and self._h.value:

@@ -63,6 +63,8 @@ _SIGS = {
     "arckv_hash_blocks_batch": (i32, [C.POINTER(P_i32), P_i64, i32, u64, P_u64, i64, P_i64]),
     "arckv_digest_blocks": (i32, [P_i32, i64, u64, P_u64, i64, P_i64]),
     "arckv_device_checks": (i32, [C.POINTER(i32), P_i64, i32, vp]),
+    "arckv_cache_save": (i32, [vp, vp, i64, P_i64]),
+    "arckv_cache_restore": (i32, [vp, i64, C.POINTER(vp)]),
     "arckv_test_set_hash_mask": (i32, [u64, P_u64]),
     "arckv_cache_create": (i32, [C.POINTER(CacheCfg), C.POINTER(vp)]),
     "arckv_cache_destroy": (i32, [vp]),

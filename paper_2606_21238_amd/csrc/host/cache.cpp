@@ -675,3 +675,149 @@ extern "C" int32_t arckv_cache_snapshot(const arckv_cache* c, int32_t list, uint
 }
 
 bool arckv::cache_checks_blocks(const arckv_cache* c) { return c != nullptr && c->check_blocks; }
+
+// -------------------------------------------------------------------------------------------
+// Checkpoint / resume: the whole state between batches as a flat little-endian image of
+// 64-bit words (identities and digests as unsigned, the rest as signed, p as its IEEE bits).
+// -------------------------------------------------------------------------------------------
+
+namespace {
+
+constexpr uint64_t kImageMagic = 0x31304356'4B435241ull;  // "ARCKVC01"
+constexpr int64_t kImageVersion = 1;
+
+struct Writer {
+  uint64_t* out;
+  int64_t cap, n = 0;
+  void put(uint64_t v) {
+    if (out != nullptr && n < cap) out[n] = v;
+    ++n;
+  }
+  void put_i(int64_t v) { put(static_cast<uint64_t>(v)); }
+};
+
+struct Reader {
+  const uint64_t* in;
+  int64_t n, i = 0;
+  bool ok = true;
+  uint64_t get() {
+    if (i >= n) { ok = false; return 0; }
+    return in[i++];
+  }
+  int64_t get_i() { return static_cast<int64_t>(get()); }
+};
+
+}  // namespace
+
+extern "C" int32_t arckv_cache_save(const arckv_cache* c, void* buf, int64_t cap, int64_t* n) {
+  if (c == nullptr || n == nullptr || cap < 0) return arckv::fail(ARCKV_EINVAL, "cache_save: bad arguments");
+  if (c->in_flight) return arckv::fail(ARCKV_ESTATE, "cache_save: a batch is in flight");
+  Writer w{static_cast<uint64_t*>(buf), buf == nullptr ? 0 : cap / 8};
+  w.put(kImageMagic);
+  w.put_i(kImageVersion);
+  for (int64_t v : {static_cast<int64_t>(c->policy), static_cast<int64_t>(c->ref_order),
+                    static_cast<int64_t>(c->window), static_cast<int64_t>(c->intra_batch_reuse),
+                    static_cast<int64_t>(c->check_blocks), c->c, c->num_phys, c->n_scratch})
+    w.put_i(v);
+  w.put(__builtin_bit_cast(uint64_t, c->p));
+  for (int64_t v : {c->references, c->requests, c->prompt_tokens, c->prefix_hit_tokens, c->computed_tokens})
+    w.put_i(v);
+  for (int64_t v : c->case_counts) w.put_i(v);
+  for (int list = ARCKV_LIST_T1; list <= ARCKV_LIST_B2; ++list) {
+    w.put_i(c->lists[list].size);
+    for (int32_t x = c->lists[list].head; x >= 0; x = c->nodes[x].next) {
+      const Node& nd = c->nodes[x];
+      w.put(nd.key);
+      w.put_i(nd.phys);
+      w.put_i(nd.depth);
+      w.put(nd.digest);
+    }
+  }
+  w.put_i(static_cast<int64_t>(c->free_blocks.size()));
+  for (int32_t b : c->free_blocks) w.put_i(b);
+  w.put_i(static_cast<int64_t>(c->scratch_fifo.size()));
+  for (int32_t b : c->scratch_fifo) w.put_i(b);
+  w.put(kImageMagic);
+  *n = w.n * 8;
+  if (buf != nullptr && cap < *n)
+    return arckv::fail(ARCKV_ENOSPC, "cache_save: image takes %lld bytes, capacity %lld",
+                       (long long)*n, (long long)cap);
+  return ARCKV_OK;
+}
+
+extern "C" int32_t arckv_cache_restore(const void* buf, int64_t n, arckv_cache** out) {
+  if (buf == nullptr || out == nullptr || n < 8 || n % 8 != 0)
+    return arckv::fail(ARCKV_EINVAL, "cache_restore: bad arguments");
+  *out = nullptr;
+  Reader r{static_cast<const uint64_t*>(buf), n / 8};
+  auto bad = [](const char* what) { return arckv::fail(ARCKV_EINVAL, "cache_restore: %s", what); };
+  if (r.get() != kImageMagic || r.get_i() != kImageVersion) return bad("not a cache image of this version");
+  arckv_cache_cfg cfg{};
+  cfg.policy = static_cast<int32_t>(r.get_i());
+  cfg.ref_order = static_cast<int32_t>(r.get_i());
+  cfg.victim_window = static_cast<int32_t>(r.get_i());
+  const int64_t reuse = r.get_i(), check = r.get_i();
+  cfg.no_intra_batch_reuse = reuse ? 0 : 1;
+  cfg.check_blocks = check ? 1 : 0;
+  cfg.capacity_blocks = r.get_i();
+  cfg.num_phys_blocks = r.get_i();
+  cfg.scratch_blocks = r.get_i();
+  const double p = __builtin_bit_cast(double, r.get());
+  cfg.frc_p = cfg.policy == ARCKV_POLICY_FRC ? p : 0.0;
+  if (!r.ok || (reuse != 0 && reuse != 1) || (check != 0 && check != 1)) return bad("truncated header");
+  arckv_cache* c = nullptr;
+  int32_t st = arckv_cache_create(&cfg, &c);
+  if (st != ARCKV_OK) return st;
+  auto fail = [&](const char* what) { arckv_cache_destroy(c); return bad(what); };
+  if (!(p >= 0.0 && p <= static_cast<double>(c->c))) return fail("p outside [0, c]");
+  c->p = p;
+  c->references = r.get_i();
+  c->requests = r.get_i();
+  c->prompt_tokens = r.get_i();
+  c->prefix_hit_tokens = r.get_i();
+  c->computed_tokens = r.get_i();
+  for (int64_t& v : c->case_counts) v = r.get_i();
+  std::vector<char> used(static_cast<size_t>(c->num_phys), 0);
+  auto take = [&](int64_t b) {            // a physical block named once, in range
+    if (b < 0 || b >= c->num_phys || used[b]) return false;
+    used[b] = 1;
+    return true;
+  };
+  int64_t total = 0;
+  for (int list = ARCKV_LIST_T1; list <= ARCKV_LIST_B2; ++list) {
+    const int64_t size = r.get_i();
+    total += size;
+    if (!r.ok || size < 0 || total > 2 * c->c) return fail("list sizes");      // |T1|+|T2|+|B1|+|B2| <= 2c
+    const bool resident = list == ARCKV_LIST_T1 || list == ARCKV_LIST_T2;
+    for (int64_t i = 0; i < size; ++i) {
+      const uint64_t key = r.get();
+      const int64_t phys = r.get_i(), depth = r.get_i();
+      const uint64_t digest = r.get();
+      if (!r.ok || c->find(key) >= 0) return fail("duplicate or truncated list entry");
+      if (resident ? !take(phys) : phys != -1) return fail("physical block of a list entry");
+      if (depth < 0 || depth > INT32_MAX) return fail("depth of a list entry");
+      const int32_t x = c->new_node(key, static_cast<int32_t>(phys));
+      c->nodes[x].depth = static_cast<int32_t>(depth);
+      c->nodes[x].digest = digest;
+      c->push_mru(x, list);
+    }
+  }
+  if (c->lists[ARCKV_LIST_T1].size + c->lists[ARCKV_LIST_T2].size > c->c) return fail("more pages than c");
+  c->free_blocks.clear();
+  c->scratch_fifo.clear();
+  for (std::deque<int32_t>* q : {&c->free_blocks, &c->scratch_fifo}) {
+    const int64_t size = r.get_i();
+    if (!r.ok || size < 0 || size > c->num_phys) return fail("free list sizes");
+    for (int64_t i = 0; i < size; ++i) {
+      const int64_t b = r.get_i();
+      if (!r.ok || !take(b)) return fail("free list entry");
+      q->push_back(static_cast<int32_t>(b));
+    }
+  }
+  if (static_cast<int64_t>(c->scratch_fifo.size()) != c->n_scratch) return fail("scratch FIFO size");
+  for (char u : used)
+    if (!u) return fail("a physical block is neither in a list nor free");
+  if (r.get() != kImageMagic || r.i != r.n) return fail("trailing words or missing end marker");
+  *out = c;
+  return ARCKV_OK;
+}

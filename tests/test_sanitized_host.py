@@ -1,5 +1,5 @@
 """The library's host C++ (hashing, ARC/DBL/LRU cache, planner, attention work plan, batch
-preparation) under AddressSanitizer and UndefinedBehaviorSanitizer (CPU only).
+preparation, checkpoint images) under AddressSanitizer and UndefinedBehaviorSanitizer (CPU only).
 
 Builds lib/libarckv_sanitize.so (host sources instrumented, HIP sources as usual) and re-runs
 the host parity suites against it in a child process, with the sanitizer runtimes preloaded
@@ -42,7 +42,7 @@ def test_host_suites_are_clean_under_asan_and_ubsan():
     assert probe.stdout.strip() == lib, probe.stdout + probe.stderr      # the instrumented build is the one loaded
     cmd = [sys.executable, "-m", "pytest", "-q", "-x", "-p", "no:cacheprovider", "-m", "not gpu",
            "tests/test_host_parity.py", "tests/test_prepare.py", "tests/test_host_streams.py",
-           "tests/test_collisions.py",
+           "tests/test_collisions.py", "tests/test_checkpoint.py",
            "-k", "not trace_full_replay and not trace_first_2000"]
     r = subprocess.run(cmd, cwd=ROOT, env=env, capture_output=True, text=True, timeout=1200)
     out = r.stdout + r.stderr
