@@ -27,7 +27,8 @@ plan and the attention work plan -> metadata H2D -> [Q/K/V projection, docqa14b]
 scatter -> prefill attention (+ split combine) -> release.  Each batch's computed-token Q/K/V are staged in
 HBM before the timed region (token ids stay on the host).  Printed: one JSON line with the
 algorithmic attention TFLOP/s over the whole step time (value), suffix tokens/s, the roofline
-of the attention kernel measured with HIP events on its stream, the CPU oracle timed on a
+of the attention kernel measured with HIP events on its stream (timing-only events, without
+the system-scope cache flush a default event record carries), the CPU oracle timed on a
 bounded sample, and (`policy_baseline`) the pure-Python ARC and LRU planners of the oracle
 against the library's planner over the trace-replay stream's block references.
 """
@@ -88,6 +89,62 @@ def measured_traffic(workload: str, kernel: str):
         return round(e["fetch_bytes_per_launch"] + e["write_bytes_per_launch"], 1)
     except (OSError, KeyError, ValueError):
         return None
+
+
+class TimingEvent:
+    """A HIP event for timing only, created with hipEventDisableSystemFence: recording it does
+    not write back and invalidate the caches (the system-scope fence a default event carries),
+    which would otherwise add to the kernels it brackets and slow the work that follows.  Same
+    interface as torch.cuda.Event for what the bench uses; `cuda_event` is the raw handle the
+    library's timed entry point records."""
+    _hip = None
+    DISABLE_SYSTEM_FENCE = 0x20000000
+
+    @classmethod
+    def _runtime(cls):
+        if cls._hip is None:
+            import ctypes
+            import torch  # noqa: F401  (the HIP runtime torch loaded is the one to use)
+            path = None
+            with open("/proc/self/maps") as f:
+                for line in f:
+                    if "libamdhip64.so" in line:
+                        path = line.split()[-1]
+                        break
+            if path is None:
+                raise RuntimeError("HIP runtime not loaded")
+            hip = ctypes.CDLL(path)
+            hip.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint]
+            hip.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+            hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+            hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+            cls._hip = hip
+        return cls._hip
+
+    def __init__(self):
+        import ctypes
+        self._c = ctypes
+        self.cuda_event = None
+        h = ctypes.c_void_p()
+        if self._runtime().hipEventCreateWithFlags(ctypes.byref(h), self.DISABLE_SYSTEM_FENCE) != 0:
+            raise RuntimeError("hipEventCreateWithFlags failed")
+        self.cuda_event = h.value
+
+    def record(self, stream=None):
+        import torch
+        s = (stream or torch.cuda.current_stream()).cuda_stream
+        if self._runtime().hipEventRecord(self.cuda_event, s) != 0:
+            raise RuntimeError("hipEventRecord failed")
+
+    def elapsed_time(self, other) -> float:
+        ms = self._c.c_float()
+        if self._runtime().hipEventElapsedTime(self._c.byref(ms), self.cuda_event, other.cuda_event) != 0:
+            raise RuntimeError("hipEventElapsedTime failed")
+        return float(ms.value)
+
+    def __del__(self):
+        if self.cuda_event is not None and self._hip is not None:
+            self._hip.hipEventDestroy(self.cuda_event)
 
 
 def cpu_model() -> str:
@@ -421,7 +478,7 @@ def main():
             host_t["release"] += h4 - h3
         return plan, db
 
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(steps)]
+    events = [[TimingEvent() for _ in range(5)] for _ in range(steps)]
     for evs in events:          # a first record creates each event's HIP handle
         for e in evs:
             e.record()
@@ -470,7 +527,7 @@ def main():
         per_launch = float(np.mean(B))
     hit = lambda a, b: (a["prefix_hit_tokens"] - b["prefix_hit_tokens"]) / max(
         1, a["prompt_tokens"] - b["prompt_tokens"])
-    kernel_name = "prefill_attn_pp_kernel" if widths and max(widths) == 256 else "prefill_attn_kernel"
+    kernel_name = "prefill_attn_pp_kernel" if widths and max(widths) == 256 else "prefill_attn_list_kernel"
     traffic = measured_traffic(args.workload, kernel_name)
 
     result = {
@@ -495,7 +552,7 @@ def main():
         "suffix_tokens_per_s": round(suffix_tokens / wall, 1),
         "roofline": {
             "bound": bound,
-            "kernel": kernel_name,   # 256-column tiles run the ping-pong kernel, narrower ones the key-half kernel
+            "kernel": kernel_name,   # 256-column tiles run the ping-pong kernel, 128-column ones the list kernel
             "achieved": round(achieved, 2),
             "peak": peak,
             "unit": unit,

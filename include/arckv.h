@@ -316,9 +316,12 @@ int32_t arckv_kv_scatter(void* k_pool, void* v_pool, const void* k_new, const vo
 
 /* Work decomposition (host): one work item is a query tile of *tile_cols (column = token x
  * query head of one KV group, token-major) of one (request, KV head) over a key range.
- * Long key ranges are split when the batch has too few tiles to fill num_cus compute units
- * (into one round of at most num_cus items); split tiles are merged by a log-sum-exp combine
- * pass.
+ * 256-column tiles: one work-group per item; long key ranges are split when the batch has too
+ * few tiles to fill num_cus compute units (into one round of at most num_cus items).
+ * 128-column tiles: the items are grouped into lists of 8 entries (the list's items, then idle
+ * entries with request -1), one list per work-group, balanced over at most num_cus lists;
+ * key ranges are cut where a list's share ends.  Split tiles are merged by a log-sum-exp
+ * combine pass.
  * cu_q, seq_lens: HOST copies of the plan's arrays.  work: host int32 buffer of
  * ARCKV_WORK_INTS * work_cap entries or NULL to query sizes.
  * Outputs: *n_work attention items, *n_combine combine items (both stored in work, the

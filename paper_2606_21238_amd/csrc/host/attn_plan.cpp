@@ -17,6 +17,14 @@
 // of all key tiles (e.g. one long history in a decode batch) is cut to that share, so that it
 // does not set the length of the launch.
 //
+// Narrow batches run persistent work-groups instead: the plan is a set of lists, one per
+// work-group (kListItems entries each: its items in order, then idle padding), at most one list
+// per compute unit when the items fit.  The tiles are packed into the lists in order, cut where
+// a list's budget runs out, so that every list carries about the same cost (key tiles, plus
+// kItemCost per item for the item's Q tile, its first tile's latency and its epilogue); a cut
+// never leaves a piece shorter than kMinPiece key tiles.  The budget is the smallest that
+// needs no more lists than compute units.  The kernel streams a list's items back to back.
+//
 // No item covers more than kMaxItemKeys keys (65536): a longer range is cut the same way, so the
 // attention kernel can hold an item's block-table entries in LDS.
 //
@@ -34,6 +42,8 @@ namespace {
 
 constexpr int kKeyTile = 64;  // keys per K/V tile (split boundaries are multiples of this)
 constexpr int kXcds = 8;      // MI355X: 8 XCDs; dispatch round-robins work-groups over them
+constexpr int64_t kItemCost = 4;  // list plans: cost of one item beyond its key tiles (measured)
+constexpr int64_t kMinPiece = 4;  // list plans: shortest piece a cut may leave, in key tiles
 
 struct Item {
   int32_t v[ARCKV_WORK_INTS];
@@ -87,6 +97,96 @@ extern "C" int32_t arckv_attention_plan(const int32_t* cu_q, const int32_t* seq_
   const int64_t base = static_cast<int64_t>(tiles.size());
   const int64_t target = static_cast<int64_t>(num_cus);  // one work-group per CU at a time
   auto key_tiles = [](const Tile& t) { return (static_cast<int64_t>(t.kv_end) + kKeyTile - 1) / kKeyTile; };
+
+  if (kCols == arckv::kNarrowCols) {
+    // ---- list plan ----------------------------------------------------------------------
+    constexpr int64_t kMaxPiece = arckv::kMaxItemKeys / kKeyTile;
+    struct Piece { int32_t tile; int64_t a, n; int32_t list; };  // key tiles [a, a + n)
+    int64_t cost = 0, min_pieces = 0;
+    for (const Tile& t : tiles) {
+      const int64_t kt = key_tiles(t);
+      const int64_t np = std::max<int64_t>(1, (kt + kMaxPiece - 1) / kMaxPiece);
+      min_pieces += np;
+      cost += kt + kItemCost * np;
+    }
+    const int64_t n_lists_max = std::max<int64_t>(target, (min_pieces + arckv::kListItems - 1) / arckv::kListItems);
+    std::vector<Piece> pieces;
+    // Packs the tiles in order into lists of budget B; returns the number of lists.
+    auto pack = [&](int64_t B, bool keep) -> int64_t {
+      if (keep) pieces.clear();
+      int64_t lists = 0, used = B, n_in = arckv::kListItems;
+      for (int32_t ti = 0; ti < static_cast<int32_t>(tiles.size()); ++ti) {
+        int64_t rem = key_tiles(tiles[ti]), a = 0;
+        while (rem > 0) {
+          if (n_in == arckv::kListItems || B - used - kItemCost < 1) {
+            ++lists; used = 0; n_in = 0;
+          }
+          const int64_t avail = std::min(B - used - kItemCost, kMaxPiece);
+          int64_t take = rem;
+          if (rem > avail) {
+            take = avail;
+            if (rem - take < kMinPiece) take = rem - kMinPiece;  // leave the next list a piece
+            if (take < kMinPiece) {
+              if (used > 0) { n_in = arckv::kListItems; continue; }  // start a fresh list
+              take = std::min(rem, kMaxPiece);                      // an empty list takes it
+            }
+          }
+          if (keep) pieces.push_back({ti, a, take, static_cast<int32_t>(lists - 1)});
+          used += take + kItemCost;
+          ++n_in;
+          a += take;
+          rem -= take;
+        }
+      }
+      return lists;
+    };
+    int64_t n_lists = 0;
+    if (base > 0) {
+      int64_t lo = std::max<int64_t>(kItemCost + kMinPiece, (cost + n_lists_max - 1) / n_lists_max);
+      int64_t hi = std::max<int64_t>(lo, cost + kItemCost);
+      while (lo < hi) {  // smallest budget that needs at most n_lists_max lists
+        const int64_t mid = lo + (hi - lo) / 2;
+        if (pack(mid, false) <= n_lists_max) hi = mid; else lo = mid + 1;
+      }
+      n_lists = pack(lo, true);
+    }
+    // items: pieces in list order; a tile cut into several pieces takes consecutive slots
+    std::vector<int32_t> n_pieces(tiles.size(), 0), first_slot(tiles.size(), -1);
+    for (const Piece& pc : pieces) ++n_pieces[pc.tile];
+    int64_t slot = 0;
+    std::vector<Item> combines;
+    for (size_t ti = 0; ti < tiles.size(); ++ti)
+      if (n_pieces[ti] > 1) {
+        const Tile& t = tiles[ti];
+        first_slot[ti] = static_cast<int32_t>(slot);
+        combines.push_back({{t.req, t.kvh, t.col_start, static_cast<int32_t>(slot), n_pieces[ti], 0, 0, 0}, 0, 0});
+        slot += n_pieces[ti];
+      }
+    std::vector<int32_t> next_piece(tiles.size(), 0);
+    const Item idle{{-1, 0, 0, 0, 0, -1, 0, 0}, 0, -1};
+    std::vector<Item> lists(static_cast<size_t>(n_lists * arckv::kListItems), idle);
+    std::vector<int32_t> fill(static_cast<size_t>(n_lists), 0);
+    for (const Piece& pc : pieces) {
+      const Tile& t = tiles[pc.tile];
+      const int32_t a = static_cast<int32_t>(pc.a * kKeyTile);
+      const int32_t b = static_cast<int32_t>(std::min<int64_t>((pc.a + pc.n) * kKeyTile, t.kv_end));
+      const int32_t sl = n_pieces[pc.tile] > 1 ? first_slot[pc.tile] + next_piece[pc.tile]++ : -1;
+      lists[static_cast<size_t>(pc.list) * arckv::kListItems + fill[pc.list]++] =
+          {{t.req, t.kvh, t.col_start, a, b, sl, 0, 0}, b - a, 0};
+    }
+    *n_work = static_cast<int64_t>(lists.size());
+    *n_combine = static_cast<int64_t>(combines.size());
+    *ws_bytes = slot * kCols * (static_cast<int64_t>(head_dim) + 1) * 4;
+    if (work == nullptr) return ARCKV_OK;
+    if (*n_work + *n_combine > work_cap)
+      return arckv::fail(ARCKV_ENOSPC, "attention_plan: %lld items, capacity %lld",
+                         (long long)(*n_work + *n_combine), (long long)work_cap);
+    int32_t* w = work;
+    for (const Item& it : lists) { std::copy(it.v, it.v + ARCKV_WORK_INTS, w); w += ARCKV_WORK_INTS; }
+    for (const Item& it : combines) { std::copy(it.v, it.v + ARCKV_WORK_INTS, w); w += ARCKV_WORK_INTS; }
+    return ARCKV_OK;
+  }
+
   int64_t cap = INT32_MAX;  // key tiles per item
   if (base > 0) {
     int64_t total_t = 0, max_t = 0;

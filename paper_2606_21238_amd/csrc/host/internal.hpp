@@ -19,6 +19,9 @@ constexpr int kNarrowCols = 4 * kWaveCols;
 // Longest key range of one attention work item: longer ranges are split into pieces (merged by
 // the combine), so that the item's block-table entries (kMaxItemKeys / 16) fit in LDS.
 constexpr int kMaxItemKeys = 65536;
+// Narrow plans give every work-group a list of this many work items (its items in order, then
+// idle padding): the attention launch has n_work / kListItems work-groups.
+constexpr int kListItems = 8;
 
 // Whether the cache was created in check mode (block digests verified by every plan).
 bool cache_checks_blocks(const arckv_cache* c);

@@ -8,14 +8,14 @@
 // Sec. 4; layout V1: K [blk][kvh][16][D], V [blk][kvh][D][16]).
 //
 // Design (MI355X-first):
-//  * One work-group = one query tile of one (request, KV head); a
-//    column is (token, head-of-group), token-major, so every K/V tile a work-group loads
-//    serves all G query heads of its KV head (GQA packed into the MFMA N dimension).  Wide
-//    tiles: 8 waves x 32 columns.  Narrow tiles (short suffixes): 4 x 32 columns, the two
-//    groups of 4 waves taking the two 32-key halves of every K/V tile with separate online
-//    softmax states that merge through LDS at the end.  Narrow tiles also serve decode-like
-//    batches (a few columns per request): eight waves keep more loads in flight per CU than
-//    a two-wave 32-column tile did (6 % faster on 64-request decode batches).
+//  * A work item is one query tile of one (request, KV head) over a key range; a column is
+//    (token, head-of-group), token-major, so every K/V tile loaded serves all G query heads
+//    of its KV head (GQA packed into the MFMA N dimension).  Wide tiles (256 columns): one
+//    work-group per item, 8 waves x 32 columns.  Narrow tiles (128 columns: short suffixes and
+//    decode-like batches): persistent work-groups that each stream a host-balanced list of
+//    items through one continuous load pipeline, 4 x 32 columns with the two groups of 4 waves
+//    taking the two 32-key halves of every K/V tile (separate online softmax states, merged
+//    through LDS at the end of each item).
 //  * Transposed formulation: S^T = K . Q^T and O^T = V^T . P^T with v_mfma_f32_32x32x16_bf16.
 //    Query columns sit on lanes, keys / head dims on the M (register) dimension, so a lane
 //    owns whole columns: row max and row sum are in-lane plus one exchange with lane +- 32.
@@ -27,15 +27,15 @@
 //    the B-operand layout of the P.V step, so P^T goes from registers to the next MFMA with
 //    no shuffle, and V^T (dim-major blocks) is read as one 16-byte operand per lane.
 //  * K/V tiles of 64 keys (4 blocks) are gathered from the scattered physical blocks with
-//    16-byte direct global-to-LDS loads into a 4-stage ring of XOR-swizzled LDS tiles; two
+//    16-byte direct global-to-LDS loads into a ring of XOR-swizzled LDS tiles; two or three
 //    tiles are in flight while the current one is multiplied.  The query tile comes through
-//    the same direct loads (narrow tiles: into LDS after the ring), so the first wait covers
+//    the same direct loads (narrow tiles: as an element of the ring), so the first wait covers
 //    the queries and tile 0 only.
 //  * fp32 online softmax in base 2 (scale * log2 e folded into one FMA per score), causal
 //    masking only on tiles that cross the diagonal, bf16 P with fp32 accumulation.
-//  * Long key ranges with too few query tiles are split by the host plan into one round of
-//    work-groups; split items write fp32 partials plus a base-2 log-sum-exp that
-//    attn_combine merges.
+//  * Long key ranges with too few query tiles are split by the host plan (wide tiles: into
+//    one round of work-groups; narrow tiles: where a list's budget ends); split items write
+//    fp32 partials plus a base-2 log-sum-exp that attn_combine merges.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -64,6 +64,9 @@ constexpr float kLazy = 8.0f;  // rescale O only when a column max grows by > 2^
 struct Work {
   int32_t req, kvh, col_start, kv_start, kv_end, slot, pad0, pad1;
 };
+static_assert(sizeof(Work) == ARCKV_WORK_INTS * sizeof(int32_t), "a work item is ARCKV_WORK_INTS ints");
+// read-only kernel inputs seen through the constant address space (scalar loads)
+typedef __attribute__((address_space(4))) const int32_t cint32;
 
 // MFMA row i of S^T is fed by K row pi(i) (bits 2 and 3 swapped): then accumulator register r
 // of a lane in half hg holds key 16 (r / 8) + 8 hg + r % 8 of its 32-key block, which is the
@@ -114,137 +117,173 @@ __device__ __forceinline__ void load_lds16(const void* g, lds_void* l) {
                : "memory", "m0");
 }
 
-// NW waves per work-group (two per SIMD), one work-group per CU (the K/V ring fills LDS).
-// KH = 1 (wide tiles): each wave owns 32 NB query columns and every key.  KH = 2 (narrow
-// tiles, short suffixes): the waves form two halves over the same 4 x 32 columns, half h
-// taking keys [32 h, 32 h + 32) of every 64-key tile, each with its own online softmax; the
-// halves merge through LDS at the end.  Both keep two waves per SIMD for any tile width.
-template <int D, int G, int NW, int NB, int KH>
-__global__ __launch_bounds__(64 * NW, 1) void prefill_attn_kernel(
+// Narrow tiles (128 query columns: short suffixes and decode-like batches) run as persistent
+// work-groups.  The host plan hands every work-group a list of up to kListItems items (its live
+// items first, then idle padding), balanced so that the lists of a launch carry about equal
+// work; a work-group streams its list back to back through one LDS ring.  The ring's elements
+// are, per item, the item's Q tile and then its K/V tiles (a 128-column Q tile is exactly the
+// size of one K/V tile pair), and the loads run three elements ahead across item boundaries,
+// so the pipeline does not drain between items.
+//
+// Eight waves: four column waves of 32 columns times two key halves; half h takes keys
+// [32 h, 32 h + 32) of every 64-key tile with its own online softmax, and at the end of an item
+// half 1 hands (m, l, O) to half 0 through the two ring stages that are free at that point.
+// Two waves share each SIMD, so one wave's exponentials overlap the other's MFMAs.
+template <int D, int G>
+__global__ __launch_bounds__(512, 1) void prefill_attn_list_kernel(
     const uint16_t* __restrict__ k_pool, const uint16_t* __restrict__ v_pool,
     const uint16_t* __restrict__ q, uint16_t* __restrict__ out,
     const int32_t* __restrict__ block_tables, int bt_stride,
     const int32_t* __restrict__ cu_q, const int32_t* __restrict__ seq_lens, int n_reqs,
     const Work* __restrict__ work, int64_t n_q, int64_t num_blocks, int hq, int hkv,
     float scale_log2, float* __restrict__ ws_o, float* __restrict__ ws_lse, int64_t ws_slots) {
-  constexpr int kThreads = 64 * NW;
-  constexpr int kNB = NB;                        // 32-column MFMA blocks per wave
-  constexpr int kWC = 32 * NB;                   // query columns per wave
-  constexpr int kCW = NW / KH;                   // waves per key half
-  constexpr int kCols = kCW * kWC;               // query columns of the work-group
-  constexpr int kMB = 2 / KH;                    // 32-key blocks of a tile per wave
-  static_assert((KH == 1 || KH == 2) && (KH == 1 || NB == 1) && kCW * KH == NW, "key halves");
+  constexpr int kThreads = 512;
+  constexpr int kCW = 4;                         // column waves of 32 columns
+  constexpr int kCols = kCW * 32;                // query columns of a narrow tile
   constexpr int KSTEPS = D / 16;                 // k-steps of Q.K^T
   constexpr int DM = D / 32;                     // 32-row blocks of O^T
   constexpr int TILE = kBK * D * 2;              // bytes of one K (or V) tile
-  constexpr int NLD = TILE / (kThreads * 16);    // 16-byte direct loads per thread per tile
+  constexpr int STAGE = 2 * TILE;                // one ring element: K then V, or a Q tile
+  static_assert(kCols * D * 2 == STAGE, "a Q tile fills one ring stage");
+  constexpr int kRing = 5;                       // three elements in flight + two free stages
   constexpr int LDB = kThreads * 16;             // bytes one load instruction moves per WG
+  constexpr int NLD = TILE / LDB;                // 16-byte direct loads per thread per K tile
+  constexpr int NEL = STAGE / LDB;               // ... per ring element
   constexpr int BLK_BYTES = 16 * D * 2;          // one block of one head, K or V
   static_assert(NLD >= 1 && TILE % LDB == 0, "tile must be a multiple of one WG-wide load");
-  constexpr int Q_BYTES = kCols * D * 2;         // the work-group's Q tile, after the ring
-  constexpr int NQ = Q_BYTES / LDB;              // its 16-byte direct loads per thread
-  static_assert(NQ >= 1 && Q_BYTES % LDB == 0, "Q tile must be a multiple of one WG-wide load");
-  __shared__ __attribute__((aligned(1024))) char smem[kStages * 2 * TILE + Q_BYTES];  // stage s: K, then V
+  constexpr int MDR = DM / 2;                    // O blocks a half hands over per merge round
+  static_assert(kCW * MDR * 4 * 64 * 16 == STAGE, "one merge round fills one stage");
+  __shared__ __attribute__((aligned(1024))) char smem[kRing * STAGE];
   if (n_q <= 0) return;
 
-  const Work w = work[blockIdx.x];
-  // an idle item (request -1) pads the XCD phase; anything else out of range is malformed
-  ARCKV_CHECK_WAVE(w.req >= n_reqs || (w.req >= 0 && (w.kvh < 0 || w.kvh >= hkv || w.col_start < 0)),
-                   ARCKV_CHECK_WORK);
-  if (w.req < 0 || w.req >= n_reqs || w.kvh < 0 || w.kvh >= hkv || w.col_start < 0) return;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int cw = wave % kCW, kh = wave / kCW;    // column wave, key half
   const int l32 = lane & 31, hg = lane >> 5;
-  const int q0 = cu_q[w.req];
-  const int S = cu_q[w.req + 1] - q0;
-  const int L = seq_lens[w.req];
-  const int P = L - S;
-  const int ncols = S * G;
-  const int32_t* bt = block_tables + static_cast<int64_t>(w.req) * bt_stride;
-  const int nblk = min((L + 15) >> 4, bt_stride);
+  auto stage = [&](int e) { return smem + (e % kRing) * STAGE; };
 
-  // ---- this lane's query columns and their Q^T operands ---------------------------------
-  int pos[kNB];
-  bool cval[kNB];
+  // ---- the items of the list ------------------------------------------------------------
+  // Entries up to the first idle one (request < 0) are the list; an entry naming no request,
+  // KV head or column is skipped (and recorded in a device-checked build).  Everything the
+  // cursors need of an entry is computed once, before the first load of the ring, into a table
+  // of two registers (lane 8 f + j holds field f of entry j), so that moving to the next item
+  // costs register reads only: a memory load there would wait for the loads of the ring.
+  enum { F_OK, F_REQ, F_KVH, F_COL, F_SLOT, F_Q0, F_NCOLS, F_P,
+         F_L, F_KVLO, F_NT, F_MINPOS, F_NBLK };  // F_OK: 1 item, 0 skipped entry, -1 past the end
+  int32_t tbl[2];
+  {
+    const int j = lane & 7, f = lane >> 3;
+    const Work w = work[static_cast<int64_t>(blockIdx.x) * arckv::kListItems + j];
+    const uint64_t idle = __builtin_amdgcn_ballot_w64(lane < arckv::kListItems && w.req < 0);
+    const bool live = (idle & ((2ull << j) - 1)) == 0;
+    const bool bad = w.req >= n_reqs || w.kvh < 0 || w.kvh >= hkv || w.col_start < 0;
+    ARCKV_CHECK_LANE(lane < arckv::kListItems && live && bad, ARCKV_CHECK_WORK);
+    const bool ok = live && !bad;
+    const int q0 = ok ? cu_q[w.req] : 0;
+    const int S = ok ? cu_q[w.req + 1] - q0 : 0;
+    const int L = ok ? seq_lens[w.req] : 0;
+    const int P = L - S, ncols = S * G;
+    const int last_col = min(w.col_start + kCols, ncols) - 1;
+    const int kv_lo = max(w.kv_start, 0);
+    const int kv_hi = min(w.kv_end, P + last_col / G + 1);
+    const int nt = ok && kv_hi > kv_lo ? (kv_hi - kv_lo + kBK - 1) / kBK : 0;
+    const int v0[8] = {ok ? 1 : (live ? 0 : -1), w.req, w.kvh, w.col_start, w.slot, q0, ncols, P};
+    const int v1[8] = {L, kv_lo, nt, P + w.col_start / G, min((L + 15) >> 4, bt_stride), 0, 0, 0};
+    int t0 = 0, t1 = 0;
 #pragma unroll
-  for (int nb = 0; nb < kNB; ++nb) {
-    const int col = w.col_start + cw * kWC + nb * 32 + l32;
-    const int tok = col / G;
-    cval[nb] = col < ncols && (q0 + tok) < n_q;
-    pos[nb] = cval[nb] ? P + tok : -1;
+    for (int k = 0; k < 8; ++k) {
+      t0 = f == k ? v0[k] : t0;
+      t1 = f == k ? v1[k] : t1;
+    }
+    tbl[0] = t0;
+    tbl[1] = t1;
   }
-  // The Q tile goes to LDS with direct loads like the K/V tiles, so that no load the compiler
-  // counts is pending and the first wait can leave later tiles in flight.  Column c (a row of
-  // q) holds its 16-byte chunks j at slot j ^ fk(c); columns past the request load row 0 of q,
-  // never read back.
-  char* const qs = smem + kStages * 2 * TILE;
-  auto load_q = [&]() {
-#pragma unroll
-    for (int j = 0; j < NQ; ++j) {
-      const int b = j * LDB + wave * 1024 + lane * 16;
-      const int c = b / (2 * D), p = (b % (2 * D)) / 16;
-      const int gc = w.col_start + c;
-      const int tok = gc / G, g = gc % G;
-      const bool ok = gc < ncols && (q0 + tok) < n_q;
-      const int64_t row = ok ? static_cast<int64_t>(q0 + tok) * hq + w.kvh * G + g : 0;
-      load_lds16(q + row * D + ((p ^ fk<D>(c)) * 8), (lds_void*)(qs + j * LDB + wave * 1024));
-    }
+  auto field = [&](int fld, int j) {
+    return fld < 8 ? __builtin_amdgcn_readlane(tbl[0], fld * 8 + j) : __builtin_amdgcn_readlane(tbl[1], (fld - 8) * 8 + j);
   };
-  bf16x8_t qf[kNB][KSTEPS];
-  auto read_q = [&]() {
-#pragma unroll
-    for (int nb = 0; nb < kNB; ++nb) {
-      const int c = cw * kWC + nb * 32 + l32;
-#pragma unroll
-      for (int ks = 0; ks < KSTEPS; ++ks)
-        qf[nb][ks] = cval[nb] ? *reinterpret_cast<const bf16x8_t*>(qs + c * 2 * D + (((ks * 2 + hg) ^ fk<D>(c)) * 16))
-                              : bf16x8_t{};
+  // The block tables are read through the constant address space: the kernel never writes
+  // them, and this keeps their (uniform) loads scalar after the epilogue stores of an earlier
+  // item, where a vector load would make the compiler wait for every load of the ring.
+  const cint32* const cbt = (const cint32*)(block_tables);
+  struct Item {
+    int j, req, kvh, col_start, slot, q0, L, P, ncols, kv_lo, nt, min_pos, nblk;
+    const cint32* bt;
+  };
+  auto find_item = [&](int j, Item& it) -> bool {
+    for (; j < arckv::kListItems; ++j) {
+      const int st = field(F_OK, j);
+      if (st < 0) return false;
+      if (st == 0) continue;
+      it.j = j;
+      it.req = field(F_REQ, j);
+      it.kvh = field(F_KVH, j);
+      it.col_start = field(F_COL, j);
+      it.slot = field(F_SLOT, j);
+      it.q0 = field(F_Q0, j);
+      it.ncols = field(F_NCOLS, j);
+      it.P = field(F_P, j);
+      it.L = field(F_L, j);
+      it.kv_lo = field(F_KVLO, j);
+      it.nt = field(F_NT, j);
+      it.min_pos = field(F_MINPOS, j);
+      it.nblk = field(F_NBLK, j);
+      it.bt = cbt + static_cast<int64_t>(it.req) * bt_stride;
+      return true;
     }
+    return false;
   };
 
-  const int last_col = min(w.col_start + kCols, ncols) - 1;
-  const int wg_max_pos = P + last_col / G;
-  const int wg_min_pos = P + w.col_start / G;
-  const int kv_lo = max(w.kv_start, 0);
-  const int kv_hi = min(w.kv_end, wg_max_pos + 1);
-  const int ntiles = kv_hi > kv_lo ? (kv_hi - kv_lo + kBK - 1) / kBK : 0;
-
-  // ---- direct global -> LDS tile loads -------------------------------------------------
-  // load i of a thread covers LDS bytes [i*LDB + wave*1024 + lane*16, +16) of the tile; each
-  // wave's 1 KiB lies inside one block, so the block's physical address is wave-uniform.
+  // ---- loads: direct global -> LDS, one ring element per call ------------------------------
+  // load i of a thread covers LDS bytes [i*LDB + wave*1024 + lane*16, +16) of a K or V tile;
+  // each wave's 1 KiB lies inside one block, so the block's physical address is wave-uniform.
   int k_off[NLD], v_off[NLD], blk_of[NLD];
 #pragma unroll
   for (int i = 0; i < NLD; ++i) {
     const int posb = i * LDB + wave * 1024 + lane * 16;
     const int r = posb / (2 * D), p = (posb % (2 * D)) / 16;      // K: row r, stored chunk p
-    blk_of[i] = posb / BLK_BYTES;
+    blk_of[i] = (i * LDB + wave * 1024) / BLK_BYTES;               // the same for every lane
     k_off[i] = (r & 15) * D + ((p ^ fk<D>(r)) * 8);               // elements inside the block
     const int qv = posb % BLK_BYTES, d = qv / 32, h = ((qv / 16) & 1) ^ sv(d);
     v_off[i] = d * 16 + h * 8;
   }
-  const int64_t head_k = static_cast<int64_t>(w.kvh) * 16 * D;   // head offset inside a block
   const int64_t blk_stride = static_cast<int64_t>(hkv) * 16 * D;  // elements per physical block
-  // Physical block numbers of the next tile to be issued: tiles are issued in order, and each
-  // issue reads the table entries of the one after it, so the scalar loads' latency is spent
-  // during a whole step rather than in front of the tile's loads.
+  // The load cursor: item `ld`, next element `lt` (-1: its Q tile, else K/V tile lt), and the
+  // physical blocks of its next K/V tile.  Those are read at the end of the element before
+  // (prefetch_ph, right before its wait), so the scalar loads' latency hides under that wait.
+  Item ld;
+  bool ld_live = find_item(0, ld);
+  int lt = -1, n_issued = 0;
   int32_t next_ph[NLD];
   auto fetch_ph = [&](int tile) {
-    const int b0 = (kv_lo + tile * kBK) >> 4;
+    const int b0 = (ld.kv_lo + tile * kBK) >> 4;
 #pragma unroll
     for (int i = 0; i < NLD; ++i) {
       const int b = b0 + blk_of[i];
-      next_ph[i] = b < nblk ? bt[b] : 0;
+      next_ph[i] = b < ld.nblk ? ld.bt[b] : 0;
     }
   };
-  fetch_ph(0);
-  // tile t (keys kv_lo + 64 t ...) lives in LDS stage t % kStages
-  auto load_tile = [&](int tile) {
-    char* st = smem + (tile % kStages) * 2 * TILE;
+  // Q tile: column c (a row of q) holds its 16-byte chunks j at slot j ^ fk(c); columns past
+  // the request load row 0 of q, never read back.
+  auto load_q = [&](char* st) {
+#pragma unroll
+    for (int j = 0; j < NEL; ++j) {
+      const int b = j * LDB + wave * 1024 + lane * 16;
+      const int c = b / (2 * D), p = (b % (2 * D)) / 16;
+      const int gc = ld.col_start + c;
+      const int tok = gc / G, g = gc % G;
+      const bool ok = gc < ld.ncols && (ld.q0 + tok) < n_q;
+      const int64_t row = ok ? static_cast<int64_t>(ld.q0 + tok) * hq + ld.kvh * G + g : 0;
+      load_lds16(q + row * D + ((p ^ fk<D>(c)) * 8), (lds_void*)(st + j * LDB + wave * 1024));
+    }
+  };
+  auto prefetch_ph = [&]() {
+    if (ld_live && lt >= 0) fetch_ph(lt);
+  };
+  auto load_kv = [&](char* st) {
     int32_t ph[NLD];
 #pragma unroll
     for (int i = 0; i < NLD; ++i) ph[i] = next_ph[i];
-    fetch_ph(tile + 1);
+    const int64_t head_k = static_cast<int64_t>(ld.kvh) * 16 * D;
 #pragma unroll
     for (int i = 0; i < NLD; ++i) {
       ARCKV_CHECK_WAVE(ph[i] < 0 || ph[i] >= num_blocks, ARCKV_CHECK_BLOCK);
@@ -254,134 +293,114 @@ __global__ __launch_bounds__(64 * NW, 1) void prefill_attn_kernel(
       load_lds16(v_pool + base + v_off[i], (lds_void*)(st + TILE + i * LDB + wave * 1024));
     }
   };
+  // Issues the next element of the list (NEL loads per thread) into its ring stage; false
+  // once the list is exhausted (nothing issued).
+  auto issue = [&]() -> bool {
+    if (!ld_live) return false;
+    char* st = stage(n_issued);
+    if (lt < 0) load_q(st);
+    else load_kv(st);
+    ++lt;
+    if (lt >= ld.nt) {
+      ld_live = find_item(ld.j + 1, ld);
+      lt = -1;
+    }
+    ++n_issued;
+    return true;
+  };
+  // End of an element: every element up to the one after next is in LDS (only the newest,
+  // issued at the start of this element, may be pending: loads complete in order), and every
+  // wave's LDS reads have returned.  The wait and the barrier are written out: a fenced
+  // __syncthreads() would also wait for the newest loads.
+  auto end_element = [&](bool issued) {
+    prefetch_ph();
+    if (issued) asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(NEL) : "memory");
+    else asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  };
+  auto lds_barrier = [&]() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); };
 
   // ---- MFMA pieces ------------------------------------------------------------------------
-  // S^T (this wave's 32 kMB keys of the tile x its columns) = K . Q^T
-  auto mma_s = [&](f32x16_t (&s)[kMB][kNB], int tile) {
-    const char* kb = smem + (tile % kStages) * 2 * TILE;
+  bf16x8_t qf[KSTEPS];
+  // S^T (this wave's 32 keys of the tile x its 32 columns) = K . Q^T
+  auto mma_s = [&](f32x16_t& s, const char* kb) {
+    s = f32x16_t{};
+    const int r = kh * 32 + pi_row(l32);
 #pragma unroll
-    for (int mb = 0; mb < kMB; ++mb)
-#pragma unroll
-      for (int nb = 0; nb < kNB; ++nb) s[mb][nb] = f32x16_t{};
-#pragma unroll
-    for (int ks = 0; ks < KSTEPS; ++ks)
-#pragma unroll
-      for (int mb = 0; mb < kMB; ++mb) {
-        const int r = (kh * kMB + mb) * 32 + pi_row(l32);
-        const int c = 2 * ks + hg;
-        const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(kb + r * 2 * D + ((c ^ fk<D>(r)) * 16));
-#pragma unroll
-        for (int nb = 0; nb < kNB; ++nb)
-          s[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[nb][ks], s[mb][nb], 0, 0, 0);
-      }
+    for (int ks = 0; ks < KSTEPS; ++ks) {
+      const int c = 2 * ks + hg;
+      const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(kb + r * 2 * D + ((c ^ fk<D>(r)) * 16));
+      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[ks], s, 0, 0, 0);
+    }
   };
-
-  f32x16_t o[DM][kNB];
-#pragma unroll
-  for (int md = 0; md < DM; ++md)
-#pragma unroll
-    for (int nb = 0; nb < kNB; ++nb) o[md][nb] = f32x16_t{};
-  float m_run[kNB], l_run[kNB];
-#pragma unroll
-  for (int nb = 0; nb < kNB; ++nb) { m_run[nb] = -INFINITY; l_run[nb] = 0.f; }
-
-  // causal / prompt-end mask: accumulator register r of this wave's S^T block mb holds key
-  // t0 + 32 (kh kMB + mb) + 16 (r / 8) + 8 hg + r % 8 of this lane's column
-  auto apply_mask = [&](f32x16_t (&s)[kMB][kNB], int t0) {
-#pragma unroll
-    for (int nb = 0; nb < kNB; ++nb)
-#pragma unroll
-      for (int mb = 0; mb < kMB; ++mb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int key = t0 + (kh * kMB + mb) * 32 + 16 * (r >> 3) + 8 * hg + (r & 7);
-          s[mb][nb][r] = key > pos[nb] ? -INFINITY : s[mb][nb][r];
-        }
-  };
-  // Column maxima of a tile (base-2 scaled) and the lazy-rescale decision, without branches:
-  // the running maximum moves only when some column of the wave grew by more than 2^kLazy;
-  // then O and l must be scaled by alpha before the next P.V product (apply_rescale).
-  float alpha[kNB];
+  f32x16_t o[DM];
+  float m_run, l_run, alpha;
   bool pending = false;  // wave-uniform
-  auto update_max = [&](f32x16_t (&s)[kMB][kNB]) {
-    float mx[kNB];
-    bool grow = false;
+  int pos = -1;          // this lane's query position (-1: no column)
+  // causal / prompt-end mask: accumulator register r holds key t0 + 32 kh + 16 (r / 8) +
+  // 8 hg + r % 8 of this lane's column
+  auto apply_mask = [&](f32x16_t& s, int t0) {
 #pragma unroll
-    for (int nb = 0; nb < kNB; ++nb) {
-      float m = -INFINITY;
-#pragma unroll
-      for (int mb = 0; mb < kMB; ++mb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) m = fmaxf(m, s[mb][nb][r]);
-      m = max_halves(m);
-      mx[nb] = m * scale_log2;
-      grow = grow || (mx[nb] > m_run[nb] + kLazy);
+    for (int r = 0; r < 16; ++r) {
+      const int key = t0 + kh * 32 + 16 * (r >> 3) + 8 * hg + (r & 7);
+      s[r] = key > pos ? -INFINITY : s[r];
     }
-    pending = __builtin_amdgcn_ballot_w64(grow) != 0;
+  };
+  // Column maximum of a tile (base-2 scaled) and the lazy-rescale decision, without branches:
+  // the running maximum moves only when some column of the wave grew by more than 2^kLazy;
+  // then O and l are scaled by alpha before the next P.V product (apply_rescale).
+  auto update_max = [&](const f32x16_t& s) {
+    float m = -INFINITY;
 #pragma unroll
-    for (int nb = 0; nb < kNB; ++nb) {
-      const float m_new = pending ? fmaxf(m_run[nb], mx[nb]) : m_run[nb];
-      alpha[nb] = m_new == -INFINITY ? 1.f : fast_exp2(m_run[nb] - m_new);
-      m_run[nb] = m_new;
-    }
+    for (int r = 0; r < 16; ++r) m = fmaxf(m, s[r]);
+    const float mx = max_halves(m) * scale_log2;
+    pending = __builtin_amdgcn_ballot_w64(mx > m_run + kLazy) != 0;
+    const float m_new = pending ? fmaxf(m_run, mx) : m_run;
+    alpha = m_new == -INFINITY ? 1.f : fast_exp2(m_run - m_new);
+    m_run = m_new;
   };
   auto apply_rescale = [&]() {
     if (pending) {
+      l_run *= alpha;
 #pragma unroll
-      for (int nb = 0; nb < kNB; ++nb) {
-        l_run[nb] *= alpha[nb];
+      for (int md = 0; md < DM; ++md) o[md] *= alpha;
+    }
+  };
+  // p = 2^(s * scale * log2 e - m) rounded to bf16: the P^T operands of the P.V product.  The
+  // row sums accumulate the fp32 p (before the rounding the P.V operand gets).
+  uint32_t pw[2][4];
+  auto exp_phase = [&](const f32x16_t& s) {
+    const float mu = m_run == -INFINITY ? 0.f : m_run;
+    float lsum = 0.f;
 #pragma unroll
-        for (int md = 0; md < DM; ++md) o[md][nb] *= alpha[nb];
+    for (int half = 0; half < 2; ++half)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const f32x2_t two = {fast_exp2(fmaf(s[8 * half + 2 * j], scale_log2, -mu)),
+                             fast_exp2(fmaf(s[8 * half + 2 * j + 1], scale_log2, -mu))};
+        lsum += two[0];
+        lsum += two[1];
+        pw[half][j] = __builtin_bit_cast(uint32_t, __builtin_convertvector(two, bf16x2_t));
       }
-    }
+    l_run += lsum;
   };
-  // p = 2^(s * scale * log2 e - m) rounded to bf16: the P^T operands of the P.V product, kept
-  // as 32-bit bf16 pairs.  (The row sum reads these scalars; extracting words from the 8-element
-  // vector instead was compiled into four reads of one register.)
-  // The row sums l accumulate the fp32 p (before the bf16 rounding the P.V operand gets); plain
-  // adds co-issue with the MFMAs where a bf16 dot product of the rounded pairs does not.
-  auto exp_phase = [&](f32x16_t (&s)[kMB][kNB], uint32_t (&pw)[kNB][2 * kMB][4]) {
+  // O^T (D x this wave's columns) += V^T . P^T over this half's two 16-key blocks of the tile
+  auto mma_pv = [&](const char* vb) {
 #pragma unroll
-    for (int nb = 0; nb < kNB; ++nb) {
-      const float mu = m_run[nb] == -INFINITY ? 0.f : m_run[nb];
-      float lsum = 0.f;
-#pragma unroll
-      for (int mb = 0; mb < kMB; ++mb)
-#pragma unroll
-        for (int half = 0; half < 2; ++half)
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const f32x2_t two = {fast_exp2(fmaf(s[mb][nb][8 * half + 2 * j], scale_log2, -mu)),
-                                 fast_exp2(fmaf(s[mb][nb][8 * half + 2 * j + 1], scale_log2, -mu))};
-            lsum += two[0];
-            lsum += two[1];
-            pw[nb][2 * mb + half][j] = __builtin_bit_cast(uint32_t, __builtin_convertvector(two, bf16x2_t));
-          }
-      l_run[nb] += lsum;
-    }
-  };
-  // O^T (D x this wave's columns) += V^T . P^T over this wave's 16-key blocks of the tile
-  auto mma_pv = [&](const uint32_t (&pw)[kNB][2 * kMB][4], int tile) {
-    const char* vb = smem + (tile % kStages) * 2 * TILE + TILE;
-#pragma unroll
-    for (int sp = 0; sp < 2 * kMB; ++sp)
+    for (int sp = 0; sp < 2; ++sp)
 #pragma unroll
       for (int md = 0; md < DM; ++md) {
         const int d = md * 32 + l32;
-        const int blk = kh * 2 * kMB + sp;
+        const int blk = kh * 2 + sp;
         const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(vb + blk * BLK_BYTES + d * 32 + ((hg ^ sv(d)) * 16));
-#pragma unroll
-        for (int nb = 0; nb < kNB; ++nb) {
-          const u32x4_t w4 = {pw[nb][sp][0], pw[nb][sp][1], pw[nb][sp][2], pw[nb][sp][3]};
-          o[md][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, __builtin_bit_cast(bf16x8_t, w4), o[md][nb], 0, 0, 0);
-        }
+        const u32x4_t w4 = {pw[sp][0], pw[sp][1], pw[sp][2], pw[sp][3]};
+        o[md] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, __builtin_bit_cast(bf16x8_t, w4), o[md], 0, 0, 0);
       }
   };
-  // keys >= L of the last tile may hold stale bytes (even NaN patterns): zero their V in LDS
-  auto zero_v_tail = [&](int tile, int t0) {
-    uint16_t* vb = reinterpret_cast<uint16_t*>(smem + (tile % kStages) * 2 * TILE + TILE);
-    for (int e = tid; e < kBK * D; e += kThreads) {
-      const int key = e & (kBK - 1), d = e / kBK;
+  // keys >= L of the prompt's last tile may hold stale bytes (even NaN patterns): zero their V
+  auto zero_v_tail = [&](char* vbytes, int t0, int L) {
+    uint16_t* vb = reinterpret_cast<uint16_t*>(vbytes);
+    for (int x = tid; x < kBK * D; x += kThreads) {
+      const int key = x & (kBK - 1), d = x / kBK;
       if (t0 + key >= L) {
         const int blk = key >> 4, kk = key & 15;
         const int h = ((kk >> 3) ^ sv(d));
@@ -390,196 +409,188 @@ __global__ __launch_bounds__(64 * NW, 1) void prefill_attn_kernel(
     }
   };
 
-  // ---- main pipeline ----------------------------------------------------------------------
-  // A ring of kStages K/V tiles; tile i+kStages-1 is issued at the start of step i into the
-  // stage tile i-1 used (free once every wave passed the barrier ending step i-1), and the
-  // wait ending step i only needs tile i+2: loads get two steps of latency slack.
-  // Step i is two MFMA phases, each in one basic block with VALU work to overlap:
-  //   A: S(i+1) = K(i+1) Q^T            || exponentials of tile i (max of tile i known)
-  //   B: O += V(i) P(i)                  || row sums of tile i, mask + max of tile i+1
-  // A rescale of O decided in B of step i is applied at the start of step i+1.  Steps whose
-  // next tile needs masking (diagonal tiles, prompt end) run in a second, peeled loop, so the
-  // main loop carries no mask code.
-  static_assert(kStages >= 4, "the wait below assumes one tile in flight beyond i+2");
-  f32x16_t sa[kMB][kNB], sb[kMB][kNB];
-  uint32_t pb[kNB][2 * kMB][4];
-  auto tile_masked = [&](int t) {
-    const int t0 = kv_lo + t * kBK;
-    return (t0 + kBK - 1 > wg_min_pos) || (t0 + kBK > L);
-  };
-  // Q, then the first tiles.  Loads complete in order: once only the later tiles' loads may
-  // be pending, Q and tile 0 are in LDS (the barrier publishes every wave's part).  S(0) is
-  // computed while tiles 1 and 2 arrive; step 0 then needs tile 1.
-  load_q();
-  if (ntiles > 0) {
-    for (int t = 0; t < kStages - 1; ++t)
-      if (t < ntiles) load_tile(t);
-  }
-  if (ntiles >= 3) asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(4 * NLD) : "memory");
-  else if (ntiles == 2) asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(2 * NLD) : "memory");
-  else asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
-  read_q();
-  if (ntiles > 0) {
-    mma_s(sa, 0);
-    if (tile_masked(0)) apply_mask(sa, kv_lo);
-    update_max(sa);
-    if (ntiles >= 3) asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(2 * NLD) : "memory");
-    else asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
-  }
-  auto step = [&](auto mask_next, f32x16_t (&sc)[kMB][kNB], f32x16_t (&sn)[kMB][kNB], int i) {
-    constexpr bool MASK_NEXT = decltype(mask_next)::value;
-    const int t0 = kv_lo + i * kBK;
-    const bool issue = i + kStages - 1 < ntiles;
-    if (issue) load_tile(i + kStages - 1);
-    if (t0 + kBK > L) {  // uniform: only the tile holding the prompt end
-      zero_v_tail(i, t0);
-      __syncthreads();
-    }
-    apply_rescale();
-    // phase A
-    mma_s(sn, i + 1);  // on the last tile this multiplies stale LDS; the result is unused
-    exp_phase(sc, pb);
-    // phase B
-    mma_pv(pb, i);
-    if constexpr (MASK_NEXT) {
-      if (i + 1 < ntiles) {  // past the key range S(i+1) is stale LDS: never feed it to the max
-        apply_mask(sn, t0 + kBK);
-        update_max(sn);
-      }
-    } else {
-      update_max(sn);  // main-loop steps always have a next tile
-    }
-    // The next step reads tile i+2 (K) and i+1 (V): only the loads just issued may be pending.
-    // The wait and the barrier are written out: a fenced __syncthreads() would also wait for
-    // those newest loads (their LDS writes count as outstanding memory operations), which
-    // would leave the ring only one tile deep.  lgkmcnt(0): this wave's LDS reads of the
-    // stage the next step overwrites have returned.
-    if (issue)
-      asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(2 * NLD * (kStages - 3)) : "memory");
-    else
-      asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
-  };
-  // first step whose next tile is masked (tile_masked is monotone in the tile index)
-  int n_main = ntiles > 0 ? ntiles - 1 : 0;
+  // ---- the pipeline -------------------------------------------------------------------------
+  // Element e is consumed after elements <= e + 1 are in LDS (a K/V tile's step multiplies the
+  // next tile's K as well); element e + 3 is issued at its start into the stage element e - 2
+  // used, free since the barrier ending element e - 1.
   {
-    int lo = 0, hi = n_main;  // smallest i in [0, n_main) with tile_masked(i + 1), else n_main
-    while (lo < hi) {
-      const int mid = (lo + hi) >> 1;
-      if (tile_masked(mid + 1)) hi = mid; else lo = mid + 1;
+    issue();
+    prefetch_ph();
+    issue();
+    prefetch_ph();
+    end_element(issue());
+  }
+  int e = 0;  // element being consumed
+  Item it;
+  f32x16_t sa, sb;
+  for (bool live = find_item(0, it); live; live = find_item(it.j + 1, it)) {
+    // ---- element e: the item's Q tile -> registers; S(0) --------------------------------
+    const bool iq = issue();
+    const int col = it.col_start + cw * 32 + l32;
+    const bool cval = col < it.ncols && (it.q0 + col / G) < n_q;
+    pos = cval ? it.P + col / G : -1;
+    {
+      const char* qs = stage(e);
+      const int c = cw * 32 + l32;
+#pragma unroll
+      for (int ks = 0; ks < KSTEPS; ++ks)
+        qf[ks] = cval ? *reinterpret_cast<const bf16x8_t*>(qs + c * 2 * D + (((ks * 2 + hg) ^ fk<D>(c)) * 16))
+                      : bf16x8_t{};
     }
-    n_main = lo;
-  }
-  int i = 0;
-  for (; i + 1 < n_main; i += 2) {
-    step(std::false_type{}, sa, sb, i);
-    step(std::false_type{}, sb, sa, i + 1);
-  }
-  if (i < n_main) {
-    step(std::false_type{}, sa, sb, i);
 #pragma unroll
-    for (int mb = 0; mb < kMB; ++mb)
-#pragma unroll
-      for (int nb = 0; nb < kNB; ++nb) sa[mb][nb] = sb[mb][nb];
-    ++i;
-  }
-  for (; i < ntiles; ++i) {
-    step(std::true_type{}, sa, sb, i);
-#pragma unroll
-    for (int mb = 0; mb < kMB; ++mb)
-#pragma unroll
-      for (int nb = 0; nb < kNB; ++nb) sa[mb][nb] = sb[mb][nb];
-  }
+    for (int md = 0; md < DM; ++md) o[md] = f32x16_t{};
+    m_run = -INFINITY;
+    l_run = 0.f;
+    pending = false;
+    const int nt = it.nt;
+    auto tile_masked = [&](int t) {
+      const int t0 = it.kv_lo + t * kBK;
+      return (t0 + kBK - 1 > it.min_pos) || (t0 + kBK > it.L);
+    };
+    if (nt > 0) {
+      mma_s(sa, stage(e + 1));
+      if (tile_masked(0)) apply_mask(sa, it.kv_lo);
+      update_max(sa);
+    }
+    end_element(iq);
+    ++e;
 
-  // ---- key halves: half 1 hands (m, l, O) to half 0 through LDS ---------------------------
-  // Every wave has passed the barrier ending its last step (or ran no step and read no LDS),
-  // so the ring is free.  Layout: O as [column wave][md][r / 4][lane] float4, then m and l as
-  // [column wave][lane]; a lane of half 0 reads exactly what the same lane of half 1 wrote.
-  if constexpr (KH == 2) {
-    f32x4_t* xo = reinterpret_cast<f32x4_t*>(smem) + cw * (DM * 4 * 64);
-    float* xm = reinterpret_cast<float*>(smem + kCW * DM * 4 * 64 * 16) + cw * 128;
-    __syncthreads();
-    if (kh == 1) {
-#pragma unroll
-      for (int md = 0; md < DM; ++md)
-#pragma unroll
-        for (int r4 = 0; r4 < 4; ++r4) {
-          f32x4_t v;
-#pragma unroll
-          for (int j = 0; j < 4; ++j) v[j] = o[md][0][4 * r4 + j];
-          xo[(md * 4 + r4) * 64 + lane] = v;
+    // ---- elements e .. e + nt - 1: the K/V tiles -------------------------------------------
+    // step i: S(i+1) = K(i+1) Q^T (beside the exponentials of tile i), O += V(i) P(i), then the
+    // mask and maximum of tile i+1.  A rescale decided at step i is applied at step i+1.  Steps
+    // whose next tile needs masking run in a second, peeled loop.
+    auto step = [&](auto mask_next, f32x16_t& sc, f32x16_t& sn, int i) {
+      constexpr bool MASK_NEXT = decltype(mask_next)::value;
+      const int t0 = it.kv_lo + i * kBK;
+      const bool iss = issue();
+      char* cur = stage(e);
+      if (t0 + kBK > it.L) {  // uniform: only the tile holding the prompt end
+        zero_v_tail(cur + TILE, t0, it.L);
+        lds_barrier();
+      }
+      apply_rescale();
+      mma_s(sn, stage(e + 1));  // past the item's last tile this reads another element: unused
+      exp_phase(sc);
+      mma_pv(cur + TILE);
+      if constexpr (MASK_NEXT) {
+        if (i + 1 < nt) {       // never feed an element that is not this item's tile to the max
+          apply_mask(sn, t0 + kBK);
+          update_max(sn);
         }
-      xm[lane] = m_run[0];
-      xm[64 + lane] = l_run[0];
+      } else {
+        update_max(sn);         // main-loop steps always have a next tile
+      }
+      end_element(iss);
+      ++e;
+    };
+    int n_main = nt > 0 ? nt - 1 : 0;
+    {
+      int lo = 0, hi = n_main;  // first step whose next tile is masked (monotone), else n_main
+      while (lo < hi) {
+        const int mid = (lo + hi) >> 1;
+        if (tile_masked(mid + 1)) hi = mid; else lo = mid + 1;
+      }
+      n_main = lo;
     }
-    __syncthreads();
-  }
-  const bool active = kh == 0;  // waves that hold the (merged) result
-  if (KH == 2 && active) {
-    const f32x4_t* xo = reinterpret_cast<const f32x4_t*>(smem) + cw * (DM * 4 * 64);
-    const float* xm = reinterpret_cast<const float*>(smem + kCW * DM * 4 * 64 * 16) + cw * 128;
-    const float mb_ = xm[lane], lb = xm[64 + lane];
-    const float m = fmaxf(m_run[0], mb_);
-    const float a = m_run[0] == -INFINITY ? 0.f : fast_exp2(m_run[0] - m);
-    const float b = mb_ == -INFINITY ? 0.f : fast_exp2(mb_ - m);
-#pragma unroll
-    for (int md = 0; md < DM; ++md)
-#pragma unroll
-      for (int r4 = 0; r4 < 4; ++r4) {
-        const f32x4_t v = xo[(md * 4 + r4) * 64 + lane];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) o[md][0][4 * r4 + j] = a * o[md][0][4 * r4 + j] + b * v[j];
-      }
-    l_run[0] = a * l_run[0] + b * lb;
-    m_run[0] = m;
-  }
+    int i = 0;
+    for (; i + 1 < n_main; i += 2) {
+      step(std::false_type{}, sa, sb, i);
+      step(std::false_type{}, sb, sa, i + 1);
+    }
+    if (i < n_main) {
+      step(std::false_type{}, sa, sb, i);
+      sa = sb;
+      ++i;
+    }
+    for (; i < nt; ++i) {
+      step(std::true_type{}, sa, sb, i);
+      sa = sb;
+    }
 
-  // ---- epilogue: O^T register r of block md holds dim 32 md + 8 (r / 4) + 4 hg + r % 4 ------
-  // O is normalised in registers; lse (base 2) is what a split item reports with it.
-  float lse[kNB];
+    // ---- key halves: half 1 hands (m, l, O) to half 0 ---------------------------------------
+    // Consumed elements e - 1 and e - 2 leave their stages free until element e + 3 and e + 4
+    // are issued (at the starts of elements e and e + 1).  Round 1: O blocks [0, MDR) through
+    // stage e - 1, m and l through stage e - 2; round 2: O blocks [MDR, DM) through stage e - 1.
+    // Layout: O as [column wave][block][r / 4][lane] float4; m, l as [column wave][lane].
+    {
+      f32x4_t* xo = reinterpret_cast<f32x4_t*>(stage(e + kRing - 1)) + cw * (MDR * 4 * 64);
+      float* xm = reinterpret_cast<float*>(stage(e + kRing - 2)) + cw * 128;
+      float a = 0.f, b = 0.f;
 #pragma unroll
-  for (int nb = 0; nb < kNB; ++nb) {
-    const float lt = sum_halves(l_run[nb]);
-    const float inv = lt > 0.f ? 1.f / lt : 0.f;
-    lse[nb] = lt > 0.f ? m_run[nb] + __log2f(lt) : -INFINITY;
+      for (int round = 0; round < 2; ++round) {
+        if (kh == 1) {
 #pragma unroll
-    for (int md = 0; md < DM; ++md) o[md][nb] *= inv;
-  }
-  auto store_out = [&](int nb) __attribute__((always_inline)) {
-    const int col = w.col_start + cw * kWC + nb * 32 + l32;  // recomputed: not kept live through the loop
-    uint16_t* dst = out + (static_cast<int64_t>(q0 + col / G) * hq + w.kvh * G + col % G) * D;
+          for (int mdr = 0; mdr < MDR; ++mdr)
 #pragma unroll
-    for (int md = 0; md < DM; ++md)
+            for (int r4 = 0; r4 < 4; ++r4) {
+              f32x4_t v;
 #pragma unroll
-      for (int r4 = 0; r4 < 4; ++r4) {
-        f32x4_t v;
+              for (int j = 0; j < 4; ++j) v[j] = o[round * MDR + mdr][4 * r4 + j];
+              xo[(mdr * 4 + r4) * 64 + lane] = v;
+            }
+          if (round == 0) {
+            xm[lane] = m_run;
+            xm[64 + lane] = l_run;
+          }
+        }
+        lds_barrier();
+        if (kh == 0) {
+          if (round == 0) {
+            const float mb = xm[lane], lb = xm[64 + lane];
+            const float m = fmaxf(m_run, mb);
+            a = m_run == -INFINITY ? 0.f : fast_exp2(m_run - m);
+            b = mb == -INFINITY ? 0.f : fast_exp2(mb - m);
+            l_run = a * l_run + b * lb;
+            m_run = m;
+          }
 #pragma unroll
-        for (int j = 0; j < 4; ++j) v[j] = o[md][nb][4 * r4 + j];
-        *reinterpret_cast<bf16x4_t*>(dst + md * 32 + 8 * r4 + 4 * hg) = __builtin_convertvector(v, bf16x4_t);
+          for (int mdr = 0; mdr < MDR; ++mdr)
+#pragma unroll
+            for (int r4 = 0; r4 < 4; ++r4) {
+              const f32x4_t v = xo[(mdr * 4 + r4) * 64 + lane];
+#pragma unroll
+              for (int j = 0; j < 4; ++j)
+                o[round * MDR + mdr][4 * r4 + j] = a * o[round * MDR + mdr][4 * r4 + j] + b * v[j];
+            }
+        }
+        if (round == 0) lds_barrier();
       }
-  };
-  if (w.slot < 0) {
-    if (active)
+    }
+    // Half 1 may run ahead into the next item: its first issue writes stage e + 3 (= e - 2),
+    // whose last reads (m, l) came before the barrier that ended round 1.
+
+    // ---- epilogue (half 0): O^T register r of block md holds dim 32 md + 8 (r / 4) + 4 hg + r % 4
+    // (the row sum pairs lanes l and l ^ 32, so every lane of the wave takes part)
+    const float lt_sum = sum_halves(l_run);
+    const float inv = lt_sum > 0.f ? 1.f / lt_sum : 0.f;
+    const float lse = lt_sum > 0.f ? m_run + __log2f(lt_sum) : -INFINITY;
+    if (kh == 0 && cval) {
+      if (it.slot < 0) {
+        uint16_t* dst = out + (static_cast<int64_t>(it.q0 + col / G) * hq + it.kvh * G + col % G) * D;
 #pragma unroll
-      for (int nb = 0; nb < kNB; ++nb)
-        if (cval[nb]) store_out(nb);
-    return;
-  }
-  if (w.slot >= ws_slots || !active) return;
+        for (int md = 0; md < DM; ++md)
 #pragma unroll
-  for (int nb = 0; nb < kNB; ++nb) {
-    if (!cval[nb]) continue;
-    const int local = cw * kWC + nb * 32 + l32;
-    float* po = ws_o + (static_cast<int64_t>(w.slot) * kCols + local) * D;
+          for (int r4 = 0; r4 < 4; ++r4) {
+            f32x4_t v;
 #pragma unroll
-    for (int md = 0; md < DM; ++md)
+            for (int j = 0; j < 4; ++j) v[j] = o[md][4 * r4 + j] * inv;
+            *reinterpret_cast<bf16x4_t*>(dst + md * 32 + 8 * r4 + 4 * hg) = __builtin_convertvector(v, bf16x4_t);
+          }
+      } else if (it.slot < ws_slots) {
+        const int local = cw * 32 + l32;
+        float* po = ws_o + (static_cast<int64_t>(it.slot) * kCols + local) * D;
 #pragma unroll
-      for (int r4 = 0; r4 < 4; ++r4) {
-        f32x4_t v;
+        for (int md = 0; md < DM; ++md)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) v[j] = o[md][nb][4 * r4 + j];
-        *reinterpret_cast<f32x4_t*>(po + md * 32 + 8 * r4 + 4 * hg) = v;
+          for (int r4 = 0; r4 < 4; ++r4) {
+            f32x4_t v;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) v[j] = o[md][4 * r4 + j] * inv;
+            *reinterpret_cast<f32x4_t*>(po + md * 32 + 8 * r4 + 4 * hg) = v;
+          }
+        if (hg == 0) ws_lse[static_cast<int64_t>(it.slot) * kCols + local] = lse;
       }
-    if (hg == 0) ws_lse[static_cast<int64_t>(w.slot) * kCols + local] = lse[nb];
+    }
   }
 }
 
@@ -660,7 +671,7 @@ __global__ __launch_bounds__(512, 1) void prefill_attn_pp_kernel(
   const int kv_hi = min(w.kv_end, wg_max_pos + 1);
   const int ntiles = kv_hi > kv_lo ? (kv_hi - kv_lo + kBK - 1) / kBK : 0;
 
-  // ---- direct global -> LDS tile loads (as in prefill_attn_kernel) -----------------------
+  // ---- direct global -> LDS tile loads (as in prefill_attn_list_kernel) ------------------
   int k_off[NLD], v_off[NLD], blk_of[NLD];
 #pragma unroll
   for (int i = 0; i < NLD; ++i) {
@@ -715,13 +726,6 @@ __global__ __launch_bounds__(512, 1) void prefill_attn_pp_kernel(
       const int b = b_lo + ((tile * kBK) >> 4) + blk_of[i];
       ph[i] = b < nblk ? bt[b] : 0;
     }
-    issue(tile, ph);
-  };
-  auto load_tile = [&](int tile) {
-    int32_t ph[NLD];
-#pragma unroll
-    for (int i = 0; i < NLD; ++i) ph[i] = __builtin_amdgcn_readlane(next_v, i);
-    fetch_next(tile + 1);
     issue(tile, ph);
   };
 
@@ -1111,16 +1115,6 @@ constexpr int kWideNB = 1;  // 32-column MFMA blocks per wave on wide tiles
 constexpr int kWideWaves = arckv::kWideCols / (32 * kWideNB);
 static_assert(kWideWaves * 32 * kWideNB == arckv::kWideCols, "wide tile width");
 
-template <int D, int G, int NW, int NB, int KH>
-void launch_attn(dim3 grid, hipStream_t st, const uint16_t* kp, const uint16_t* vp,
-                 const uint16_t* q, uint16_t* out, const int32_t* bt, int bt_stride,
-                 const int32_t* cu_q, const int32_t* seq_lens, int n_reqs, const Work* work,
-                 int64_t n_q, int64_t num_blocks, int hq, int hkv, float scale_log2, float* ws_o,
-                 float* ws_lse, int64_t ws_slots) {
-  hipLaunchKernelGGL((prefill_attn_kernel<D, G, NW, NB, KH>), grid, dim3(64 * NW), 0, st, kp, vp, q, out,
-                     bt, bt_stride, cu_q, seq_lens, n_reqs, work, n_q, num_blocks, hq, hkv,
-                     scale_log2, ws_o, ws_lse, ws_slots);
-}
 
 }  // namespace
 
@@ -1144,6 +1138,9 @@ int32_t prefill_attention(const void* k_pool, const void* v_pool, const void* q,
     return arckv::fail(ARCKV_EUNSUPPORTED, "prefill_attention: group size %d not in {1,2,4,5,8}", G);
   if (tile_cols != arckv::kWideCols && tile_cols != arckv::kNarrowCols)
     return arckv::fail(ARCKV_EINVAL, "prefill_attention: tile_cols %d is not a planned width", tile_cols);
+  if (tile_cols == arckv::kNarrowCols && n_work % arckv::kListItems != 0)
+    return arckv::fail(ARCKV_EINVAL, "prefill_attention: a narrow plan has lists of %d items; n_work %lld",
+                       arckv::kListItems, (long long)n_work);
   if (n_work == 0 && n_combine == 0) {  // nothing to run; the events still mark the stream
     for (hipEvent_t ev : {ev_begin, ev_mid, ev_end})
       if (ev != nullptr && hipEventRecord(ev, static_cast<hipStream_t>(stream)) != hipSuccess)
@@ -1175,6 +1172,7 @@ int32_t prefill_attention(const void* k_pool, const void* v_pool, const void* q,
   if (!record(ev_begin)) return arckv::fail(ARCKV_EDEVICE, "prefill_attention: event record failed");
   if (n_work > 0) {
     const dim3 grid(static_cast<unsigned>(n_work));
+    const dim3 list_grid(static_cast<unsigned>(n_work / arckv::kListItems));
 #define ARCKV_LAUNCH(DD, GG)                                                                   \
   do {                                                                                         \
     if (tile_cols == arckv::kWideCols)                                                         \
@@ -1182,9 +1180,9 @@ int32_t prefill_attention(const void* k_pool, const void* v_pool, const void* q,
                          block_tables, bt_stride, cu_q, seq_lens, n_reqs, wk, n_q, num_blocks, \
                          num_q_heads, num_kv_heads, scale_log2, ws_o, ws_lse, ws_slots);      \
     else                                                                                       \
-      launch_attn<DD, GG, 8, 1, 2>(grid, st, kp, vp, qp, op, block_tables, bt_stride, cu_q, seq_lens, \
-                             n_reqs, wk, n_q, num_blocks, num_q_heads, num_kv_heads,           \
-                             scale_log2, ws_o, ws_lse, ws_slots);                              \
+      hipLaunchKernelGGL((prefill_attn_list_kernel<DD, GG>), list_grid, dim3(512), 0, st, kp, vp, qp, \
+                         op, block_tables, bt_stride, cu_q, seq_lens, n_reqs, wk, n_q, num_blocks, \
+                         num_q_heads, num_kv_heads, scale_log2, ws_o, ws_lse, ws_slots);      \
   } while (0)
     if (head_dim == 64) {
       switch (G) {

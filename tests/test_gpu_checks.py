@@ -108,3 +108,29 @@ def test_malformed_work_items_are_recorded(checked):
     kind, _ = ak.device_checks()
     assert kind == _lib.CHECK_WORK
     compare(bits(out), oracle_out(b, hq, hkv, d), "the valid items' output")
+
+
+def test_malformed_list_entries_are_skipped_and_recorded(checked):
+    print_case("checked build: narrow list plan with an entry naming no request")
+    reqs, hq, hkv, d = [(300, 290), (500, 480), (2000, 1990)], 8, 2, 128    # <= 80 columns: lists
+    b = build_batch(reqs, hq, hkv, d, seed=83)
+    ap = ak.attention_plan(b["cu"], b["seq"], hq, hkv, d)
+    assert ap.tile_cols == 128
+    work = ap.work.copy()
+    lists = work[: ap.n_work].reshape(-1, 8, 8)
+    n_live = (lists[:, :, 0] >= 0).sum(axis=1)
+    k = int(np.argmax(n_live < 8))
+    assert n_live[k] < 8
+    lst = lists[k]
+    lst[1: n_live[k] + 1] = lst[: n_live[k]].copy()          # the bogus entry goes first:
+    lst[0] = [7, 0, 0, 0, 64, -1, 0, 0]                       # the list's items follow it
+    out = torch.empty_like(b["q"])
+    ws = torch.zeros(max(ap.ws_bytes, 1), dtype=torch.uint8, device=DEV)
+    ak.prefill_attention(b["kp"], b["vp"], b["q"], out, torch.from_numpy(b["bt"]).to(DEV),
+                         torch.from_numpy(b["cu"]).to(DEV), torch.from_numpy(b["seq"]).to(DEV),
+                         torch.from_numpy(np.ascontiguousarray(work)).to(DEV), ap.n_work, ap.n_combine,
+                         ap.tile_cols, d ** -0.5, ws, ap.ws_bytes)
+    torch.cuda.synchronize()
+    kind, _ = ak.device_checks()
+    assert kind == _lib.CHECK_WORK
+    compare(bits(out), oracle_out(b, hq, hkv, d), "the list's valid items")

@@ -262,6 +262,9 @@ def test_error_statuses_match_the_oracle():
         assert e2.value.code == "EINVAL"
 
 
+ITEM_COST = 4   # the list planner's cost of one item, in key tiles (kItemCost)
+
+
 def attention_plan_coverage(cu_q, seq_lens, hq, hkv, d, num_cus):
     ap = ak.attention_plan(cu_q, seq_lens, hq, hkv, d, num_cus)
     g = hq // hkv
@@ -270,6 +273,12 @@ def attention_plan_coverage(cu_q, seq_lens, hq, hkv, d, num_cus):
     assert tc == (128 if max_cols <= 128 else 256)
     items = ap.work[: ap.n_work]
     comb = ap.work[ap.n_work: ap.n_work + ap.n_combine]
+    lists = tc == 128               # narrow plans: one list of 8 entries per work-group
+    if lists:
+        assert ap.n_work % 8 == 0
+        for lst in items.reshape(-1, 8, 8):
+            live = lst[:, 0] >= 0
+            assert live[0] and not (live[1:] & ~live[:-1]).any()    # live items, then padding
     cover, n_live, n_slots, max_piece = {}, 0, 0, 0
     for it in items:
         req, kvh, cs, a, b, slot = (int(x) for x in it[:6])
@@ -280,7 +289,7 @@ def attention_plan_coverage(cu_q, seq_lens, hq, hkv, d, num_cus):
         assert a % 64 == 0 and b > a
         max_piece = max(max_piece, (b - a + 63) // 64)
         cover.setdefault((req, kvh, cs), []).append((a, b, slot))
-    n_tiles, total_tiles = 0, 0
+    n_tiles, total_tiles, min_pieces = 0, 0, 0
     for r in range(len(seq_lens)):
         S = cu_q[r + 1] - cu_q[r]
         P = seq_lens[r] - S
@@ -289,6 +298,7 @@ def attention_plan_coverage(cu_q, seq_lens, hq, hkv, d, num_cus):
             kv_end = P + last // g + 1
             n_tiles += hkv
             total_tiles += hkv * (-(-kv_end // 64))
+            min_pieces += hkv * max(1, -(-(-(-kv_end // 64)) // 1024))
             for h in range(hkv):
                 ranges = sorted(cover.pop((r, h, cs)))
                 assert ranges[0][0] == 0 and ranges[-1][1] == kv_end
@@ -298,14 +308,30 @@ def attention_plan_coverage(cu_q, seq_lens, hq, hkv, d, num_cus):
                 else:
                     slots = [x[2] for x in ranges]
                     assert slots == list(range(slots[0], slots[0] + len(slots)))
-                    # pieces of whole key tiles, as equal as whole tiles allow
                     sizes = [(x[1] - x[0] + 63) // 64 for x in ranges]
-                    assert max(sizes) - min(sizes) <= 1
+                    if lists:   # cuts leave no piece under 4 key tiles
+                        assert min(sizes) >= 4
+                    else:       # pieces of whole key tiles, as equal as whole tiles allow
+                        assert max(sizes) - min(sizes) <= 1
                     assert any(list(c[:5]) == [r, h, cs, slots[0], len(slots)] for c in comb)
     assert not cover
     base = n_tiles
     share = max(8, -(-total_tiles // num_cus))
-    if base < num_cus:
+    if lists:
+        # at most one list per CU unless the 8-entry lists force more; equal cost per list
+        # (key tiles + ITEM_COST per item) up to what a budget cut can leave unused
+        n_lists = ap.n_work // 8
+        n_target = max(num_cus, -(-min_pieces // 8))
+        assert n_lists <= n_target
+        costs, full = [], False
+        for lst in items.reshape(-1, 8, 8):
+            live = lst[lst[:, 0] >= 0]
+            full |= len(live) == 8
+            costs.append(int(((live[:, 4] - live[:, 3] + 63) // 64).sum()) + ITEM_COST * len(live))
+        # a list closes with at most 2 * 4 - 1 key tiles + one item's cost unused
+        fair = -(-(total_tiles + ITEM_COST * min_pieces) // n_target)
+        assert full or max(costs) <= max(fair + 8 + ITEM_COST, max_piece + ITEM_COST)
+    elif base < num_cus:
         assert n_live <= num_cus          # split into one round: at most one item per CU
     else:
         assert max_piece <= max(share, 1)  # several rounds: no piece beyond one CU's share
@@ -322,7 +348,7 @@ def test_attention_plan_covers_every_tile_once():
     ap = attention_plan_coverage(np.cumsum([0] + [128] * 8).tolist(), [8320] * 8, 32, 8, 128, 256)
     assert ap.n_combine == 128 and ap.ws_bytes > 0         # short suffixes: split key ranges
     ap = attention_plan_coverage([0, 16], [32784], 32, 8, 128, 256)
-    assert ap.n_combine == 8 and ap.n_work <= 256           # one round of pieces
+    assert ap.n_combine == 8 and ap.n_work // 8 <= 256      # one list per CU at most
     ap = attention_plan_coverage([0, 2048, 4096, 6144, 8192], [34816] * 4, 64, 8, 128, 256)
     assert ap.n_combine == 0                                # plenty of tiles: no split
     rng = np.random.default_rng(3)
@@ -333,6 +359,28 @@ def test_attention_plan_covers_every_tile_once():
     # G = 5 (40 / 8 heads): tiles of 256 columns end inside a token's group of heads
     attention_plan_coverage(np.concatenate([[0], np.cumsum(S)]).tolist(), L.tolist(), 40, 8, 128, 256)
     attention_plan_coverage([0, 51, 103], [4000, 103], 40, 8, 128, 256)
+
+
+def test_list_plans_cover_and_balance():
+    """Narrow batches (at most 128 columns per request): per-work-group lists of 8 entries,
+    about equal cost per list, no cut piece under 4 key tiles."""
+    rng = np.random.default_rng(11)
+    hist = np.clip(np.exp(rng.normal(7.5, 0.8, 256)), 256, 16384).astype(np.int64) // 16 * 16
+    for S, n, hq, hkv, cus in ((32, 16, 32, 8, 256), (1, 64, 32, 8, 256), (16, 16, 32, 8, 256),
+                               (1, 64, 32, 8, 100000), (25, 9, 40, 8, 256), (1, 3, 8, 1, 4),
+                               (64, 5, 16, 8, 256), (128, 2, 8, 8, 256)):
+        L = (hist[:n] + S).tolist()
+        cu = (np.arange(n + 1) * S).tolist()
+        ap = attention_plan_coverage(cu, L, hq, hkv, 128, cus)
+        assert ap.tile_cols == 128
+    # many tiny requests: the 8-entry lists, not the CU count, bound the lists
+    n = 700
+    ap = attention_plan_coverage(list(range(n + 1)), [40] * n, 32, 8, 128, 256)
+    assert ap.n_work // 8 == -(-n * 8 // 8) and ap.n_combine == 0
+    # a history longer than one item's key cap (65536 keys) is cut even when nothing else is
+    ap = attention_plan_coverage([0, 1], [200000], 8, 1, 128, 4)
+    w = ap.work[: ap.n_work]
+    assert (w[w[:, 0] >= 0, 4] - w[w[:, 0] >= 0, 3] <= 65536).all()
 
 
 def test_attention_plan_caps_the_keys_of_one_item():
@@ -372,6 +420,7 @@ def test_attention_plan_order_is_xcd_phased_and_longest_first(seed):
     hkv = [8, 2, 8, 1][seed]
     hq = hkv * [4, 8, 4, 5][seed]
     ap = ak.attention_plan(np.concatenate([[0], np.cumsum(S)]), L, hq, hkv, 128, 256)
+    assert ap.tile_cols == 256          # (narrow batches use per-work-group lists instead)
     items = ap.work[: ap.n_work]
     assert ap.n_work == 0 or items[-1][0] >= 0
     groups = {(int(it[0]), int(it[1])) for it in items if it[0] >= 0}
