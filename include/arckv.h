@@ -289,7 +289,7 @@ int32_t arckv_cache_save(const arckv_cache* cache, void* buf, int64_t cap, int64
 int32_t arckv_cache_restore(const void* buf, int64_t n, arckv_cache** out);
 
 /* ---------------------------------------------------------------------------------------
- * Device: KV scatter (Sec. 3: the engine processes a miss by regenerating the block).
+ * Device: KV scatter (Sec. 3: a missed block's K/V is recomputed and stored again).
  * ------------------------------------------------------------------------------------- */
 
 /* Bytes of one pool (K or V) in layout V1. */

@@ -1,10 +1,10 @@
 // KV scatter: write the K/V rows of the computed (uncached) tokens into their pool slots.
 //
-// The serving engine processes a miss by regenerating the block's KV (paper, Sec. 3); the
-// tokens of a batch that prefill computes are written into the physical blocks the planner
-// chose.  Pool layout version 1: K [blocks][kv_heads][16][D] (token-major), V
-// [blocks][kv_heads][D][16] (dim-major, so that the attention kernel's P.V contraction reads
-// 8 consecutive tokens of one dimension as one 16-byte operand).
+// A cache miss costs a recomputation: prefill produces the block's K/V again (paper, Sec. 3),
+// and the rows of the tokens it computed go into the physical blocks the planner chose.
+// Pool layout version 1: K [blocks][kv_heads][16][D] (token-major), V [blocks][kv_heads][D][16]
+// (dim-major, so that the attention kernel's P.V contraction reads 8 consecutive tokens of one
+// dimension as one 16-byte operand).
 //
 // A work-group handles 64 tokens of one KV head and DPW of its head dimensions: 16 for small
 // batches, so that a decode step still spreads over many work-groups; the whole head
