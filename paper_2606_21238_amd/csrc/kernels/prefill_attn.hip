@@ -1022,6 +1022,8 @@ __global__ __launch_bounds__(kCombineThreads) void attn_combine_kernel(
   const int q0 = cu_q[w.req];
   const int ncols = (cu_q[w.req + 1] - q0) * G;
   const int c0 = blockIdx.y * kCombineCols;  // first local column of this block
+  if (w.col_start + c0 >= ncols) return;     // (uniform) no column of the request here: decode
+                                             // tiles fill 4 to 8 of their 128 columns
   constexpr int D4 = D / 4;
   constexpr int PER = kCombineCols * D4 / kCombineThreads;  // float4 slices per thread
   static_assert(PER * kCombineThreads == kCombineCols * D4, "combine split");
