@@ -378,6 +378,24 @@ def test_decode_full_batch():
         compare(got, ref, f"decode step {k}")
 
 
+def test_list_plan_with_full_lists_over_several_rounds():
+    """Narrow batch of 600 one-token requests over short histories: the list plan packs 8 items
+    into every list and needs more lists than CUs (several rounds of persistent work-groups);
+    one history longer than an item's key cap is split into pieces.  Every row checked."""
+    hq, hkv, d = 16, 4, 128
+    rng = np.random.default_rng(91)
+    L = rng.integers(2, 300, 600)
+    L[17] = 70000                                   # beyond one item's 65536-key cap
+    reqs = [(int(x), int(x) - 1) for x in L]
+    print_case(f"list plan: {len(reqs)} one-token requests, hq={hq} hkv={hkv} d={d}")
+    b = build_batch(reqs, hq, hkv, d, seed=92)
+    got, ap = run_attention(b, hq, hkv, d, 256)
+    lists = ap.work[: ap.n_work].reshape(-1, 8, 8)
+    assert ap.tile_cols == 128 and len(lists) > 256
+    assert ((lists[:, :, 0] >= 0).sum(axis=1) == 8).sum() > 100 and ap.n_combine >= 1
+    compare(got, oracle_out(b, hq, hkv, d), "full lists")
+
+
 def test_longctx_sampled_rows():
     cfg = get_config("longctx")
     print_case("config longctx (4 x (32768 cached + 2048)), row-sampled")
