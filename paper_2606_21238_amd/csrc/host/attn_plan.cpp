@@ -143,7 +143,10 @@ extern "C" int32_t arckv_attention_plan(const int32_t* cu_q, const int32_t* seq_
     int64_t n_lists = 0;
     if (base > 0) {
       int64_t lo = std::max<int64_t>(kItemCost + kMinPiece, (cost + n_lists_max - 1) / n_lists_max);
-      int64_t hi = std::max<int64_t>(lo, cost + kItemCost);
+      // a list closes with less than 2 kMinPiece + kItemCost unused, so a budget that much above
+      // the even share usually fits; the whole range is searched only when it does not
+      int64_t hi = lo + 2 * kMinPiece + kItemCost;
+      if (pack(hi, false) > n_lists_max) hi = std::max<int64_t>(hi, cost + kItemCost);
       while (lo < hi) {  // smallest budget that needs at most n_lists_max lists
         const int64_t mid = lo + (hi - lo) / 2;
         if (pack(mid, false) <= n_lists_max) hi = mid; else lo = mid + 1;
