@@ -60,6 +60,7 @@ typedef __attribute__((address_space(3))) void lds_void;
 constexpr int kStages = 4;                         // K/V tiles resident in LDS (ring)
 constexpr int kBK = 64;        // keys per K/V tile (4 blocks of 16)
 constexpr float kLazy = 8.0f;  // rescale O only when a column max grows by > 2^8
+constexpr float kLazySum = 256.0f;  // 2^kLazy
 
 struct Work {
   int32_t req, kvh, col_start, kv_start, kv_end, slot, pad0, pad1;
@@ -759,35 +760,48 @@ __global__ __launch_bounds__(512, 1) void prefill_attn_pp_kernel(
           sacc[mb][r] = key > pos ? -INFINITY : sacc[mb][r];
         }
     }
-    float m = -INFINITY;
+    // Exponentials against the running maximum first.  Every term p = 2^(s c - m) is >= 0,
+    // so a lane whose sum stays <= 2^kLazy has every term <= 2^kLazy, which is all the lazy
+    // rescale has to guarantee.  Only when some lane's sum exceeds that (or on the item's
+    // first tile, before any maximum is known) are the column maxima taken, O and l rescaled
+    // and the exponentials computed again.
+    auto exps = [&](float mu) {
+      float sum = 0.f;
 #pragma unroll
-    for (int mb = 0; mb < 2; ++mb)
+      for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) m = fmaxf(m, sacc[mb][r]);
-    const float mx = max_halves(m) * scale_log2;
-    const bool pending = __builtin_amdgcn_ballot_w64(mx > m_run + kLazy) != 0;   // wave-uniform
+        for (int half = 0; half < 2; ++half)
+#pragma unroll
+          for (int jj = 0; jj < 4; ++jj) {
+            const f32x2_t two = {fast_exp2(fmaf(sacc[mb][8 * half + 2 * jj], scale_log2, -mu)),
+                                 fast_exp2(fmaf(sacc[mb][8 * half + 2 * jj + 1], scale_log2, -mu))};
+            sum += two[0];
+            sum += two[1];
+            pw[2 * mb + half][jj] = __builtin_bit_cast(uint32_t, __builtin_convertvector(two, bf16x2_t));
+          }
+      return sum;
+    };
+    float lsum = 0.f;
+    bool pending = true;
+    if (j > 0) {                                                   // wave-uniform
+      lsum = exps(m_run == -INFINITY ? 0.f : m_run);
+      pending = __builtin_amdgcn_ballot_w64(!(lsum <= kLazySum)) != 0;   // also catches inf / NaN sums
+    }
     if (pending) {
+      float m = -INFINITY;
+#pragma unroll
+      for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) m = fmaxf(m, sacc[mb][r]);
+      const float mx = max_halves(m) * scale_log2;
       const float m_new = fmaxf(m_run, mx);
       const float alpha = m_new == -INFINITY ? 1.f : fast_exp2(m_run - m_new);
       m_run = m_new;
       l_run *= alpha;
 #pragma unroll
       for (int md = 0; md < DM; ++md) o[md] *= alpha;
+      lsum = exps(m_run == -INFINITY ? 0.f : m_run);
     }
-    const float mu = m_run == -INFINITY ? 0.f : m_run;
-    float lsum = 0.f;
-#pragma unroll
-    for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-      for (int half = 0; half < 2; ++half)
-#pragma unroll
-        for (int jj = 0; jj < 4; ++jj) {
-          const f32x2_t two = {fast_exp2(fmaf(sacc[mb][8 * half + 2 * jj], scale_log2, -mu)),
-                               fast_exp2(fmaf(sacc[mb][8 * half + 2 * jj + 1], scale_log2, -mu))};
-          lsum += two[0];
-          lsum += two[1];
-          pw[2 * mb + half][jj] = __builtin_bit_cast(uint32_t, __builtin_convertvector(two, bf16x2_t));
-        }
     l_run += lsum;
   };
   // keys >= L of the last tile may hold stale bytes (even NaN patterns): zero their V in LDS

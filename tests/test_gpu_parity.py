@@ -96,9 +96,11 @@ def test_scatter_block_runs_bit_exact(d, hkv, n, start):
 # attention on directly built batches (random placement, edge lengths)
 # ------------------------------------------------------------------------------------------
 
-def build_batch(reqs, hq, hkv, d, seed, extra_blocks=5):
+def build_batch(reqs, hq, hkv, d, seed, extra_blocks=5, k_gain=None, v_gain=1.0):
     """reqs: [(L, P)].  Random placement of every request's blocks in one pool; all L tokens'
-    K/V written by the library scatter; returns device tensors and oracle-side copies."""
+    K/V written by the library scatter; returns device tensors and oracle-side copies.
+    k_gain: optional function of a token's position in its prompt (numpy array in, array out)
+    scaling its K row, so that scores grow, fall or jump along the keys; v_gain scales V."""
     rng = np.random.default_rng(seed)
     nb = [(L + 15) // 16 for L, _ in reqs]
     nphys = sum(nb) + extra_blocks
@@ -116,6 +118,12 @@ def build_batch(reqs, hq, hkv, d, seed, extra_blocks=5):
     cu = np.concatenate([[0], np.cumsum(Ss)]).astype(np.int32)
     k_all = randn_bf16((sum(Ls), hkv, d), seed + 1)
     v_all = randn_bf16((sum(Ls), hkv, d), seed + 2)
+    if k_gain is not None:
+        pos = np.concatenate([np.arange(L) for L in Ls]).astype(np.float64)
+        gain = torch.from_numpy(np.asarray(k_gain(pos), dtype=np.float32)).to(DEV)
+        k_all = (k_all.float() * gain[:, None, None]).to(torch.bfloat16)
+    if v_gain != 1.0:
+        v_all = (v_all.float() * v_gain).to(torch.bfloat16)
     q_all = randn_bf16((sum(Ss), hq, d), seed + 3)
     slots = np.concatenate([tables[r][np.arange(L) // 16] * 16 + np.arange(L) % 16
                             for r, L in enumerate(Ls)]).astype(np.int32)
@@ -188,6 +196,33 @@ def test_attention_sweep(case, num_cus):
     compare(got, ref, f"case {case}")
     if num_cus > 1000 and max(L for L, _ in reqs) > 512:   # splits are >= 512 keys
         assert (ap.work[: ap.n_work, 5] >= 0).any()
+
+
+# Scores that grow, jump or spike along the keys, so that the running maximum moves after the
+# first key tile of an item (the online softmax's rescale), and scores that fall (it never
+# does).  With N(0, 1) inputs a 128-dim score has a standard deviation of about 1.4 in log2
+# units, so gains of 4-30 move the maxima by tens to hundreds; V is scaled down to keep the
+# (nearly one-hot) outputs small next to the tolerance.
+RESCALE = [
+    ("linear growth", lambda t: 1.0 + t / 128.0),
+    ("steps every 512 keys", lambda t: 1.0 + 4.0 * np.floor(t / 512.0)),
+    ("spikes on every 97th key", lambda t: np.where(t % 97 == 13, 8.0, 1.0)),
+    ("moderate rises (sums past 2^8 without one large term)", lambda t: 1.0 + 0.35 * (np.floor(t / 64.0) % 12)),
+    ("falling", lambda t: 30.0 / (1.0 + t / 64.0)),
+]
+
+
+@pytest.mark.parametrize("num_cus", [256, 100000])
+@pytest.mark.parametrize("case", range(len(RESCALE)))
+def test_attention_moving_maxima(case, num_cus):
+    name, gain = RESCALE[case]
+    for reqs, hq, hkv, d in (([(3000, 2000), (700, 0)], 32, 8, 128),               # wide tiles
+                             ([(L, L - 1) for L in (5000, 2049, 300)], 32, 8, 128),  # lists (decode)
+                             ([(1500, 1000)], 8, 2, 64)):
+        print_case(f"moving maxima '{name}' {reqs} hq={hq} hkv={hkv} d={d} num_cus={num_cus}")
+        b = build_batch(reqs, hq, hkv, d, seed=1300 + 7 * case, k_gain=gain, v_gain=0.25)
+        got, _ = run_attention(b, hq, hkv, d, num_cus)
+        compare(got, oracle_out(b, hq, hkv, d), f"{name}, {reqs}")
 
 
 def test_attention_beyond_the_item_key_cap():
