@@ -19,20 +19,25 @@
 //  * Transposed formulation: S^T = K . Q^T and O^T = V^T . P^T with v_mfma_f32_32x32x16_bf16.
 //    Query columns sit on lanes, keys / head dims on the M (register) dimension, so a lane
 //    owns whole columns: row max and row sum are in-lane plus one exchange with lane +- 32.
-//    Each wave owns kWaveCols columns (32-column MFMA N blocks); with 32 columns a wave fits
-//    in 256 registers and two work-groups share a CU, so each SIMD interleaves two waves'
-//    MFMA and softmax work.
+//    Each wave owns 32 columns (one MFMA N block); with 32 columns a wave fits in 256
+//    registers, so a SIMD holds two waves of the work-group and interleaves one wave's MFMAs
+//    with the other's softmax.
 //  * K rows are fed to the MFMA in an order that swaps bits 2 and 3 of the row index; the
 //    accumulator layout of S^T then puts 8 consecutive keys per lane half, which is exactly
 //    the B-operand layout of the P.V step, so P^T goes from registers to the next MFMA with
 //    no shuffle, and V^T (dim-major blocks) is read as one 16-byte operand per lane.
 //  * K/V tiles of 64 keys (4 blocks) are gathered from the scattered physical blocks with
-//    16-byte direct global-to-LDS loads into a ring of XOR-swizzled LDS tiles; two or three
+//    16-byte direct global-to-LDS loads (the block's base in SGPRs, a 32-bit offset per lane)
+//    into a ring of XOR-swizzled LDS tiles; two or three
 //    tiles are in flight while the current one is multiplied.  The query tile comes through
 //    the same direct loads (narrow tiles: as an element of the ring), so the first wait covers
 //    the queries and tile 0 only.
 //  * fp32 online softmax in base 2 (scale * log2 e folded into one FMA per score), causal
-//    masking only on tiles that cross the diagonal, bf16 P with fp32 accumulation.
+//    masking only on tiles that cross the diagonal, bf16 P with fp32 accumulation.  The
+//    running maximum is lazy: O and l are rescaled only when a score exceeds it by more than
+//    2^kLazy.  The wide kernel finds that from the exponentials' lane sums (non-negative
+//    terms: a sum within the bound keeps every term within it) and takes column maxima only
+//    on an item's first tile or when a sum exceeds the bound.
 //  * Long key ranges with too few query tiles are split by the host plan (wide tiles: into
 //    one round of work-groups; narrow tiles: where a list's budget ends); split items write
 //    fp32 partials plus a base-2 log-sum-exp that attn_combine merges.
@@ -256,6 +261,8 @@ __global__ __launch_bounds__(512, 1) void prefill_attn_list_kernel(
     v_off[i] = d * 16 + h * 8;
   }
   const int64_t blk_stride = static_cast<int64_t>(hkv) * 16 * D;  // elements per physical block
+  // block entries outside [0, num_blocks) (negative ones too, as unsigned) read block 0
+  const uint32_t nb32 = static_cast<uint32_t>(num_blocks < INT32_MAX ? num_blocks : INT32_MAX);
   // The load cursor: item `ld`, next element `lt` (-1: its Q tile, else K/V tile lt), and the
   // physical blocks of its next K/V tile.  Those are read at the end of the element before
   // (prefetch_ph, right before its wait), so the scalar loads' latency hides under that wait.
@@ -297,7 +304,7 @@ __global__ __launch_bounds__(512, 1) void prefill_attn_list_kernel(
     for (int i = 0; i < NLD; ++i) {
       ARCKV_CHECK_WAVE(ph[i] < 0 || ph[i] >= num_blocks, ARCKV_CHECK_BLOCK);
       // wave-uniform (the wave's 1 KiB lies in one block); an entry out of range reads block 0
-      const int32_t pb = __builtin_amdgcn_readfirstlane((ph[i] < 0 || ph[i] >= num_blocks) ? 0 : ph[i]);
+      const int32_t pb = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(ph[i]) >= nb32 ? 0 : ph[i]);
       const int64_t base = static_cast<int64_t>(pb) * blk_stride + head_k;
       load_lds16_s(k_pool + base, static_cast<uint32_t>(k_off[i]) * 2u, (lds_void*)(st + i * LDB + wave * 1024));
       load_lds16_s(v_pool + base, static_cast<uint32_t>(v_off[i]) * 2u, (lds_void*)(st + TILE + i * LDB + wave * 1024));
@@ -380,7 +387,7 @@ __global__ __launch_bounds__(512, 1) void prefill_attn_list_kernel(
   uint32_t pw[2][4];
   auto exp_phase = [&](const f32x16_t& s) {
     const float mu = m_run == -INFINITY ? 0.f : m_run;
-    float lsum = 0.f;
+    float lsum = -0.f;                   // -0 + x == x for every x: the first add folds away
 #pragma unroll
     for (int half = 0; half < 2; ++half)
 #pragma unroll
@@ -694,6 +701,7 @@ __global__ __launch_bounds__(512, 1) void prefill_attn_pp_kernel(
   }
   const int64_t head_k = static_cast<int64_t>(w.kvh) * 16 * D;
   const int64_t blk_stride = static_cast<int64_t>(hkv) * 16 * D;
+  const uint32_t nb32 = static_cast<uint32_t>(num_blocks < INT32_MAX ? num_blocks : INT32_MAX);
   // The item's block-table entries (blocks b_lo .. b_lo + n_tbl - 1) are copied to LDS once:
   // the loop then looks them up there.  Scalar loads of the table inside the loop would force
   // a wait for the scalar memory round trip at every tile (and, while one is in flight, full
@@ -723,7 +731,7 @@ __global__ __launch_bounds__(512, 1) void prefill_attn_pp_kernel(
     for (int i = 0; i < NLD; ++i) {
       ARCKV_CHECK_WAVE(ph[i] < 0 || ph[i] >= num_blocks, ARCKV_CHECK_BLOCK);
       // wave-uniform (the wave's 1 KiB lies in one block); an entry out of range reads block 0
-      const int32_t pb = __builtin_amdgcn_readfirstlane((ph[i] < 0 || ph[i] >= num_blocks) ? 0 : ph[i]);
+      const int32_t pb = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(ph[i]) >= nb32 ? 0 : ph[i]);
       const int64_t base = static_cast<int64_t>(pb) * blk_stride + head_k;
       load_lds16_s(k_pool + base, static_cast<uint32_t>(k_off[i]) * 2u, (lds_void*)(st + i * LDB + wave * 1024));
       load_lds16_s(v_pool + base, static_cast<uint32_t>(v_off[i]) * 2u, (lds_void*)(st + TILE + i * LDB + wave * 1024));
@@ -766,7 +774,7 @@ __global__ __launch_bounds__(512, 1) void prefill_attn_pp_kernel(
     // first tile, before any maximum is known) are the column maxima taken, O and l rescaled
     // and the exponentials computed again.
     auto exps = [&](float mu) {
-      float sum = 0.f;
+      float sum = -0.f;                  // -0 + x == x for every x: the first add folds away
 #pragma unroll
       for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
@@ -849,7 +857,7 @@ __global__ __launch_bounds__(512, 1) void prefill_attn_pp_kernel(
       for (int i = 0; i < NLD; ++i) {
         const int32_t ph = __builtin_amdgcn_readlane(next_v, i);
         ARCKV_CHECK_WAVE(ph < 0 || ph >= num_blocks, ARCKV_CHECK_BLOCK);
-        const int32_t pb = (ph < 0 || ph >= num_blocks) ? 0 : ph;  // never used unmasked
+        const int32_t pb = static_cast<uint32_t>(ph) >= nb32 ? 0 : ph;  // never used unmasked
         const int64_t base = static_cast<int64_t>(pb) * blk_stride + head_k;
         ld_src[2 * i] = k_pool + base;
         ld_ofs[2 * i] = static_cast<uint32_t>(k_off[i]) * 2u;
