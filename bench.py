@@ -338,6 +338,9 @@ def main():
     ap.add_argument("--policy", default="arc", choices=["arc", "lru", "dbl"])
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle CPU time")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--separate-scatter", action="store_true",
+                    help="docqa14b: project to K/V rows and scatter them in a second launch "
+                         "(default: the projection writes K/V into the pool itself)")
     ap.add_argument("--policy-sample", type=int, default=1200,
                     help="requests of the trace stream the Python planners run on (0: no policy baseline)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
@@ -463,11 +466,14 @@ def main():
         h1 = h2 = time.perf_counter()
         if ev is not None:
             ev[0].record()
-        if layer:
+        if layer and not args.separate_scatter:
+            eng.project_to_pool(db, x, w_qkv, q, theta)          # K/V straight into the pool
+        elif layer:
             eng.project(db, x, w_qkv, q, kn, vn, theta)
         if ev is not None:
             ev[1].record()
-        eng.scatter(db, kn, vn)
+        if not layer or args.separate_scatter:
+            eng.scatter(db, kn, vn)
         eng.attention(db, q, out, events=None if ev is None else ev[2:])
         h3 = time.perf_counter()
         eng.release()
@@ -588,8 +594,10 @@ def main():
 
     if layer:
         result["layer"] = {
-            "what": "per step: Q/K/V projection (fused bf16 MFMA GEMM + rotary epilogue), KV scatter, "
-                    "attention, combine; value counts projection + attention flops",
+            "what": ("per step: Q/K/V projection (fused bf16 MFMA GEMM + rotary epilogue"
+                     + (") then KV scatter" if args.separate_scatter else ", K/V written into the pool by it")
+                     + ", attention, combine; value counts projection + attention flops"),
+            "scatter_fused_into_projection": not args.separate_scatter,
             "projection_tflops": round(float(np.sum(proj_f)) / float(np.sum(t_proj)) / 1e12, 2),
             "projection_frac_of_bf16_peak": round(float(np.sum(proj_f)) / float(np.sum(t_proj)) / 1e12
                                                   / PEAK_BF16_TFLOPS, 4),

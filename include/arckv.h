@@ -456,6 +456,24 @@ int32_t arckv_qkv_rope(const void* x, const void* w_qkv, int64_t n_tokens, int32
                        double rope_theta, void* workspace, int64_t ws_bytes, void* q_out,
                        void* k_out, void* v_out, void* stream);
 
+/* The same producer with the KV scatter fused into it: Q as arckv_qkv_rope writes it, and K
+ * and V of token t written straight into the paged pools at slot_mapping[t] (layout V1, as
+ * arckv_kv_scatter writes them: pool[slot] <- the token's rotated K row and its V row), so
+ * the scatter launch and the [n_tokens][num_kv_heads][head_dim] K/V rows disappear (Sec. 3:
+ * the K/V of blocks that missed the cache are computed again and stored in the pool).
+ * k_pool, v_pool: device, num_blocks blocks,
+ * 16-byte aligned.  slot_mapping: device int32 [n_tokens]; a slot outside
+ * [0, 16 num_blocks) is skipped.  The bytes written equal arckv_qkv_rope followed by
+ * arckv_kv_scatter on the same slots (two tokens with the same slot: one of them wins).
+ * Other arguments, requirements and errors as arckv_qkv_rope; EINVAL also for num_blocks
+ * outside [1, 2^27] or a NULL slot_mapping. */
+int32_t arckv_qkv_rope_to_pool(const void* x, const void* w_qkv, int64_t n_tokens, int32_t hidden,
+                               int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                               const int32_t* cu_q, const int32_t* seq_lens, int32_t n_reqs,
+                               double rope_theta, void* workspace, int64_t ws_bytes, void* q_out,
+                               void* k_pool, void* v_pool, int64_t num_blocks,
+                               const int32_t* slot_mapping, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -393,6 +393,31 @@ def qkv_rope(x, w_qkv, cu_q, seq_lens, num_q_heads: int, num_kv_heads: int, rope
         C.c_void_p(_stream(stream))), "arckv_qkv_rope")
 
 
+def qkv_rope_to_pool(x, w_qkv, cu_q, seq_lens, num_q_heads: int, num_kv_heads: int, rope_theta: float,
+                     q_out, k_pool, v_pool, slot_mapping, workspace, stream=None):
+    """qkv_rope with the KV scatter fused in (arckv_qkv_rope_to_pool): Q into q_out [T, Hq, D],
+    K and V into the paged pools (layout V1, k_pool [N][Hkv][16][D], v_pool [N][Hkv][D][16]) at
+    slot_mapping [T] int32."""
+    t, h = int(x.shape[0]), int(x.shape[1])
+    d = int(q_out.shape[2])
+    n_out = (num_q_heads + 2 * num_kv_heads) * d
+    if tuple(w_qkv.shape) != (n_out, h):
+        raise ValueError(f"w_qkv must be [{n_out}, {h}]")
+    if tuple(q_out.shape) != (t, num_q_heads, d):
+        raise ValueError("q_out shape does not match x and the head counts")
+    nb = int(k_pool.shape[0])
+    if tuple(k_pool.shape) != (nb, num_kv_heads, 16, d) or tuple(v_pool.shape) != (nb, num_kv_heads, d, 16):
+        raise ValueError("k_pool / v_pool must be layout V1 with matching heads and head_dim")
+    if slot_mapping.numel() != t or cu_q.numel() != seq_lens.numel() + 1:
+        raise ValueError("slot_mapping must have one slot per token, cu_q len(seq_lens) + 1 entries")
+    _lib.check(lib().arckv_qkv_rope_to_pool(
+        _dev(x, 16, "x"), _dev(w_qkv, 16, "w_qkv"), t, h, num_q_heads, num_kv_heads, d,
+        _dev(cu_q, 32, "cu_q"), _dev(seq_lens, 32, "seq_lens"), int(seq_lens.numel()), float(rope_theta),
+        _dev(workspace, None, "workspace"), int(workspace.numel() * workspace.element_size()),
+        _dev(q_out, 16, "q_out"), _dev(k_pool, 16, "k_pool"), _dev(v_pool, 16, "v_pool"), nb,
+        _dev(slot_mapping, 32, "slot_mapping"), C.c_void_p(_stream(stream))), "arckv_qkv_rope_to_pool")
+
+
 @dataclass
 class AttnPlan:
     work: np.ndarray     # int32 [n_work + n_combine, 8]

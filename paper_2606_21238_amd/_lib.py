@@ -78,6 +78,8 @@ _SIGS = {
     "arckv_pool_bytes": (i64, [i64, i32, i32]),
     "arckv_kv_scatter": (i32, [vp, vp, vp, vp, vp, i64, i64, i32, i32, vp]),
     "arckv_qkv_rope": (i32, [vp, vp, i64, i32, i32, i32, i32, vp, vp, i32, f64, vp, i64, vp, vp, vp, vp]),
+    "arckv_qkv_rope_to_pool": (i32, [vp, vp, i64, i32, i32, i32, i32, vp, vp, i32, f64, vp, i64, vp, vp, vp,
+                                      i64, vp, vp]),
     "arckv_attention_plan": (i32, [P_i32, P_i32, i32, i32, i32, i32, i32, P_i32, i64, P_i64, P_i64,
                                    P_i64, P_i32]),
     "arckv_prepare_batch": (i32, [vp, vp, vp, i32, u64, i32, i32, i32, i32, vp, i64, vp, vp,

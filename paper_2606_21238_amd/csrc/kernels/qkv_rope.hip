@@ -29,6 +29,7 @@
 
 #include <algorithm>
 #include <cmath>
+#include <type_traits>
 
 #include "../host/internal.hpp"
 
@@ -100,12 +101,18 @@ __global__ __launch_bounds__(256) void rope_table_kernel(int64_t n_tokens, const
   }
 }
 
-template <int D>
+// POOL: K and V go straight into the paged pools (layout V1; k_out and v_out are then the
+// pools) at slots[t] instead of into [token][head][dim] rows: K rows as 16-byte chunks, V (dim-major blocks) as 8 consecutive tokens of one dim per
+// 16-byte store where the 8 tokens hold 8 aligned consecutive slots, else one 2-byte store per
+// token.  Slots outside [0, n_slots) are skipped, as the scatter does.
+template <int D, bool POOL>
 __global__ __launch_bounds__(kThreads, 1) void qkv_gemm_rope_kernel(
     const uint16_t* __restrict__ x, const uint16_t* __restrict__ w, int n_tokens, int hidden,
     int n_out, int hq, int hkv, const float2* __restrict__ tab, uint16_t* __restrict__ q_out,
-    uint16_t* __restrict__ k_out, uint16_t* __restrict__ v_out) {
+    uint16_t* __restrict__ k_out, uint16_t* __restrict__ v_out, const int32_t* __restrict__ slots,
+    int64_t n_slots) {
   __shared__ __attribute__((aligned(1024))) char smem[kTM * (kTN * 2 + 16)];   // ring, then the y tile
+  __shared__ int32_t tslot[POOL ? kTM : 1];                                      // the tile's slots
   // Tile order.  Work-groups are dealt to the 8 XCDs in turn (b -> XCD b % 8) and each XCD has
   // its own L2, so logical tile L = (b % 8) * (G / 8) + b / 8 gives every XCD a contiguous run
   // of tiles; runs go over groups of kGroupM token tiles output-tile by output-tile, so the
@@ -215,6 +222,8 @@ __global__ __launch_bounds__(kThreads, 1) void qkv_gemm_rope_kernel(
   asm volatile("s_barrier" ::: "memory");
   constexpr int kPitch = kTN * 2 + 16;
   char* ep = smem;
+  if constexpr (POOL)   // read once here (published by the barrier below), not per chunk
+    if (tid < kTM) tslot[tid] = t0 + tid < n_tokens ? slots[t0 + tid] : -1;
 #pragma unroll
   for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
@@ -233,6 +242,7 @@ __global__ __launch_bounds__(kThreads, 1) void qkv_gemm_rope_kernel(
     const int row = qc / (kTN / 8), o = (qc % (kTN / 8)) * 8;
     const int t = t0 + row, n = n0 + o;
     if (t >= n_tokens || n >= n_out) continue;
+    if (POOL && n >= nrot) continue;               // V: the pass below
     const int head = n / D, i0 = n % D;
     const u32x4_t own = *reinterpret_cast<const u32x4_t*>(ep + row * kPitch + o * 2);
     u32x4_t res = own;
@@ -252,45 +262,98 @@ __global__ __launch_bounds__(kThreads, 1) void qkv_gemm_rope_kernel(
       }
     }
     uint16_t* dst;
-    if (head < hq) dst = q_out + (static_cast<int64_t>(t) * hq + head) * D + i0;
-    else if (head < hq + hkv) dst = k_out + (static_cast<int64_t>(t) * hkv + head - hq) * D + i0;
-    else dst = v_out + (static_cast<int64_t>(t) * hkv + head - hq - hkv) * D + i0;
+    if (head < hq) {
+      dst = q_out + (static_cast<int64_t>(t) * hq + head) * D + i0;
+    } else if (head < hq + hkv) {
+      if constexpr (POOL) {
+        const int32_t sl = tslot[row];
+        if (sl < 0 || sl >= n_slots) continue;
+        dst = k_out + ((static_cast<int64_t>(sl >> 4) * hkv + head - hq) * 16 + (sl & 15)) * D + i0;
+      } else {
+        dst = k_out + (static_cast<int64_t>(t) * hkv + head - hq) * D + i0;
+      }
+    } else {
+      dst = v_out + (static_cast<int64_t>(t) * hkv + head - hq - hkv) * D + i0;
+    }
     *reinterpret_cast<u32x4_t*>(dst) = res;
+  }
+  if constexpr (POOL) {
+    // V columns of the tile into the dim-major pool: item p is 8 tokens (rows 8 g .. 8 g + 7)
+    // of one output column; consecutive threads take consecutive columns of the same tokens.
+    if (n0 + kTN > nrot) {                                        // uniform
+#pragma unroll 2
+      for (int it = 0; it < (kTM / 8) * kTN / kThreads; ++it) {
+        const int p = it * kThreads + tid;
+        const int g = p / kTN, oc = p % kTN;
+        const int n = n0 + oc, tf = t0 + 8 * g;
+        if (n < nrot || n >= n_out || tf >= n_tokens) continue;
+        const int vh = (n - nrot) / D, dim = (n - nrot) % D;
+        int32_t sl[8];
+        uint16_t val[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          sl[j] = tslot[8 * g + j];                               // -1 past the last token
+          val[j] = *reinterpret_cast<const uint16_t*>(ep + (8 * g + j) * kPitch + oc * 2);
+        }
+        bool run = (sl[0] & 7) == 0 && sl[0] >= 0 && sl[0] + 7 < n_slots;
+#pragma unroll
+        for (int j = 1; j < 8; ++j) run = run && sl[j] == sl[0] + j;
+        if (run) {     // 8 aligned consecutive slots: one block, one 16-byte row segment
+          u32x4_t v;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) v[j] = static_cast<uint32_t>(val[2 * j]) | (static_cast<uint32_t>(val[2 * j + 1]) << 16);
+          *reinterpret_cast<u32x4_t*>(v_out + ((static_cast<int64_t>(sl[0] >> 4) * hkv + vh) * D + dim) * 16 +
+                                      (sl[0] & 15)) = v;
+        } else {
+#pragma unroll
+          for (int j = 0; j < 8; ++j)
+            if (sl[j] >= 0 && sl[j] < n_slots)
+              v_out[((static_cast<int64_t>(sl[j] >> 4) * hkv + vh) * D + dim) * 16 + (sl[j] & 15)] = val[j];
+        }
+      }
+    }
   }
 }
 
 }  // namespace
 
-extern "C" int32_t arckv_qkv_rope(const void* x, const void* w_qkv, int64_t n_tokens, int32_t hidden,
-                                  int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
-                                  const int32_t* cu_q, const int32_t* seq_lens, int32_t n_reqs,
-                                  double rope_theta, void* workspace, int64_t ws_bytes, void* q_out,
-                                  void* k_out, void* v_out, void* stream) {
+namespace {
+
+// Shared by arckv_qkv_rope and arckv_qkv_rope_to_pool: pool == true writes K and V into the
+// pools k_dst / v_dst (num_blocks blocks) at slots.
+int32_t qkv_rope_launch(const char* fn, const void* x, const void* w_qkv, int64_t n_tokens, int32_t hidden,
+                        int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim, const int32_t* cu_q,
+                        const int32_t* seq_lens, int32_t n_reqs, double rope_theta, void* workspace,
+                        int64_t ws_bytes, void* q_out, void* k_dst, void* v_dst, bool pool, int64_t num_blocks,
+                        const int32_t* slots, void* stream) {
   if (n_tokens < 0 || hidden < 1 || num_q_heads < 1 || num_kv_heads < 1 || n_reqs < 0 ||
       num_q_heads % num_kv_heads != 0 || !(rope_theta > 1.0) || !std::isfinite(rope_theta))
-    return arckv::fail(ARCKV_EINVAL, "qkv_rope: bad sizes or theta");
+    return arckv::fail(ARCKV_EINVAL, "%s: bad sizes or theta", fn);
   if (head_dim != 64 && head_dim != 128)
-    return arckv::fail(ARCKV_EUNSUPPORTED, "qkv_rope: head_dim %d not in {64,128}", head_dim);
+    return arckv::fail(ARCKV_EUNSUPPORTED, "%s: head_dim %d not in {64,128}", fn, head_dim);
   const int64_t n_out = static_cast<int64_t>(num_q_heads + 2 * num_kv_heads) * head_dim;
   if (hidden % kKB != 0 || hidden > (1 << 22) || n_out % 128 != 0)   // (32-bit load offsets in a tile)
     return arckv::fail(ARCKV_EUNSUPPORTED,
-                       "qkv_rope: hidden %d must be a multiple of %d (at most 2^22) and the %lld outputs of 128",
-                       hidden, kKB, (long long)n_out);
+                       "%s: hidden %d must be a multiple of %d (at most 2^22) and the %lld outputs of 128",
+                       fn, hidden, kKB, (long long)n_out);
+  if (pool && (num_blocks < 1 || num_blocks > (int64_t{1} << 27)))
+    return arckv::fail(ARCKV_EINVAL, "%s: num_blocks %lld", fn, (long long)num_blocks);
   if (n_tokens == 0) return ARCKV_OK;
   if (n_tokens > INT32_MAX - kTM || n_out > INT32_MAX || n_reqs < 1 ||
       static_cast<int64_t>(hidden) * n_tokens > (int64_t{1} << 40))
-    return arckv::fail(ARCKV_EINVAL, "qkv_rope: %lld tokens, %lld outputs, %d requests",
+    return arckv::fail(ARCKV_EINVAL, "%s: %lld tokens, %lld outputs, %d requests", fn,
                        (long long)n_tokens, (long long)n_out, n_reqs);
   if (x == nullptr || w_qkv == nullptr || cu_q == nullptr || seq_lens == nullptr ||
-      workspace == nullptr || q_out == nullptr || k_out == nullptr || v_out == nullptr)
-    return arckv::fail(ARCKV_EINVAL, "qkv_rope: NULL pointer");
+      workspace == nullptr || q_out == nullptr || k_dst == nullptr || v_dst == nullptr ||
+      (pool && slots == nullptr))
+    return arckv::fail(ARCKV_EINVAL, "%s: NULL pointer", fn);
   for (const void* p : {x, w_qkv, static_cast<const void*>(workspace), static_cast<const void*>(q_out),
-                        static_cast<const void*>(k_out), static_cast<const void*>(v_out)})
+                        static_cast<const void*>(k_dst), static_cast<const void*>(v_dst)})
     if (reinterpret_cast<uintptr_t>(p) % 16 != 0)
-      return arckv::fail(ARCKV_EINVAL, "qkv_rope: x, w_qkv, workspace and outputs must be 16-byte aligned");
+      return arckv::fail(ARCKV_EINVAL, "%s: x, w_qkv, workspace and outputs must be 16-byte aligned", fn);
   const int64_t tab_bytes = n_tokens * (head_dim / 2) * static_cast<int64_t>(sizeof(float2));
   if (ws_bytes < tab_bytes)
-    return arckv::fail(ARCKV_ENOSPC, "qkv_rope: workspace %lld bytes < %lld", (long long)ws_bytes,
+    return arckv::fail(ARCKV_ENOSPC, "%s: workspace %lld bytes < %lld", fn, (long long)ws_bytes,
                        (long long)tab_bytes);
   auto* s = static_cast<hipStream_t>(stream);
   auto* tab = static_cast<float2*>(workspace);
@@ -300,19 +363,48 @@ extern "C" int32_t arckv_qkv_rope(const void* x, const void* w_qkv, int64_t n_to
   auto* xp = static_cast<const uint16_t*>(x);
   auto* wp = static_cast<const uint16_t*>(w_qkv);
   auto* q = static_cast<uint16_t*>(q_out);
-  auto* k = static_cast<uint16_t*>(k_out);
-  auto* v = static_cast<uint16_t*>(v_out);
+  auto* k = static_cast<uint16_t*>(k_dst);
+  auto* v = static_cast<uint16_t*>(v_dst);
   const int T = static_cast<int>(n_tokens), N = static_cast<int>(n_out);
+  const int64_t n_slots = pool ? num_blocks * 16 : 0;
+  auto go = [&](auto d_tag, auto pool_tag) {
+    constexpr int D = decltype(d_tag)::value;
+    constexpr bool P = decltype(pool_tag)::value;
+    hipLaunchKernelGGL(rope_table_kernel<D>, tgrid, dim3(256), 0, s, n_tokens, cu_q, seq_lens, n_reqs, rope_theta, tab);
+    hipLaunchKernelGGL((qkv_gemm_rope_kernel<D, P>), grid, dim3(kThreads), 0, s, xp, wp, T, hidden, N,
+                       num_q_heads, num_kv_heads, tab, q, k, v, slots, n_slots);
+  };
+  using D64 = std::integral_constant<int, 64>;
+  using D128 = std::integral_constant<int, 128>;
   if (head_dim == 64) {
-    hipLaunchKernelGGL(rope_table_kernel<64>, tgrid, dim3(256), 0, s, n_tokens, cu_q, seq_lens, n_reqs, rope_theta, tab);
-    hipLaunchKernelGGL(qkv_gemm_rope_kernel<64>, grid, dim3(kThreads), 0, s, xp, wp, T, hidden, N, num_q_heads,
-                       num_kv_heads, tab, q, k, v);
+    if (pool) go(D64{}, std::true_type{}); else go(D64{}, std::false_type{});
   } else {
-    hipLaunchKernelGGL(rope_table_kernel<128>, tgrid, dim3(256), 0, s, n_tokens, cu_q, seq_lens, n_reqs, rope_theta, tab);
-    hipLaunchKernelGGL(qkv_gemm_rope_kernel<128>, grid, dim3(kThreads), 0, s, xp, wp, T, hidden, N, num_q_heads,
-                       num_kv_heads, tab, q, k, v);
+    if (pool) go(D128{}, std::true_type{}); else go(D128{}, std::false_type{});
   }
   const hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return arckv::fail(ARCKV_EDEVICE, "qkv_rope: %s", hipGetErrorString(e));
+  if (e != hipSuccess) return arckv::fail(ARCKV_EDEVICE, "%s: %s", fn, hipGetErrorString(e));
   return ARCKV_OK;
+}
+
+}  // namespace
+
+extern "C" int32_t arckv_qkv_rope(const void* x, const void* w_qkv, int64_t n_tokens, int32_t hidden,
+                                  int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                                  const int32_t* cu_q, const int32_t* seq_lens, int32_t n_reqs,
+                                  double rope_theta, void* workspace, int64_t ws_bytes, void* q_out,
+                                  void* k_out, void* v_out, void* stream) {
+  return qkv_rope_launch("qkv_rope", x, w_qkv, n_tokens, hidden, num_q_heads, num_kv_heads, head_dim, cu_q,
+                         seq_lens, n_reqs, rope_theta, workspace, ws_bytes, q_out, k_out, v_out, false, 0,
+                         nullptr, stream);
+}
+
+extern "C" int32_t arckv_qkv_rope_to_pool(const void* x, const void* w_qkv, int64_t n_tokens, int32_t hidden,
+                                          int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                                          const int32_t* cu_q, const int32_t* seq_lens, int32_t n_reqs,
+                                          double rope_theta, void* workspace, int64_t ws_bytes, void* q_out,
+                                          void* k_pool, void* v_pool, int64_t num_blocks,
+                                          const int32_t* slot_mapping, void* stream) {
+  return qkv_rope_launch("qkv_rope_to_pool", x, w_qkv, n_tokens, hidden, num_q_heads, num_kv_heads, head_dim,
+                         cu_q, seq_lens, n_reqs, rope_theta, workspace, ws_bytes, q_out, k_pool, v_pool, true,
+                         num_blocks, slot_mapping, stream);
 }

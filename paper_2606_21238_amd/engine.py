@@ -220,6 +220,27 @@ class PrefillEngine:
                                         q.data_ptr(), k_new.data_ptr(), v_new.data_ptr(), self._stream(stream)),
                    "arckv_qkv_rope")
 
+    def project_to_pool(self, db: DeviceBatch, x, w_qkv, q, rope_theta: float, stream=None):
+        """project() with the KV scatter fused in (arckv_qkv_rope_to_pool): Q into q, the batch's
+        K and V straight into the engine's pools at the plan's slots; no scatter() follows."""
+        import torch
+        t, h = db.n_tokens, int(x.shape[1])
+        n_out = (self.hq + 2 * self.hkv) * self.d
+        if tuple(x.shape) != (t, h) or tuple(w_qkv.shape) != (n_out, h) or x.element_size() != 2 or \
+                not (x.is_contiguous() and w_qkv.is_contiguous()):
+            raise ValueError(f"x must be contiguous 16-bit [{t}, H] and w_qkv [{n_out}, H]")
+        if tuple(q.shape) != (t, self.hq, self.d) or not q.is_contiguous() or q.element_size() != 2:
+            raise ValueError("q must be contiguous 16-bit [n_tokens, heads, D]")
+        need = 4 * t * self.d
+        if self._y is None or self._y.numel() < need:
+            with torch.cuda.stream(self._torch_stream(stream)):
+                self._y = torch.empty(max(need, 1), dtype=torch.uint8, device=self.device)
+        _lib.check(lib().arckv_qkv_rope_to_pool(
+            x.data_ptr(), w_qkv.data_ptr(), t, h, self.hq, self.hkv, self.d, db.cu_q.data_ptr(),
+            db.seq_lens.data_ptr(), db.plan.n_reqs, float(rope_theta), self._y.data_ptr(), self._y.numel(),
+            q.data_ptr(), self.k_pool.data_ptr(), self.v_pool.data_ptr(), self.num_phys,
+            db.slot_mapping.data_ptr(), self._stream(stream)), "arckv_qkv_rope_to_pool")
+
     def attention(self, db: DeviceBatch, q, out, stream=None, events=None):
         """Prefill attention of the batch.  `events`: optional (begin, mid, end) torch.cuda.Event
         triple (already recorded once, so that each has its HIP handle), recorded by the library

@@ -132,3 +132,69 @@ def test_layer_path_projection_scatter_attention():
     okv.scatter(okp, ovp, kb, vb, slots)
     ref = oatt.prefill_attention(qb[P:], okp, ovp, [table], cu, sl, d ** -0.5)
     compare(bits(out), ref, "layer path")
+
+
+def slot_pattern(kind, reqs, nblk, rng):
+    """Slots of the computed tokens: 'prefill' places each request's positions P..L-1 through a
+    random block table (8-token runs wherever a request's positions are 8-aligned), 'random'
+    is a permutation of the pool's slots (no runs), 'skips' is 'prefill' with some slots -1 or
+    past the pool."""
+    if kind == "random":
+        T = sum(L - P for L, P in reqs)
+        return rng.permutation(nblk * 16)[:T].astype(np.int32)
+    perm = rng.permutation(nblk)
+    out, o = [], 0
+    for L, P in reqs:
+        n = (L + 15) // 16
+        table = perm[o:o + n]
+        o += n
+        pos = np.arange(P, L)
+        out.append(table[pos // 16] * 16 + pos % 16)
+    s = np.concatenate(out).astype(np.int32)
+    if kind == "skips":
+        idx = rng.choice(len(s), max(1, len(s) // 20), replace=False)
+        s[idx[::2]] = -1
+        s[idx[1::2]] = nblk * 16 + 5
+    return s
+
+
+@pytest.mark.parametrize("kind", ["prefill", "random", "skips"])
+@pytest.mark.parametrize("reqs,hidden,hq,hkv,d", [
+    ([(2100, 2048), (300, 0), (17, 5), (40, 33)], 512, 40, 8, 128),   # Qwen3-14B heads
+    ([(700, 100), (129, 1)], 256, 6, 1, 64),       # one output tile holds Q, K and V columns
+    ([(520, 0), (9, 0)], 128, 5, 1, 128),          # Q and K share a tile, V a half tile
+])
+def test_qkv_rope_to_pool_equals_projection_then_scatter(kind, reqs, hidden, hq, hkv, d):
+    """arckv_qkv_rope_to_pool against arckv_qkv_rope followed by arckv_kv_scatter (itself
+    checked against the oracle above and in the scatter tests): Q and both whole pools,
+    including the untouched sentinel bytes, bit for bit."""
+    print_case(f"qkv_rope_to_pool {kind} {reqs} hidden={hidden} hq={hq} hkv={hkv} d={d}")
+    rng = np.random.default_rng(hidden + d + len(kind))
+    S = [L - P for L, P in reqs]
+    T = sum(S)
+    nblk = sum((L + 15) // 16 for L, _ in reqs) + 6
+    cu = torch.from_numpy(np.concatenate([[0], np.cumsum(S)]).astype(np.int32)).to(DEV)
+    sl = torch.from_numpy(np.array([L for L, _ in reqs], dtype=np.int32)).to(DEV)
+    slots = torch.from_numpy(slot_pattern(kind, reqs, nblk, rng)).to(DEV)
+    x = randn_bf16((T, hidden), 21 + hidden)
+    w = randn_bf16(((hq + 2 * hkv) * d, hidden), 22 + hidden, hidden ** -0.5)
+    ws = torch.empty(4 * T * d, dtype=torch.uint8, device=DEV)
+
+    q_a = torch.empty((T, hq, d), dtype=torch.bfloat16, device=DEV)
+    k_a = torch.empty((T, hkv, d), dtype=torch.bfloat16, device=DEV)
+    v_a = torch.empty((T, hkv, d), dtype=torch.bfloat16, device=DEV)
+    kp_a = torch.full((nblk, hkv, 16, d), -1, dtype=torch.int16, device=DEV)
+    vp_a = torch.full((nblk, hkv, d, 16), -1, dtype=torch.int16, device=DEV)
+    ak.qkv_rope(x, w, cu, sl, hq, hkv, THETA, q_a, k_a, v_a, ws)
+    ak.kv_scatter(kp_a, vp_a, k_a, v_a, slots)
+
+    q_b = torch.full((T, hq, d), float("nan"), dtype=torch.bfloat16, device=DEV)
+    kp_b = torch.full((nblk, hkv, 16, d), -1, dtype=torch.int16, device=DEV)
+    vp_b = torch.full((nblk, hkv, d, 16), -1, dtype=torch.int16, device=DEV)
+    ak.qkv_rope_to_pool(x, w, cu, sl, hq, hkv, THETA, q_b, kp_b, vp_b, slots, ws)
+    torch.cuda.synchronize()
+    assert np.array_equal(bits(q_a), bits(q_b)), "Q differs"
+    assert np.array_equal(bits(kp_a), bits(kp_b)), "K pool differs"
+    assert np.array_equal(bits(vp_a), bits(vp_b)), "V pool differs"
+    written = int((bits(kp_b) != 0xFFFF).any(axis=(1, 3)).sum())
+    assert written > 0
