@@ -595,7 +595,7 @@ def main():
     if layer:
         result["layer"] = {
             "what": ("per step: Q/K/V projection (fused bf16 MFMA GEMM + rotary epilogue"
-                     + (") then KV scatter" if args.separate_scatter else ", K/V written into the pool by it")
+                     + (") then KV scatter" if args.separate_scatter else ", K/V written into the pool by it)")
                      + ", attention, combine; value counts projection + attention flops"),
             "scatter_fused_into_projection": not args.separate_scatter,
             "projection_tflops": round(float(np.sum(proj_f)) / float(np.sum(t_proj)) / 1e12, 2),
