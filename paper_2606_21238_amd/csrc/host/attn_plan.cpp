@@ -44,6 +44,7 @@ constexpr int kKeyTile = 64;  // keys per K/V tile (split boundaries are multipl
 constexpr int kXcds = 8;      // MI355X: 8 XCDs; dispatch round-robins work-groups over them
 constexpr int64_t kItemCost = 4;  // list plans: cost of one item beyond its key tiles (measured)
 constexpr int64_t kMinPiece = 4;  // list plans: shortest piece a cut may leave, in key tiles
+constexpr int64_t kXcdSkewPermille = 25;  // list plans: budget shifted from odd to even XCDs (measured)
 
 struct Item {
   int32_t v[ARCKV_WORK_INTS];
@@ -111,17 +112,22 @@ extern "C" int32_t arckv_attention_plan(const int32_t* cu_q, const int32_t* seq_
     }
     const int64_t n_lists_max = std::max<int64_t>(target, (min_pieces + arckv::kListItems - 1) / arckv::kListItems);
     std::vector<Piece> pieces;
-    // Packs the tiles in order into lists of budget B; returns the number of lists.
+    // Packs the tiles in order into lists of budget B; returns the number of lists.  List k
+    // runs on XCD k % 8; the work-groups of odd XCDs measured about 5 % slower per key tile
+    // than those of even ones on every box timed, so even lists get B (1 + kXcdSkew) and odd
+    // ones B (1 - kXcdSkew).
     auto pack = [&](int64_t B, bool keep) -> int64_t {
       if (keep) pieces.clear();
-      int64_t lists = 0, used = B, n_in = arckv::kListItems;
+      const int64_t skew = B * kXcdSkewPermille / 1000;
+      int64_t lists = 0, used = B, n_in = arckv::kListItems, Bk = B;
       for (int32_t ti = 0; ti < static_cast<int32_t>(tiles.size()); ++ti) {
         int64_t rem = key_tiles(tiles[ti]), a = 0;
         while (rem > 0) {
-          if (n_in == arckv::kListItems || B - used - kItemCost < 1) {
+          if (n_in == arckv::kListItems || Bk - used - kItemCost < 1) {
             ++lists; used = 0; n_in = 0;
+            Bk = (lists - 1) % 2 == 0 ? B + skew : B - skew;
           }
-          const int64_t avail = std::min(B - used - kItemCost, kMaxPiece);
+          const int64_t avail = std::min(Bk - used - kItemCost, kMaxPiece);
           int64_t take = rem;
           if (rem > avail) {
             take = avail;
