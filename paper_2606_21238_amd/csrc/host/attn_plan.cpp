@@ -238,8 +238,10 @@ extern "C" int32_t arckv_attention_plan(const int32_t* cu_q, const int32_t* seq_
     slot += ns;
   }
 
-  // XCD-aware order: assign whole groups to XCDs (largest first, to the least-loaded XCD),
-  // then emit position-major so work-group i runs on XCD i % 8; each XCD's list is longest first.
+  // XCD-aware order: assign whole groups to XCDs (largest first, to the XCD that would finish
+  // first: odd XCDs, measured about 5 % slower per key tile, count their work 2.5 % heavier and
+  // even ones 2.5 % lighter), then emit position-major so work-group i runs on XCD i % 8; each
+  // XCD's list is longest first.
   const int64_t n_groups = static_cast<int64_t>(n_reqs) * num_kv_heads;  // group = req * hkv + kvh
   std::vector<int64_t> cost_of(static_cast<size_t>(n_groups), 0);
   std::vector<char> used(static_cast<size_t>(n_groups), 0);
@@ -255,9 +257,12 @@ extern "C" int32_t arckv_attention_plan(const int32_t* cu_q, const int32_t* seq_
   });
   std::vector<int32_t> xcd_of(static_cast<size_t>(n_groups), 0);
   int64_t load[kXcds] = {0};
+  auto finish = [&](int x, int64_t c) {   // relative finishing time with c more work
+    return (load[x] + c) * (x % 2 == 0 ? 1000 - kXcdSkewPermille : 1000 + kXcdSkewPermille);
+  };
   for (const auto& g : groups) {
     int best = 0;
-    for (int x = 1; x < kXcds; ++x) if (load[x] < load[best]) best = x;
+    for (int x = 1; x < kXcds; ++x) if (finish(x, g.second) < finish(best, g.second)) best = x;
     xcd_of[g.first] = best;
     load[best] += g.second;
   }
