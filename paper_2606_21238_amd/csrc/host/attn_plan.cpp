@@ -44,7 +44,7 @@ constexpr int kKeyTile = 64;  // keys per K/V tile (split boundaries are multipl
 constexpr int kXcds = 8;      // MI355X: 8 XCDs; dispatch round-robins work-groups over them
 constexpr int64_t kItemCost = 4;  // list plans: cost of one item beyond its key tiles (measured)
 constexpr int64_t kMinPiece = 4;  // list plans: shortest piece a cut may leave, in key tiles
-constexpr int64_t kXcdSkewPermille = 25;  // list plans: budget shifted from odd to even XCDs (measured)
+constexpr int64_t kXcdSkewPermille = 25;  // work shifted from odd to even XCDs, per mille (measured)
 
 struct Item {
   int32_t v[ARCKV_WORK_INTS];
@@ -114,8 +114,8 @@ extern "C" int32_t arckv_attention_plan(const int32_t* cu_q, const int32_t* seq_
     std::vector<Piece> pieces;
     // Packs the tiles in order into lists of budget B; returns the number of lists.  List k
     // runs on XCD k % 8; the work-groups of odd XCDs measured about 5 % slower per key tile
-    // than those of even ones on every box timed, so even lists get B (1 + kXcdSkew) and odd
-    // ones B (1 - kXcdSkew).
+    // than those of even ones on the boxes timed, so even lists get a budget of
+    // B (1 + kXcdSkewPermille / 1000) and odd ones B (1 - kXcdSkewPermille / 1000).
     auto pack = [&](int64_t B, bool keep) -> int64_t {
       if (keep) pieces.clear();
       const int64_t skew = B * kXcdSkewPermille / 1000;
