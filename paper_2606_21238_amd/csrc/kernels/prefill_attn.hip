@@ -165,8 +165,8 @@ __global__ __launch_bounds__(512, 1) void prefill_attn_list_kernel(
   constexpr int NEL = STAGE / LDB;               // ... per ring element
   constexpr int BLK_BYTES = 16 * D * 2;          // one block of one head, K or V
   static_assert(NLD >= 1 && TILE % LDB == 0, "tile must be a multiple of one WG-wide load");
-  constexpr int MDR = DM / 2;                    // O blocks a half hands over per merge round
-  static_assert(kCW * MDR * 4 * 64 * 16 == STAGE, "one merge round fills one stage");
+  constexpr int MDR = DM / 2;                    // O blocks a half hands over per merge pass
+  static_assert(kCW * MDR * 4 * 64 * 16 == STAGE, "one merge pass fills one stage");
   __shared__ __attribute__((aligned(1024))) char smem[kRing * STAGE];
   if (n_q <= 0) return;
 
@@ -526,15 +526,15 @@ __global__ __launch_bounds__(512, 1) void prefill_attn_list_kernel(
 
     // ---- key halves: half 1 hands (m, l, O) to half 0 ---------------------------------------
     // Consumed elements e - 1 and e - 2 leave their stages free until element e + 3 and e + 4
-    // are issued (at the starts of elements e and e + 1).  Round 1: O blocks [0, MDR) through
-    // stage e - 1, m and l through stage e - 2; round 2: O blocks [MDR, DM) through stage e - 1.
+    // are issued (at the starts of elements e and e + 1).  Pass 0: O blocks [0, MDR) through
+    // stage e - 1, m and l through stage e - 2; pass 1: O blocks [MDR, DM) through stage e - 1.
     // Layout: O as [column wave][block][r / 4][lane] float4; m, l as [column wave][lane].
     {
       f32x4_t* xo = reinterpret_cast<f32x4_t*>(stage(e + kRing - 1)) + cw * (MDR * 4 * 64);
       float* xm = reinterpret_cast<float*>(stage(e + kRing - 2)) + cw * 128;
       float a = 0.f, b = 0.f;
 #pragma unroll
-      for (int round = 0; round < 2; ++round) {
+      for (int pass = 0; pass < 2; ++pass) {
         if (kh == 1) {
 #pragma unroll
           for (int mdr = 0; mdr < MDR; ++mdr)
@@ -542,17 +542,17 @@ __global__ __launch_bounds__(512, 1) void prefill_attn_list_kernel(
             for (int r4 = 0; r4 < 4; ++r4) {
               f32x4_t v;
 #pragma unroll
-              for (int j = 0; j < 4; ++j) v[j] = o[round * MDR + mdr][4 * r4 + j];
+              for (int j = 0; j < 4; ++j) v[j] = o[pass * MDR + mdr][4 * r4 + j];
               xo[(mdr * 4 + r4) * 64 + lane] = v;
             }
-          if (round == 0) {
+          if (pass == 0) {
             xm[lane] = m_run;
             xm[64 + lane] = l_run;
           }
         }
         lds_barrier();
         if (kh == 0) {
-          if (round == 0) {
+          if (pass == 0) {
             const float mb = xm[lane], lb = xm[64 + lane];
             const float m = fmaxf(m_run, mb);
             a = m_run == -INFINITY ? 0.f : fast_exp2(m_run - m);
@@ -567,14 +567,14 @@ __global__ __launch_bounds__(512, 1) void prefill_attn_list_kernel(
               const f32x4_t v = xo[(mdr * 4 + r4) * 64 + lane];
 #pragma unroll
               for (int j = 0; j < 4; ++j)
-                o[round * MDR + mdr][4 * r4 + j] = a * o[round * MDR + mdr][4 * r4 + j] + b * v[j];
+                o[pass * MDR + mdr][4 * r4 + j] = a * o[pass * MDR + mdr][4 * r4 + j] + b * v[j];
             }
         }
-        if (round == 0) lds_barrier();
+        if (pass == 0) lds_barrier();
       }
     }
     // Half 1 may run ahead into the next item: its first issue writes stage e + 3 (= e - 2),
-    // whose last reads (m, l) came before the barrier that ended round 1.
+    // whose last reads (m, l) came before the barrier that ended pass 0.
 
     // ---- epilogue (half 0): O^T register r of block md holds dim 32 md + 8 (r / 4) + 4 hg + r % 4
     // (the row sum pairs lanes l and l ^ 32, so every lane of the wave takes part)
