@@ -82,6 +82,26 @@ def test_qkv_rope_validates_arguments_without_touching_a_device():
                             None) == _lib.ENOSPC
 
 
+def test_qkv_rope_to_pool_validates_arguments_without_touching_a_device():
+    """The producer that writes K/V into the pool shares the producer's checks and adds its own
+    (pool size, slot mapping); every refusal happens before any device work, so the fake
+    addresses below are never read."""
+    L = ak.lib()
+    a, m = 0x10000, 0x10002
+
+    def call(t=4, d=128, nb=8, slots=a, kp=a, ws=1 << 20, theta=1.0e6):
+        return L.arckv_qkv_rope_to_pool(a, a, t, 64, 4, 2, d, a, a, 1, theta, a, ws, a, kp, a, nb, slots, None)
+
+    assert call(d=96) == _lib.EUNSUPPORTED
+    assert call(theta=1.0) == _lib.EINVAL
+    assert call(nb=0) == _lib.EINVAL and b"num_blocks" in L.arckv_last_error()
+    assert call(nb=(1 << 27) + 1) == _lib.EINVAL
+    assert call(slots=None) == _lib.EINVAL and b"NULL" in L.arckv_last_error()
+    assert call(kp=m) == _lib.EINVAL and b"aligned" in L.arckv_last_error()
+    assert call(ws=4 * 4 * 128 - 1) == _lib.ENOSPC
+    assert call(t=0) == _lib.OK                                        # nothing to do
+
+
 def test_device_checks_only_in_the_checked_build():
     """The product build has no device checks (EUNSUPPORTED, no GPU touched); the checked
     debug build exists beside it and exports the same calls."""
